@@ -1,0 +1,268 @@
+/*
+ * speechkv.h - C ABI of the SpeechKV hot path on AMD Instinct MI355X (gfx950).
+ *
+ * SpeechKV (arXiv 2607.06827, "Compress the Cache, Not the Speech Embedding")
+ * shortens the speech part of a speech LLM's KV cache inside the LLM.  From
+ * layer l0 onward a learned linear gate scores every speech key, a softmax over
+ * each non-overlapping window of w consecutive speech positions turns the
+ * scores into weights, and the window's keys and values are replaced by their
+ * weighted sums (Sec. III-B, Eq. 4).  Text positions are left as they are.
+ * Full-resolution queries then attend over the shorter cache (Sec. III-B,
+ * Eq. 5) under a mask that keeps attention causal.  At inference the pooling
+ * runs once, at prefill, and decoding attends over the stored compressed cache
+ * (Sec. III-C).
+ *
+ * Three calls carry the method:
+ *   speechkv_pool_kv       prefill-time pooling into the paged cache (Eq. 4)
+ *   speechkv_decode_attn   one-query-per-sequence attention over the cache (Eq. 5)
+ *   speechkv_prefill_attn  full-resolution queries over the cache (Eq. 5 + mask)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers documented as "device" point into GPU memory of the current HIP
+ *   device; pointers documented as "host" point into CPU memory.  The caller
+ *   owns every buffer.  The library allocates nothing, frees nothing, keeps no
+ *   mutable global state and never synchronises; it is safe to call from
+ *   several host threads.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Work is enqueued asynchronously on it.
+ * - Every argument is validated on the host before anything is enqueued.  A
+ *   call that returns an error has enqueued nothing.  Values that live in
+ *   device memory (span lengths, cache lengths, block-table entries) cannot be
+ *   checked on the host: they are caller obligations listed per call.  The
+ *   kernels clamp every index they derive from them, so a violation gives
+ *   wrong results but no out-of-bounds access.
+ * - Layers are numbered from 0.  Layer `layer` is compressed iff layer >= l0;
+ *   otherwise the effective window is 1 and pooling is the identity.  (The
+ *   paper numbers layers from 1: its l0 = 5, which leaves the first 4 layers
+ *   at full resolution, is l0 = 4 here.)
+ * - Element types: SPEECHKV_DTYPE_F32 (fp32) or SPEECHKV_DTYPE_BF16 (bf16).
+ *   Arithmetic is fp32 in every kernel; results are rounded to nearest-even
+ *   into the element type when stored.
+ * - Supported shapes: head_dim in {64, 128}; num_q_heads = G * num_kv_heads
+ *   with G in {1, 2, 4, 8}; page_size a power of two in [8, 256].
+ */
+#ifndef SPEECHKV_H
+#define SPEECHKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes.  Every call returns SPEECHKV_OK or one negative code. */
+#define SPEECHKV_OK 0
+#define SPEECHKV_ERR_INVALID_ARG (-1) /* null pointer, bad size or count      */
+#define SPEECHKV_ERR_UNSUPPORTED (-2) /* dtype, head_dim, G or page_size      */
+#define SPEECHKV_ERR_WORKSPACE (-3)   /* workspace missing or too small       */
+#define SPEECHKV_ERR_ALIAS (-4)       /* raw K/V overlap the destination pool */
+#define SPEECHKV_ERR_HIP (-5)         /* the HIP runtime refused a launch     */
+
+/* Element types. */
+#define SPEECHKV_DTYPE_F32 0
+#define SPEECHKV_DTYPE_BF16 1
+
+/* Mask modes for speech queries against pooled windows (Sec. III-B: each
+ * query attends only to positions that precede it; the figure that draws the
+ * mask is not part of the text, so two readings are offered).
+ *   WINDOW_END   pooled window i becomes visible at its last frame
+ *                (default: no query ever sees a frame later than itself).
+ *   WINDOW_START pooled window i becomes visible at its first frame. */
+#define SPEECHKV_MASK_WINDOW_END 0
+#define SPEECHKV_MASK_WINDOW_START 1
+
+/*
+ * Paged KV cache of one layer (the per-layer cache of Sec. III-C).
+ *
+ * k_pages, v_pages  device, element type `dtype`, each laid out
+ *                   [num_pages][num_kv_heads][page_size][head_dim]: one
+ *                   (page, kv head) is a contiguous run of page_size rows.
+ * block_table       device int32 [batch][max_pages_per_seq]; entry
+ *                   (b, j) is the page that holds cache slots
+ *                   [j*page_size, (j+1)*page_size) of sequence b.
+ *                   Caller obligation: entries are in [0, num_pages), and no
+ *                   page is shared by two sequences that one call writes.
+ *                   (Entries outside that range are skipped by the kernels.)
+ */
+typedef struct speechkv_paged_kv {
+  void* k_pages;
+  void* v_pages;
+  const int32_t* block_table;
+  int32_t num_pages;
+  int32_t page_size;
+  int32_t max_pages_per_seq;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t dtype;
+} speechkv_paged_kv;
+
+/*
+ * Where the speech sits inside each sequence (Sec. III-A: the LLM input is the
+ * concatenation of speech and text; Sec. III-B: pooling acts on the T speech
+ * positions only).  Sequence b at full resolution is
+ *     [ prefix_len[b] text | speech_len[b] speech frames | suffix_len[b] text ].
+ *
+ * prefix_len, speech_len, suffix_len  device int32 [batch], each >= 0.
+ * max_speech_len  host: an upper bound on every speech_len[b].
+ * max_total_len   host: an upper bound on every prefix+speech+suffix length.
+ * The two host bounds size the launch grids without a device round trip.
+ * Caller obligation: the bounds hold.  (Work beyond them is not done.)
+ */
+typedef struct speechkv_spans {
+  const int32_t* prefix_len;
+  const int32_t* speech_len;
+  const int32_t* suffix_len;
+  int32_t max_speech_len;
+  int32_t max_total_len;
+} speechkv_spans;
+
+/*
+ * speechkv_pool_kv - learned window pooling of the speech keys and values,
+ * written straight into the paged cache (Sec. III-B, Eq. 4; Sec. III-C).
+ *
+ * For every sequence b and KV head g, with P, T, N its span lengths and
+ * w_eff = (layer >= l0) ? w : 1, nW = ceil(T / w_eff):
+ *   cache slot c in [0, P)          <- raw row c                (bitwise copy)
+ *   cache slot P + i, i in [0, nW)  <- sum_j alpha_j * raw row j over the
+ *       window j in [P + i*w_eff, min(P + (i+1)*w_eff, P + T)), where
+ *       alpha = softmax_j(gate_u[g] . K[b, j, g]) over that window.  The same
+ *       alpha weights the keys and the values.  A last window shorter than
+ *       w_eff (T % w_eff != 0) is pooled over the frames it has.
+ *   cache slot P + nW + m, m in [0, N) <- raw row P + T + m      (bitwise copy)
+ * The gate of the paper is affine, g(k) = u . k + bias; the bias adds the same
+ * constant to every logit of a window and cancels in the softmax, so only u
+ * is taken.  With w_eff = 1 every weight is exactly 1 and the cache receives
+ * the raw rows bitwise.
+ *
+ * k_raw, v_raw   device, element type cache->dtype.  Element (b, s, g, e) is
+ *                at index b*stride_b + s*stride_s + g*stride_h + e; e (the
+ *                head_dim axis) is contiguous.  Strides are in elements and
+ *                must keep each row 16-byte aligned.
+ * batch          number of sequences (>= 1).
+ * raw_len        rows per sequence in k_raw/v_raw (>= 1).  Caller
+ *                obligation: prefix+speech+suffix <= raw_len.
+ * spans          host pointer to the span description.
+ * w              window size R of the paper (>= 1).
+ * gate_u         device fp32 [num_kv_heads][head_dim], the gate vector of
+ *                this layer per KV head, or NULL for the zero gate (uniform
+ *                averaging, the paper's initialisation).
+ * layer, l0      layer index and first compressed layer (both >= 0).
+ * cache          host pointer to the destination cache description.  Caller
+ *                obligation: each sequence has pages for P + nW + N slots.
+ * cache_len_out  device int32 [batch] receiving P + nW + N, or NULL.
+ * Errors: INVALID_ARG, UNSUPPORTED, ALIAS (the raw K/V byte range overlaps
+ *         the page pool it would write), HIP.
+ */
+int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
+                     int64_t stride_s, int64_t stride_h, int32_t batch,
+                     int32_t raw_len, const speechkv_spans* spans, int32_t w,
+                     const float* gate_u, int32_t layer, int32_t l0,
+                     const speechkv_paged_kv* cache, int32_t* cache_len_out,
+                     void* stream);
+
+/*
+ * speechkv_decode_attn - one decoding step of attention over the compressed
+ * cache (Sec. III-B, Eq. 5; Sec. III-C: the cache holds the pooled speech, so
+ * every step reads R times fewer speech entries).
+ *
+ * For every sequence b and query head h (KV head g = h / G, G = num_q_heads /
+ * num_kv_heads), with L = cache_len[b]:
+ *   out[b, h] = sum_{c < L} softmax_c(scale * q[b, h] . K[b, c, g]) V[b, c, g]
+ * Every cached slot is visible to the newest token.  If k_new and v_new are
+ * given, the newest token's key and value are first stored in slot L - 1 and
+ * take part in the step.  L = 0 gives out = 0.
+ *
+ * q, out         device, element type cache->dtype, [batch][num_q_heads][head_dim].
+ * cache_len      device int32 [batch].  Caller obligations: 0 <= cache_len[b]
+ *                <= max_cache_len and the sequence has pages for them.
+ * max_cache_len  host bound on cache_len (sizes the split-K grid).
+ * k_new, v_new   device [batch][num_kv_heads][head_dim] of cache->dtype, or
+ *                both NULL.
+ * scale          logit scale, 1/sqrt(head_dim) in the paper.
+ * num_splits     number of key ranges each (sequence, KV head) is split into
+ *                (split-K); 0 selects speechkv_decode_num_splits().  With more
+ *                than one split the partial results are merged by a
+ *                log-sum-exp reduction in a fixed order, so results are
+ *                deterministic for a given num_splits.
+ * workspace      device scratch of at least
+ *                speechkv_decode_workspace_bytes(...) bytes (16-byte
+ *                aligned); may be NULL when that size is 0.  Its contents on
+ *                entry do not matter.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.
+ */
+int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
+                         const speechkv_paged_kv* cache,
+                         const int32_t* cache_len, int32_t max_cache_len,
+                         const void* k_new, const void* v_new, float scale,
+                         int32_t num_splits, void* out, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/*
+ * speechkv_prefill_attn - full-resolution queries over the compressed cache,
+ * causal over the compressed sequence (Sec. III-B, Eq. 5 and the mask that
+ * follows it; Sec. III-C: the same computation is applied on the fly during
+ * training).
+ *
+ * Query row p of sequence b is full-resolution position p, p in [0, P+T+N).
+ * Key c of the compressed sequence (length P + nW + N, as written by
+ * speechkv_pool_kv) becomes visible at position tau(c):
+ *   prefix key c < P             tau = c
+ *   pooled key P + i             tau = last frame of window i  (WINDOW_END)
+ *                                tau = first frame of window i (WINDOW_START)
+ *   suffix key P + nW + m        tau = P + T + m
+ * and row p attends to the keys with tau(c) <= p.  tau is increasing in c, so
+ * each row sees a prefix of the cache.  A row that sees no key (for example a
+ * speech row before the first window closes when P = 0) gets out = 0 and
+ * lse = -inf.  With w_eff = 1 this is ordinary causal attention.
+ *
+ * q, out         device, element type cache->dtype,
+ *                [batch][q_len][num_q_heads][head_dim], dense.  Rows
+ *                p >= P+T+N of a sequence are neither read nor written.
+ * q_len          rows allocated per sequence (>= max_total_len).
+ * spans, w, layer, l0  as for speechkv_pool_kv (they define nW and tau).
+ * mask_mode      SPEECHKV_MASK_WINDOW_END or SPEECHKV_MASK_WINDOW_START.
+ * scale          logit scale, 1/sqrt(head_dim) in the paper.
+ * lse            device fp32 [batch][num_q_heads][q_len] receiving the
+ *                natural-log log-sum-exp of each row's scaled logits, or NULL.
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ */
+int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
+                          int32_t q_len, const speechkv_paged_kv* cache,
+                          const speechkv_spans* spans, int32_t w, int32_t layer,
+                          int32_t l0, int32_t mask_mode, float scale, void* out,
+                          float* lse, void* stream);
+
+/* Length of the compressed sequence, P + ceil(T / w_eff) + N (Sec. III-B,
+ * Sec. III-C), or -1 for a negative length, w < 1 or negative layer/l0.
+ * Host only. */
+int64_t speechkv_compressed_len(int32_t prefix_len, int32_t speech_len,
+                                int32_t suffix_len, int32_t w, int32_t layer,
+                                int32_t l0);
+
+/* Split count chosen by speechkv_decode_attn when num_splits = 0, from the
+ * number of (sequence, KV head) pairs and the longest cache.  Host only;
+ * returns -1 on a non-positive batch/num_kv_heads or a negative length. */
+int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads,
+                                   int32_t max_cache_len);
+
+/* Bytes of workspace speechkv_decode_attn needs for num_splits splits
+ * (0 = the automatic choice), or 0 when no workspace is needed.  Host only;
+ * returns 0 for invalid arguments (the decode call reports those). */
+size_t speechkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads,
+                                       int32_t num_kv_heads, int32_t head_dim,
+                                       int32_t max_cache_len,
+                                       int32_t num_splits);
+
+/* Static text for a status code.  Host only; never NULL. */
+const char* speechkv_status_string(int status);
+
+/* Library version string, e.g. "0.1.0".  Host only. */
+const char* speechkv_version(void);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* SPEECHKV_H */
