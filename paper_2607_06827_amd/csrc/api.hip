@@ -1,0 +1,270 @@
+// C-ABI host layer of libspeechkv: argument validation, grid sizing and
+// dispatch to the kernels.  Every check runs before the first HIP call, so a
+// call that returns an error has enqueued nothing.  No allocation, no global
+// mutable state, no synchronisation.
+#include "../../include/speechkv.h"
+
+#include <stdint.h>
+
+#include "kernels.hpp"
+
+namespace {
+
+constexpr int kMaxGrid = 65535;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int elt_size(int dtype) { return dtype == SPEECHKV_DTYPE_BF16 ? 2 : 4; }
+
+int log2_exact(int x) {
+  int s = 0;
+  while ((1 << s) < x) ++s;
+  return (1 << s) == x ? s : -1;
+}
+
+// Checks shared by every call on the cache description.
+int check_cache(const speechkv_paged_kv* c) {
+  if (!c || !c->k_pages || !c->v_pages || !c->block_table) return SPEECHKV_ERR_INVALID_ARG;
+  if (c->num_pages < 1 || c->max_pages_per_seq < 1 || c->num_kv_heads < 1)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (c->dtype != SPEECHKV_DTYPE_F32 && c->dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return SPEECHKV_ERR_UNSUPPORTED;
+  if (c->page_size < 8 || c->page_size > 256 || log2_exact(c->page_size) < 0)
+    return SPEECHKV_ERR_UNSUPPORTED;
+  if (c->num_kv_heads > kMaxGrid) return SPEECHKV_ERR_UNSUPPORTED;
+  if ((int64_t)c->max_pages_per_seq * c->page_size > INT32_MAX) return SPEECHKV_ERR_INVALID_ARG;
+  if (!aligned16(c->k_pages) || !aligned16(c->v_pages)) return SPEECHKV_ERR_INVALID_ARG;
+  return SPEECHKV_OK;
+}
+
+int check_spans(const speechkv_spans* s) {
+  if (!s || !s->prefix_len || !s->speech_len || !s->suffix_len) return SPEECHKV_ERR_INVALID_ARG;
+  if (s->max_speech_len < 0 || s->max_total_len < 0 || s->max_speech_len > s->max_total_len)
+    return SPEECHKV_ERR_INVALID_ARG;
+  return SPEECHKV_OK;
+}
+
+skv::PagedView view_of(const speechkv_paged_kv* c) {
+  skv::PagedView v;
+  v.num_pages = c->num_pages;
+  v.page_shift = log2_exact(c->page_size);
+  v.max_pages = c->max_pages_per_seq;
+  v.kv_heads = c->num_kv_heads;
+  return v;
+}
+
+int group_of(int num_q_heads, int num_kv_heads) {
+  if (num_q_heads < 1 || num_q_heads % num_kv_heads) return -1;
+  const int g = num_q_heads / num_kv_heads;
+  return (g == 1 || g == 2 || g == 4 || g == 8) ? g : -1;
+}
+
+int64_t page_pool_bytes(const speechkv_paged_kv* c) {
+  return (int64_t)c->num_pages * c->num_kv_heads * c->page_size * c->head_dim * elt_size(c->dtype);
+}
+
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + (uintptr_t)nb && b0 < a0 + (uintptr_t)na;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? SPEECHKV_OK : SPEECHKV_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int64_t speechkv_compressed_len(int32_t prefix_len, int32_t speech_len, int32_t suffix_len,
+                                int32_t w, int32_t layer, int32_t l0) {
+  if (prefix_len < 0 || speech_len < 0 || suffix_len < 0 || w < 1 || layer < 0 || l0 < 0) return -1;
+  const int64_t weff = layer >= l0 ? w : 1;
+  return (int64_t)prefix_len + (speech_len + weff - 1) / weff + suffix_len;
+}
+
+int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t max_cache_len) {
+  if (batch < 1 || num_kv_heads < 1 || max_cache_len < 0) return -1;
+  // Aim at about 1024 blocks (4 per CU on 256 CUs) while keeping at least
+  // 128 keys per split, so that each block streams >= 64 KB of bf16 K/V and
+  // the partials stay a small fraction of the traffic.
+  const int64_t units = (int64_t)batch * num_kv_heads;
+  int64_t s = (1024 + units - 1) / units;
+  const int64_t by_len = (max_cache_len + 127) / 128;
+  if (s > by_len) s = by_len;
+  if (s > 64) s = 64;
+  if (s < 1) s = 1;
+  return (int32_t)s;
+}
+
+size_t speechkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t head_dim, int32_t max_cache_len, int32_t num_splits) {
+  if (batch < 1 || num_q_heads < 1 || num_kv_heads < 1 || head_dim < 1 || max_cache_len < 0 ||
+      num_splits < 0)
+    return 0;
+  const int32_t s = num_splits ? num_splits : speechkv_decode_num_splits(batch, num_kv_heads, max_cache_len);
+  if (s <= 1) return 0;
+  const size_t rows = (size_t)batch * num_q_heads * s;
+  size_t o_bytes = rows * head_dim * sizeof(float);
+  o_bytes = (o_bytes + 255) & ~(size_t)255;
+  return o_bytes + rows * 2 * sizeof(float);
+}
+
+const char* speechkv_status_string(int status) {
+  switch (status) {
+    case SPEECHKV_OK: return "ok";
+    case SPEECHKV_ERR_INVALID_ARG: return "invalid argument";
+    case SPEECHKV_ERR_UNSUPPORTED: return "unsupported dtype, head_dim, group size or page size";
+    case SPEECHKV_ERR_WORKSPACE: return "workspace missing or too small";
+    case SPEECHKV_ERR_ALIAS: return "raw K/V overlap the destination page pool";
+    case SPEECHKV_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* speechkv_version(void) { return "0.1.0"; }
+
+int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
+                     int64_t stride_h, int32_t batch, int32_t raw_len, const speechkv_spans* spans,
+                     int32_t w, const float* gate_u, int32_t layer, int32_t l0,
+                     const speechkv_paged_kv* cache, int32_t* cache_len_out, void* stream) {
+  if (!k_raw || !v_raw) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_cache(cache);
+  if (st) return st;
+  if ((st = check_spans(spans))) return st;
+  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || w < 1 || layer < 0 || l0 < 0)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (stride_b < 0 || stride_s < 0 || stride_h < 0) return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > raw_len) return SPEECHKV_ERR_INVALID_ARG;
+  const int esz = elt_size(cache->dtype);
+  const int D = cache->head_dim;
+  const int64_t per16 = 16 / esz;  // elements per 16 bytes
+  if (stride_b % per16 || stride_s % per16 || stride_h % per16) return SPEECHKV_ERR_INVALID_ARG;
+  if (!aligned16(k_raw) || !aligned16(v_raw)) return SPEECHKV_ERR_INVALID_ARG;
+  if (gate_u && !aligned16(gate_u)) return SPEECHKV_ERR_INVALID_ARG;
+  // byte extent of the raw tensors versus the pool they are written into
+  const int64_t last = (int64_t)(batch - 1) * stride_b + (int64_t)(raw_len - 1) * stride_s +
+                       (int64_t)(cache->num_kv_heads - 1) * stride_h + D;
+  const int64_t raw_bytes = last * esz;
+  const int64_t pool_bytes = page_pool_bytes(cache);
+  if (overlaps(k_raw, raw_bytes, cache->k_pages, pool_bytes) ||
+      overlaps(k_raw, raw_bytes, cache->v_pages, pool_bytes) ||
+      overlaps(v_raw, raw_bytes, cache->k_pages, pool_bytes) ||
+      overlaps(v_raw, raw_bytes, cache->v_pages, pool_bytes))
+    return SPEECHKV_ERR_ALIAS;
+  skv::PoolArgs a;
+  a.k_raw = k_raw;
+  a.v_raw = v_raw;
+  a.stride_b = stride_b;
+  a.stride_s = stride_s;
+  a.stride_h = stride_h;
+  a.raw_len = raw_len;
+  a.prefix_len = spans->prefix_len;
+  a.speech_len = spans->speech_len;
+  a.suffix_len = spans->suffix_len;
+  a.w_eff = layer >= l0 ? w : 1;
+  a.gate = gate_u;
+  a.k_pages = cache->k_pages;
+  a.v_pages = cache->v_pages;
+  a.table = cache->block_table;
+  a.pv = view_of(cache);
+  a.cache_len_out = cache_len_out;
+  a.max_out = spans->max_total_len;
+  return status_of(skv::launch_pool(a, cache->dtype, D, batch, static_cast<hipStream_t>(stream)));
+}
+
+int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
+                         const speechkv_paged_kv* cache, const int32_t* cache_len,
+                         int32_t max_cache_len, const void* k_new, const void* v_new, float scale,
+                         int32_t num_splits, void* out, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  if (!q || !out || !cache_len) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_cache(cache);
+  if (st) return st;
+  if (batch < 1 || batch > kMaxGrid || max_cache_len < 0 || num_splits < 0 || num_splits > kMaxGrid)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if ((k_new == nullptr) != (v_new == nullptr)) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale == scale)) return SPEECHKV_ERR_INVALID_ARG;
+  if ((int64_t)max_cache_len > (int64_t)cache->max_pages_per_seq * cache->page_size)
+    return SPEECHKV_ERR_INVALID_ARG;
+  const int group = group_of(num_q_heads, cache->num_kv_heads);
+  if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
+  if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(out) || (k_new && (!aligned16(k_new) || !aligned16(v_new))))
+    return SPEECHKV_ERR_INVALID_ARG;
+  const int splits = num_splits ? num_splits
+                                : speechkv_decode_num_splits(batch, cache->num_kv_heads, max_cache_len);
+  const size_t need = speechkv_decode_workspace_bytes(batch, num_q_heads, cache->num_kv_heads,
+                                                      cache->head_dim, max_cache_len, splits);
+  if (need && (!workspace || workspace_bytes < need || !aligned16(workspace))) return SPEECHKV_ERR_WORKSPACE;
+  skv::DecodeArgs a;
+  a.q = q;
+  a.k_pages = cache->k_pages;
+  a.v_pages = cache->v_pages;
+  a.table = cache->block_table;
+  a.pv = view_of(cache);
+  a.cache_len = cache_len;
+  a.max_len = max_cache_len;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.num_splits = splits;
+  a.out = out;
+  a.ws_o = nullptr;
+  a.ws_ml = nullptr;
+  if (splits > 1) {
+    const size_t rows = (size_t)batch * num_q_heads * splits;
+    size_t o_bytes = rows * cache->head_dim * sizeof(float);
+    o_bytes = (o_bytes + 255) & ~(size_t)255;
+    a.ws_o = static_cast<float*>(workspace);
+    a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + o_bytes);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = skv::launch_decode(a, cache->dtype, cache->head_dim, group, batch, s);
+  if (e != hipSuccess) return SPEECHKV_ERR_HIP;
+  if (splits > 1) e = skv::launch_decode_merge(a, cache->dtype, cache->head_dim, num_q_heads, batch, s);
+  return status_of(e);
+}
+
+int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                          const speechkv_paged_kv* cache, const speechkv_spans* spans, int32_t w,
+                          int32_t layer, int32_t l0, int32_t mask_mode, float scale, void* out,
+                          float* lse, void* stream) {
+  if (!q || !out) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_cache(cache);
+  if (st) return st;
+  if ((st = check_spans(spans))) return st;
+  if (batch < 1 || q_len < 1 || w < 1 || layer < 0 || l0 < 0) return SPEECHKV_ERR_INVALID_ARG;
+  if (mask_mode != SPEECHKV_MASK_WINDOW_END && mask_mode != SPEECHKV_MASK_WINDOW_START)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > q_len) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale == scale)) return SPEECHKV_ERR_INVALID_ARG;
+  if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
+  const int group = group_of(num_q_heads, cache->num_kv_heads);
+  if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len == 0) return SPEECHKV_OK;
+  const int rows_per_tile = skv::prefill_rows_per_tile(group);
+  const int64_t tiles = (spans->max_total_len + rows_per_tile - 1) / rows_per_tile;
+  if ((int64_t)batch * cache->num_kv_heads * tiles > INT32_MAX) return SPEECHKV_ERR_INVALID_ARG;
+  skv::PrefillArgs a;
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.k_pages = cache->k_pages;
+  a.v_pages = cache->v_pages;
+  a.table = cache->block_table;
+  a.pv = view_of(cache);
+  a.prefix_len = spans->prefix_len;
+  a.speech_len = spans->speech_len;
+  a.suffix_len = spans->suffix_len;
+  a.w_eff = layer >= l0 ? w : 1;
+  a.mask_mode = mask_mode;
+  a.q_len = q_len;
+  a.num_tiles = (int)tiles;
+  a.num_q_heads = num_q_heads;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  return status_of(skv::launch_prefill(a, cache->dtype, cache->head_dim, group, batch,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,134 @@
+// Device helpers shared by the SpeechKV kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace skv {
+
+typedef unsigned short bf16_bits;  // raw bf16 storage
+
+// ------------------------------------------------------------------ numerics
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
+
+// ------------------------------------------------------ 8-element row chunks
+// Every kernel moves head_dim rows in chunks of 8 elements: 16 bytes of bf16
+// or 32 bytes of fp32.
+
+template <typename T>
+struct Chunk;
+
+template <>
+struct Chunk<bf16_bits> {
+  uint4 raw;  // 8 bf16
+  __device__ __forceinline__ void load(const bf16_bits* p) { raw = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void store(bf16_bits* p) const { *reinterpret_cast<uint4*>(p) = raw; }
+  __device__ __forceinline__ void zero() { raw = make_uint4(0, 0, 0, 0); }
+  __device__ __forceinline__ void to_float(float* f) const {
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  __device__ __forceinline__ void from_float(const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16(f[2 * i]) | (f32_to_bf16(f[2 * i + 1]) << 16);
+    raw = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+
+template <>
+struct Chunk<float> {
+  float4 a, b;  // 8 fp32
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void store(float* p) const {
+    reinterpret_cast<float4*>(p)[0] = a;
+    reinterpret_cast<float4*>(p)[1] = b;
+  }
+  __device__ __forceinline__ void zero() {
+    a = make_float4(0.f, 0.f, 0.f, 0.f);
+    b = a;
+  }
+  __device__ __forceinline__ void to_float(float* f) const {
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+    f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  __device__ __forceinline__ void from_float(const float* f) {
+    a = make_float4(f[0], f[1], f[2], f[3]);
+    b = make_float4(f[4], f[5], f[6], f[7]);
+  }
+};
+
+// -------------------------------------------------------- lane reductions
+// DPP row operations act inside rows of 16 lanes.  After the four steps
+// below every lane of a 16-lane row (8-lane group for kLanes = 8) holds the
+// row's sum.
+
+template <int kCtrl>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, false));
+}
+
+constexpr int kDppQuadXor1 = 0xB1;    // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;    // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <- 7 - i within 8
+constexpr int kDppMirror = 0x140;     // lane i <- 15 - i within 16
+
+template <int kLanes>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(kLanes == 8 || kLanes == 16, "group of 8 or 16 lanes");
+  x += dpp<kDppQuadXor1>(x);
+  x += dpp<kDppQuadXor2>(x);
+  x += dpp<kDppHalfMirror>(x);
+  if (kLanes == 16) x += dpp<kDppMirror>(x);
+  return x;
+}
+
+__device__ __forceinline__ float xor_shuffle(float x, int mask) { return __shfl_xor(x, mask, 64); }
+
+// ----------------------------------------------------------- paged cache
+struct PagedView {
+  int64_t num_pages;
+  int page_shift;      // log2(page_size)
+  int max_pages;       // per sequence
+  int kv_heads;
+};
+
+// Element offset of row `slot` of (page, head) in a [pages][heads][page][D] pool.
+template <int D>
+__device__ __forceinline__ int64_t page_row(int64_t page, int head, int slot, const PagedView& pv) {
+  return (((page * pv.kv_heads + head) << pv.page_shift) + slot) * (int64_t)D;
+}
+
+// Page holding cache slot c of sequence b, or -1 when the table entry is out
+// of range (the caller then skips the row).
+__device__ __forceinline__ int64_t page_of(const int32_t* __restrict__ table, int b, int c,
+                                           const PagedView& pv) {
+  int idx = c >> pv.page_shift;
+  if (idx >= pv.max_pages) return -1;
+  int64_t page = table[(int64_t)b * pv.max_pages + idx];
+  return (page >= 0 && page < pv.num_pages) ? page : -1;
+}
+
+}  // namespace skv

@@ -1,0 +1,320 @@
+// Full-resolution queries attending over the compressed cache under the
+// causal mask over compressed positions (arXiv 2607.06827, Sec. III-B, Eq. 5
+// and the mask described after it; Sec. III-C: the same computation runs on
+// the fly in training).
+//
+// Mask.  Key c is visible from full-resolution position tau(c): prefix keys at
+// their own position, pooled window i at its last frame (WINDOW_END) or first
+// frame (WINDOW_START), suffix key m at P + T + m.  tau is increasing, so row
+// p sees the prefix [0, n_vis(p)) of the cache and a query tile needs only the
+// key tiles below n_vis of its last row; rows are masked per element inside
+// the last tiles.
+//
+// Tiling (wave64, 32x32 MFMA).  A block owns one (sequence, KV head) and 32*RB
+// query rows for all G query heads of the group (G*RB waves, RB = max(1, 4/G)),
+// so every K/V tile staged in LDS serves G*RB waves.  Each wave holds its 32
+// query rows in registers and, per 32-key tile, computes
+//     S^T = K Q^T            (keys x queries; A = K tile, B = Q^T)
+// so that the C layout puts one query per lane column.  The online softmax
+// then runs per lane (row max exchanged with the partner lane l^32), and the
+// probabilities already sit in the B-operand layout of
+//     O^T += V^T P^T          (A = V^T tile from LDS, B = P^T)
+// with the key order of the C layout carried into the V^T reads.  V is
+// transposed while it is staged into LDS.  bf16 uses
+// v_mfma_f32_32x32x16_bf16 (8 elements per lane per operand), fp32 uses
+// v_mfma_f32_32x32x2_f32 (1 element), both accumulating in fp32.
+//
+// Blocks are remapped so that the eight XCDs each run a contiguous range of
+// (sequence, head, tile) items: tiles of one (b, g) share that XCD's L2 copy
+// of the compressed K/V.  Heavy tiles (late rows) are issued first.
+#include "kernels.hpp"
+
+namespace skv {
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x8_t __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+template <typename T>
+struct Mfma;
+
+template <>
+struct Mfma<bf16_bits> {
+  static constexpr int kPack = 8;  // elements per lane per operand
+  typedef bf16x8_t Frag;
+  static __device__ __forceinline__ f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ Frag load(const bf16_bits* p) {
+    return __builtin_bit_cast(Frag, *reinterpret_cast<const u16x8_t*>(p));
+  }
+  static __device__ __forceinline__ Frag zero() { return __builtin_bit_cast(Frag, u16x8_t{0, 0, 0, 0, 0, 0, 0, 0}); }
+  // keys 8*(i/4) + 4*hg + (i%4) for i = 8kk .. 8kk+7: two runs of four
+  static __device__ __forceinline__ Frag load_vt(const bf16_bits* row, int kk, int hg) {
+    u16x4_t lo = *reinterpret_cast<const u16x4_t*>(row + 16 * kk + 4 * hg);
+    u16x4_t hi = *reinterpret_cast<const u16x4_t*>(row + 16 * kk + 8 + 4 * hg);
+    u16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(Frag, v);
+  }
+  static __device__ __forceinline__ float round_p(float p) { return bf16_to_f32(f32_to_bf16(p)); }
+  static __device__ __forceinline__ Frag pack_p(const float* p) {
+    u16x8_t v;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (unsigned short)f32_to_bf16(p[i]);
+    return __builtin_bit_cast(Frag, v);
+  }
+};
+
+template <>
+struct Mfma<float> {
+  static constexpr int kPack = 1;
+  typedef float Frag;
+  static __device__ __forceinline__ f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ Frag load(const float* p) { return *p; }
+  static __device__ __forceinline__ Frag zero() { return 0.f; }
+  // key 8*(kk/4) + 4*hg + (kk%4)
+  static __device__ __forceinline__ Frag load_vt(const float* row, int kk, int hg) {
+    return row[8 * (kk / 4) + 4 * hg + (kk % 4)];
+  }
+  static __device__ __forceinline__ float round_p(float p) { return p; }
+  static __device__ __forceinline__ Frag pack_p(const float* p) { return p[0]; }
+};
+
+// Number of compressed keys visible from full-resolution row p.
+__device__ __forceinline__ int visible_keys(int p, int P, int T, int nW, int w, int mode) {
+  if (p < P) return p + 1;
+  const int t = p - P;
+  if (t < T) {
+    if (mode == 1) return P + t / w + 1;        // window visible from its first frame
+    return (t == T - 1) ? P + nW : P + (t + 1) / w;  // ... from its last frame
+  }
+  return P + nW + (t - T) + 1;
+}
+
+template <int G>
+struct PrefillShape {
+  static constexpr int kRowBlocks = G >= 4 ? 1 : 4 / G;
+  static constexpr int kWaves = G * kRowBlocks;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kRows = 32 * kRowBlocks;
+};
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(PrefillArgs a) {
+  typedef Mfma<T> M;
+  typedef typename M::Frag Frag;
+  constexpr int kThreads = PrefillShape<G>::kThreads;
+  constexpr int kRows = PrefillShape<G>::kRows;
+  constexpr int kKeys = 32;                       // keys per tile
+  constexpr int kPack = M::kPack;
+  constexpr int kStep = 2 * kPack;                // head-dim elements per QK MFMA
+  constexpr int kQChunks = D / kStep;
+  constexpr int kElems16 = 16 / (int)sizeof(T);   // elements per 16-byte chunk
+  constexpr int kChunksPerRow = D / kElems16;
+  constexpr int kRowK = D + kElems16;             // padded K row (elements)
+  constexpr int kRowV = kKeys + (sizeof(T) == 2 ? 8 : 4);  // padded V^T row
+  constexpr float kLn2 = 0.6931471805599453f;
+
+  __shared__ __attribute__((aligned(16))) T s_k[kKeys * kRowK];
+  __shared__ __attribute__((aligned(16))) T s_vt[D * kRowV];
+
+  // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int tile = a.num_tiles - 1 - item % a.num_tiles;
+  const int g = (item / a.num_tiles) % heads;
+  const int b = item / a.num_tiles / heads;
+
+  const int P = max(a.prefix_len[b], 0);
+  const int T_ = max(a.speech_len[b], 0);
+  const int N = max(a.suffix_len[b], 0);
+  const int w = a.w_eff;
+  const int nW = (T_ + w - 1) / w;
+  const int rows = min(P + T_ + N, a.q_len);
+  const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
+  const int p0 = tile * kRows;
+  if (p0 >= rows) return;
+  const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = g * G + wave % G;
+  const int col = lane & 31, hg = lane >> 5;
+  const int p = p0 + (wave / G) * 32 + col;
+  const bool qvalid = p < rows;
+  const int nvis = qvalid ? visible_keys(p, P, T_, nW, w, a.mask_mode) : 0;
+  const int hq = a.num_q_heads;
+  const int slot_mask = (1 << a.pv.page_shift) - 1;
+
+  // this lane's query row, as the B operand of S^T = K Q^T
+  Frag qf[kQChunks];
+  const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + p) * hq + h) * D;
+#pragma unroll
+  for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = qvalid ? M::load(qrow + kc * kStep + hg * kPack) : M::zero();
+
+  f32x16_t o[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  float m_run = neg_inf(), l_run = 0.f;
+
+  const T* kpool = static_cast<const T*>(a.k_pages);
+  const T* vpool = static_cast<const T*>(a.v_pages);
+  const int ntiles = (kmax + kKeys - 1) / kKeys;
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int kb = kt * kKeys;
+    // stage K (row-major) and V (transposed) for keys [kb, kb + 32); two keys
+    // per work item so that V^T pairs are written as one LDS word
+    for (int idx = tid; idx < (kKeys / 2) * kChunksPerRow; idx += kThreads) {
+      const int pair = idx / kChunksPerRow, ch = idx % kChunksPerRow;
+      uint4 vv[2];
+#pragma unroll
+      for (int rr = 0; rr < 2; ++rr) {
+        const int key = kb + 2 * pair + rr;
+        int64_t page = -1;
+        if (key < kmax) page = page_of(a.table, b, key, a.pv);
+        uint4 kv = make_uint4(0, 0, 0, 0);
+        vv[rr] = kv;
+        if (page >= 0) {
+          const int64_t off = page_row<D>(page, g, key & slot_mask, a.pv) + ch * kElems16;
+          kv = *reinterpret_cast<const uint4*>(kpool + off);
+          vv[rr] = *reinterpret_cast<const uint4*>(vpool + off);
+        }
+        *reinterpret_cast<uint4*>(&s_k[(2 * pair + rr) * kRowK + ch * kElems16]) = kv;
+      }
+      const uint32_t w0[4] = {vv[0].x, vv[0].y, vv[0].z, vv[0].w};
+      const uint32_t w1[4] = {vv[1].x, vv[1].y, vv[1].z, vv[1].w};
+      if (sizeof(T) == 2) {
+        // element e of a chunk is half e%2 of word e/2; keys (2*pair, 2*pair+1)
+        // of one element form one 32-bit LDS word of V^T
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t lo = e % 2 ? w0[e / 2] >> 16 : w0[e / 2] & 0xffffu;
+          const uint32_t hi = e % 2 ? w1[e / 2] >> 16 : w1[e / 2] & 0xffffu;
+          *reinterpret_cast<uint32_t*>(&s_vt[(ch * 8 + e) * kRowV + 2 * pair]) = lo | (hi << 16);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          *reinterpret_cast<uint2*>(&s_vt[(ch * 4 + e) * kRowV + 2 * pair]) = make_uint2(w0[e], w1[e]);
+      }
+    }
+    __syncthreads();
+
+    // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
+    f32x16_t st;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) st[i] = 0.f;
+    const T* krow = &s_k[col * kRowK + hg * kPack];
+#pragma unroll
+    for (int kc = 0; kc < kQChunks; ++kc) st = M::mma(M::load(krow + kc * kStep), qf[kc], st);
+
+    float pr[16];
+    float mt = neg_inf();
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
+      pr[i] = key < nvis ? st[i] * a.scale_log2 : neg_inf();
+      mt = fmaxf(mt, pr[i]);
+    }
+    mt = fmaxf(mt, xor_shuffle(mt, 32));
+    const float mn = fmaxf(m_run, mt);
+    if (mn != neg_inf()) {
+      const float corr = fast_exp2(m_run - mn);
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        // the P.V product takes P in the element type: normalise by the sum
+        // of exactly those values so that the weights sum to one
+        pr[i] = M::round_p(fast_exp2(pr[i] - mn));
+        sum += pr[i];
+      }
+      l_run = l_run * corr + sum;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+      m_run = mn;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) pr[i] = 0.f;
+    }
+
+    // O^T += V^T P^T over the 32 keys of the tile
+#pragma unroll
+    for (int kk = 0; kk < kKeys / kStep; ++kk) {
+      const Frag pf = M::pack_p(pr + kk * kPack);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const Frag vf = M::load_vt(&s_vt[(db * 32 + col) * kRowV], kk, hg);
+        o[db] = M::mma(vf, pf, o[db]);
+      }
+    }
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + xor_shuffle(l_run, 32);
+  if (!qvalid) return;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  T* orow = static_cast<T*>(a.out) + (((int64_t)b * a.q_len + p) * hq + h) * D;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+    for (int ig = 0; ig < 4; ++ig) {
+      const int d0 = db * 32 + 8 * ig + 4 * hg;
+      if (sizeof(T) == 2) {
+        u16x4_t v;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = (unsigned short)f32_to_bf16(o[db][4 * ig + t] * inv);
+        *reinterpret_cast<u16x4_t*>(reinterpret_cast<bf16_bits*>(orow) + d0) = v;
+      } else {
+        float4 v = make_float4(o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
+                               o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(orow) + d0) = v;
+      }
+    }
+  }
+  if (hg == 0 && a.lse)
+    a.lse[((int64_t)b * hq + h) * a.q_len + p] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : neg_inf();
+}
+
+template <typename T, int D>
+hipError_t launch_prefill_d(const PrefillArgs& a, int group, int batch, hipStream_t s) {
+  const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
+  switch (group) {
+    case 1: return launch_struct(prefill_kernel<T, D, 1>, dim3(items), dim3(PrefillShape<1>::kThreads), s, a);
+    case 2: return launch_struct(prefill_kernel<T, D, 2>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
+    case 4: return launch_struct(prefill_kernel<T, D, 4>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
+    default: return launch_struct(prefill_kernel<T, D, 8>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
+  }
+}
+
+}  // namespace
+
+int prefill_rows_per_tile(int group) {
+  switch (group) {
+    case 1: return PrefillShape<1>::kRows;
+    case 2: return PrefillShape<2>::kRows;
+    case 4: return PrefillShape<4>::kRows;
+    default: return PrefillShape<8>::kRows;
+  }
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int group, int batch,
+                          hipStream_t s) {
+  if (dtype == 1) {
+    if (head_dim == 128) return launch_prefill_d<bf16_bits, 128>(a, group, batch, s);
+    return launch_prefill_d<bf16_bits, 64>(a, group, batch, s);
+  }
+  if (head_dim == 128) return launch_prefill_d<float, 128>(a, group, batch, s);
+  return launch_prefill_d<float, 64>(a, group, batch, s);
+}
+
+}  // namespace skv

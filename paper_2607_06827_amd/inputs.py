@@ -122,6 +122,12 @@ def _normal(shape, device, seed) -> torch.Tensor:
                        dtype=torch.float32)
 
 
+def normal(shape, seed: int, device="cpu", scale: float = 1.0,
+           dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Seeded N(0, scale^2) tensor drawn in fp32, rounded once to `dtype`."""
+    return (_normal(tuple(shape), device, stream_seed(seed, 0, 99)) * scale).to(dtype)
+
+
 def ar1(eps: torch.Tensor, rho: float, chunk: int = 64) -> torch.Tensor:
     """Stationary AR(1) along dim 1 of eps [B, T, F] (fp32, any device).
 

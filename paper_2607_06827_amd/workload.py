@@ -1,0 +1,152 @@
+"""Device-resident SpeechKV jobs: every layer's inputs, caches and outputs.
+
+A job is one batch of sequences through the whole hot path, layer by layer:
+  prefill   pool the raw K/V of each layer into its paged cache (identity
+            below l0), then attend with the full-resolution queries;
+  decode    for each step and each layer, store the new token's K/V and
+            attend over the cache (one query per sequence).
+This module only allocates device memory, fills it from `inputs` and issues
+the library calls in order; all computation happens in libspeechkv's kernels.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import inputs
+from .speechkv import (PagedKV, Spans, speechkv_compressed_len, speechkv_decode_attn,
+                       speechkv_decode_num_splits, speechkv_decode_workspace_bytes,
+                       speechkv_pool_kv, speechkv_prefill_attn)
+
+
+class Job:
+    """All buffers of one workload on one device.
+
+    layers        which layer indices to build (default: all); layer ids keep
+                  their meaning with respect to l0.
+    l0            first compressed layer (default wl.l0; num_layers or more
+                  means no compression, the full-KV reference run).
+    with_prefill  allocate prefill queries/outputs and run prefill attention.
+    keep_decode   keep every decode output ([layers, steps, B, Hq, D]) rather
+                  than reusing one buffer.
+    share_inputs  another Job whose input tensors this one reuses.
+    """
+
+    def __init__(self, wl: inputs.Workload, device="cuda", layers: Optional[Sequence[int]] = None,
+                 l0: Optional[int] = None, with_prefill: bool = True, keep_decode: bool = False,
+                 share_inputs: Optional["Job"] = None, shuffle_pages: bool = True,
+                 num_splits: int = 0):
+        self.wl = wl
+        self.device = torch.device(device)
+        self.layers: List[int] = list(range(wl.num_layers)) if layers is None else list(layers)
+        self.l0 = wl.l0 if l0 is None else l0
+        self.with_prefill = with_prefill
+        self.num_splits = num_splits
+        B, Hq, Hkv, D = wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+        S = wl.prefill_len
+        dev = self.device
+        self.scale = D ** -0.5
+
+        ints = lambda v: torch.full((B,), v, dtype=torch.int32, device=dev)
+        self.spans = Spans(ints(wl.prefix_len), ints(wl.speech_len), ints(wl.suffix_len),
+                           wl.speech_len, S)
+
+        src = share_inputs
+        self.k_raw, self.v_raw, self.gate, self.q_prefill = [], [], [], []
+        self.q_dec, self.k_new, self.v_new = [], [], []
+        for i, l in enumerate(self.layers):
+            if src is not None:
+                j = src.layers.index(l)
+                self.k_raw.append(src.k_raw[j]); self.v_raw.append(src.v_raw[j])
+                self.gate.append(src.gate[j])
+                self.q_prefill.append(src.q_prefill[j] if with_prefill else None)
+                self.q_dec.append(src.q_dec[j]); self.k_new.append(src.k_new[j])
+                self.v_new.append(src.v_new[j])
+                continue
+            k, v = inputs.raw_kv(wl, l, device=dev)
+            self.k_raw.append(k); self.v_raw.append(v)
+            self.gate.append(inputs.gate(wl, l, device=dev))
+            self.q_prefill.append(inputs.prefill_q(wl, l, device=dev) if with_prefill else None)
+            steps = range(wl.decode_steps)
+            self.q_dec.append(torch.stack([inputs.decode_q(wl, l, s, device=dev) for s in steps])
+                              if wl.decode_steps else None)
+            kn = [inputs.decode_kv_new(wl, l, s, device=dev) for s in steps]
+            self.k_new.append(torch.stack([x[0] for x in kn]) if kn else None)
+            self.v_new.append(torch.stack([x[1] for x in kn]) if kn else None)
+
+        # caches sized for prefill plus every decoded token
+        self.prefill_clen = [speechkv_compressed_len(wl.prefix_len, wl.speech_len, wl.suffix_len,
+                                                     wl.w, l, self.l0) for l in self.layers]
+        self.caches: List[PagedKV] = []
+        self.cache_len_out = []
+        for i, l in enumerate(self.layers):
+            cap = self.prefill_clen[i] + wl.decode_steps
+            pages = max(1, -(-cap // wl.page_size))
+            table, total = inputs.block_table(B, pages, wl.seed, layer=l, shuffle=shuffle_pages)
+            kp = torch.empty(total, Hkv, wl.page_size, D, dtype=wl.torch_dtype, device=dev)
+            vp = torch.empty_like(kp)
+            self.caches.append(PagedKV(kp, vp, table.to(dev)))
+            self.cache_len_out.append(torch.zeros(B, dtype=torch.int32, device=dev))
+
+        # decode cache lengths per (layer, step): prefill length + tokens so far
+        self.dec_len = [torch.stack([ints(self.prefill_clen[i] + s + 1)
+                                     for s in range(wl.decode_steps)]) if wl.decode_steps else None
+                        for i in range(len(self.layers))]
+        max_len = max(self.prefill_clen) + wl.decode_steps
+        splits = [num_splits or speechkv_decode_num_splits(B, Hkv, c + wl.decode_steps)
+                  for c in self.prefill_clen]
+        ws = max(speechkv_decode_workspace_bytes(B, Hq, Hkv, D, max_len, s) for s in splits)
+        self.workspace = torch.empty(max(ws, 16) // 4 + 4, dtype=torch.float32, device=dev)
+
+        self.prefill_out = (torch.empty(B, S, Hq, D, dtype=wl.torch_dtype, device=dev)
+                            if with_prefill else None)
+        n_out = len(self.layers) * wl.decode_steps if keep_decode else 1
+        self.keep_decode = keep_decode
+        self.decode_out = torch.empty(max(n_out, 1), B, Hq, D, dtype=wl.torch_dtype, device=dev)
+
+    # ------------------------------------------------------------------ steps
+    def run_prefill(self, stream=None, layers: Optional[Sequence[int]] = None):
+        wl = self.wl
+        for i, l in enumerate(self.layers):
+            if layers is not None and l not in layers:
+                continue
+            speechkv_pool_kv(self.k_raw[i], self.v_raw[i], self.spans, wl.w, self.gate[i], l,
+                             self.l0, self.caches[i], self.cache_len_out[i], stream=stream)
+            if self.with_prefill:
+                speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.w, l,
+                                      self.l0, self.prefill_out, scale=self.scale, stream=stream)
+
+    def decode_out_at(self, i: int, step: int) -> torch.Tensor:
+        return self.decode_out[i * self.wl.decode_steps + step if self.keep_decode else 0]
+
+    def run_decode_step(self, step: int, stream=None):
+        for i in range(len(self.layers)):
+            self.decode_layer(i, step, stream)
+
+    def decode_layer(self, i: int, step: int, stream=None):
+        wl = self.wl
+        speechkv_decode_attn(self.q_dec[i][step], self.caches[i], self.dec_len[i][step],
+                             self.prefill_clen[i] + step + 1, self.decode_out_at(i, step),
+                             k_new=self.k_new[i][step], v_new=self.v_new[i][step],
+                             scale=self.scale, num_splits=self.num_splits,
+                             workspace=self.workspace, stream=stream)
+
+    def run(self, stream=None):
+        """The whole job: prefill of every layer, then every decode step."""
+        self.run_prefill(stream)
+        for s in range(self.wl.decode_steps):
+            self.run_decode_step(s, stream)
+
+    # ------------------------------------------------------------- accounting
+    def decode_bytes(self, step: int) -> int:
+        """Algorithmic HBM bytes of one decode step over all layers: every
+        cached K and V row once, plus q, the new K/V and out."""
+        wl = self.wl
+        e = 2 if wl.dtype == "bf16" else 4
+        row = wl.num_kv_heads * wl.head_dim * e
+        total = 0
+        for i in range(len(self.layers)):
+            L = self.prefill_clen[i] + step + 1
+            total += wl.batch * (2 * row * L + 2 * wl.num_q_heads * wl.head_dim * e + 2 * row)
+        return total

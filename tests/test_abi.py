@@ -1,0 +1,168 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol, its
+host helpers are right, and invalid arguments are rejected before any HIP call
+(so these run without a GPU; no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2607_06827_amd import speechkv as skv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "speechkv.h")
+lib = skv._lib
+
+FAKE = 0x10000000  # 16-byte aligned, never dereferenced on these paths
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(speechkv_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
+                          "speechkv_compressed_len", "speechkv_decode_num_splits",
+                          "speechkv_decode_workspace_bytes", "speechkv_status_string",
+                          "speechkv_version"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    for code in (0, -1, -2, -3, -4, -5):
+        assert skv.speechkv_status_string(code) and skv.speechkv_status_string(code) != "unknown status"
+    assert skv.speechkv_status_string(17) == "unknown status"
+    assert re.fullmatch(r"\d+\.\d+\.\d+", skv.speechkv_version())
+
+
+def test_compressed_len_agrees_with_oracle():
+    for P in (0, 3, 32):
+        for T in (0, 1, 3, 4, 5, 60, 375, 750, 7500):
+            for N in (0, 7):
+                for w in (1, 2, 3, 4, 8):
+                    for layer, l0 in ((0, 0), (3, 5), (14, 14), (27, 14)):
+                        assert skv.speechkv_compressed_len(P, T, N, w, layer, l0) == \
+                            oracle.compressed_len(P, T, N, w, layer, l0)
+    assert skv.speechkv_compressed_len(32, 375, 0, 4, 0, 0) == 32 + 94
+    assert skv.speechkv_compressed_len(32, 1500, 64, 4, 0, 0) == 471
+    assert skv.speechkv_compressed_len(-1, 3, 0, 4, 0, 0) == -1
+    assert skv.speechkv_compressed_len(1, 3, 0, 0, 0, 0) == -1
+
+
+def test_split_choice_and_workspace():
+    s = skv.speechkv_decode_num_splits(64, 8, 348)
+    assert 1 <= s <= 64
+    assert skv.speechkv_decode_num_splits(1, 2, 39) == 1
+    assert skv.speechkv_decode_num_splits(0, 8, 10) == -1
+    assert skv.speechkv_decode_workspace_bytes(1, 4, 2, 64, 39, 1) == 0
+    n = skv.speechkv_decode_workspace_bytes(16, 16, 8, 128, 7788, 8)
+    assert n >= 16 * 16 * 8 * (128 + 2) * 4
+    assert skv.speechkv_decode_workspace_bytes(16, 16, 8, 128, 7788, 0) == \
+        skv.speechkv_decode_workspace_bytes(16, 16, 8, 128, 7788,
+                                            skv.speechkv_decode_num_splits(16, 8, 7788))
+
+
+def cache(**kw):
+    c = dict(k_pages=FAKE, v_pages=FAKE + (1 << 24), block_table=FAKE + (2 << 24), num_pages=64,
+             page_size=16, max_pages_per_seq=8, num_kv_heads=2, head_dim=64,
+             dtype=skv.DTYPE_BF16)
+    c.update(kw)
+    return skv._PagedKV(**c)
+
+
+def spans(**kw):
+    s = dict(prefix_len=FAKE + (3 << 24), speech_len=FAKE + (3 << 24) + 64,
+             suffix_len=FAKE + (3 << 24) + 128, max_speech_len=40, max_total_len=60)
+    s.update(kw)
+    return skv._Spans(**s)
+
+
+RAW = FAKE + (8 << 24)
+
+
+def pool(c=None, s=None, **kw):
+    a = dict(k=RAW, v=RAW + (1 << 22), sb=60 * 2 * 64, ss=2 * 64, sh=64, batch=2, raw_len=60, w=4,
+             gate=None, layer=1, l0=0, clen=None)
+    a.update(kw)
+    c = c or cache()
+    s = s or spans()
+    return lib.speechkv_pool_kv(a["k"], a["v"], a["sb"], a["ss"], a["sh"], a["batch"], a["raw_len"],
+                                ctypes.byref(s), a["w"], a["gate"], a["layer"], a["l0"],
+                                ctypes.byref(c), a["clen"], None)
+
+
+def decode(c=None, **kw):
+    a = dict(q=FAKE + (9 << 24), batch=2, hq=4, clen=FAKE + (10 << 24), max_len=100, kn=None,
+             vn=None, scale=0.125, splits=0, out=FAKE + (11 << 24), ws=None, ws_bytes=0)
+    a.update(kw)
+    c = c or cache()
+    return lib.speechkv_decode_attn(a["q"], a["batch"], a["hq"], ctypes.byref(c), a["clen"],
+                                    a["max_len"], a["kn"], a["vn"], a["scale"], a["splits"],
+                                    a["out"], a["ws"], a["ws_bytes"], None)
+
+
+def prefill(c=None, s=None, **kw):
+    a = dict(q=FAKE + (12 << 24), batch=2, hq=4, q_len=60, w=4, layer=1, l0=0, mode=0,
+             scale=0.125, out=FAKE + (13 << 24), lse=None)
+    a.update(kw)
+    c = c or cache()
+    s = s or spans()
+    return lib.speechkv_prefill_attn(a["q"], a["batch"], a["hq"], a["q_len"], ctypes.byref(c),
+                                     ctypes.byref(s), a["w"], a["layer"], a["l0"], a["mode"],
+                                     a["scale"], a["out"], a["lse"], None)
+
+
+E_ARG, E_UNS, E_WS, E_ALIAS = skv.ERR_INVALID_ARG, skv.ERR_UNSUPPORTED, skv.ERR_WORKSPACE, skv.ERR_ALIAS
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=0), E_ARG), (dict(w=0), E_ARG),
+    (dict(layer=-1), E_ARG), (dict(sb=-8), E_ARG), (dict(ss=3), E_ARG), (dict(k=RAW + 4), E_ARG),
+    (dict(gate=FAKE + 4), E_ARG), (dict(raw_len=50), E_ARG),
+    (dict(k=FAKE), E_ALIAS), (dict(v=FAKE + (1 << 24) + 256), E_ALIAS),
+])
+def test_pool_rejects(kw, code):
+    assert pool(**kw) == code
+
+
+@pytest.mark.parametrize("ckw,code", [
+    (dict(dtype=7), E_UNS), (dict(head_dim=96), E_UNS), (dict(page_size=12), E_UNS),
+    (dict(page_size=4), E_UNS), (dict(page_size=512), E_UNS), (dict(num_pages=0), E_ARG),
+    (dict(k_pages=None), E_ARG), (dict(block_table=None), E_ARG), (dict(k_pages=FAKE + 2), E_ARG),
+])
+def test_cache_description_rejected_by_every_call(ckw, code):
+    assert pool(c=cache(**ckw)) == code
+    assert decode(c=cache(**ckw)) == code
+    assert prefill(c=cache(**ckw)) == code
+
+
+@pytest.mark.parametrize("skw", [dict(prefix_len=None), dict(max_total_len=-1),
+                                 dict(max_speech_len=70)])
+def test_bad_spans(skw):
+    assert pool(s=spans(**skw)) == E_ARG
+    assert prefill(s=spans(**skw)) == E_ARG
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(clen=None), E_ARG), (dict(batch=0), E_ARG),
+    (dict(hq=3), E_ARG), (dict(hq=6), E_UNS), (dict(hq=32), E_UNS), (dict(max_len=-1), E_ARG),
+    (dict(max_len=129), E_ARG), (dict(kn=FAKE), E_ARG), (dict(splits=-1), E_ARG),
+    (dict(scale=float("nan")), E_ARG), (dict(q=FAKE + 8), E_ARG),
+    (dict(splits=4), E_WS), (dict(splits=4, ws=FAKE + (14 << 24), ws_bytes=64), E_WS),
+])
+def test_decode_rejects(kw, code):
+    assert decode(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(q_len=59), E_ARG), (dict(mode=2), E_ARG),
+    (dict(w=0), E_ARG), (dict(hq=6), E_UNS), (dict(hq=5), E_ARG), (dict(lse=FAKE + 2), E_ARG),
+    (dict(scale=float("nan")), E_ARG), (dict(batch=0), E_ARG),
+])
+def test_prefill_rejects(kw, code):
+    assert prefill(**kw) == code

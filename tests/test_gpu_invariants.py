@@ -1,0 +1,162 @@
+"""GPU invariants of the kernels (no oracle needed for the equalities).
+
+- decode output does not depend on the split count (and equals the oracle);
+- V == 1 gives O == 1 on every row that sees a key;
+- a decode step equals the prefill row of the same query at the same position;
+- page placement changes nothing (shuffled vs identity block tables);
+- repeated runs are bit-for-bit identical;
+- invalid calls with real device buffers return their error and write nothing.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import TOL, f64, gather, rel_err
+from paper_2607_06827_amd import inputs
+from paper_2607_06827_amd import speechkv as skv
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+DEV = "cuda"
+
+
+def setup(B=3, Hq=8, Hkv=2, D=128, P=(5, 0, 31), T=(301, 77, 500), N=(7, 2, 0), w=4,
+          dtype=torch.bfloat16, seed=11, shuffle=True, ones_v=False, page_size=16):
+    rows = [p + t + n for p, t, n in zip(P, T, N)]
+    S = max(rows)
+    k = inputs.normal((B, S, Hkv, D), seed, dtype=dtype).to(DEV)
+    v = (torch.ones(B, S, Hkv, D, dtype=dtype) if ones_v
+         else inputs.normal((B, S, Hkv, D), seed + 1, dtype=dtype)).to(DEV)
+    u = inputs.normal((Hkv, D), seed + 2, scale=D ** -0.5).to(DEV)
+    q = inputs.normal((B, S, Hq, D), seed + 3, dtype=dtype).to(DEV)
+    clen = [skv.speechkv_compressed_len(p, t, n, w, 0, 0) for p, t, n in zip(P, T, N)]
+    pages = -(-(max(clen) + 4) // page_size)
+    table, total = inputs.block_table(B, pages, seed, shuffle=shuffle)
+    cache = skv.PagedKV(torch.zeros(total, Hkv, page_size, D, dtype=dtype, device=DEV),
+                        torch.zeros(total, Hkv, page_size, D, dtype=dtype, device=DEV), table.to(DEV))
+    spans = skv.Spans(*(torch.tensor(x, dtype=torch.int32, device=DEV) for x in (P, T, N)),
+                      max(T), S)
+    return dict(k=k, v=v, u=u, q=q, cache=cache, spans=spans, clen=clen, rows=rows, S=S, w=w,
+                B=B, Hq=Hq, Hkv=Hkv, D=D, dtype=dtype, P=P, T=T, N=N)
+
+
+def pool(x):
+    skv.speechkv_pool_kv(x["k"], x["v"], x["spans"], x["w"], x["u"], 0, 0, x["cache"])
+
+
+def prefill(x, mode=0):
+    out = torch.zeros(x["B"], x["S"], x["Hq"], x["D"], dtype=x["dtype"], device=DEV)
+    skv.speechkv_prefill_attn(x["q"], x["cache"], x["spans"], x["w"], 0, 0, out, mask_mode=mode)
+    return out
+
+
+def decode(x, q, lens, splits=0):
+    out = torch.zeros(x["B"], x["Hq"], x["D"], dtype=x["dtype"], device=DEV)
+    n = skv.speechkv_decode_workspace_bytes(x["B"], x["Hq"], x["Hkv"], x["D"], max(lens), splits)
+    ws = torch.empty(max(n, 16) // 4 + 4, dtype=torch.float32, device=DEV)
+    skv.speechkv_decode_attn(q, x["cache"], torch.tensor(lens, dtype=torch.int32, device=DEV),
+                             max(lens), out, num_splits=splits, workspace=ws)
+    return out
+
+
+def test_decode_independent_of_split_count():
+    x = setup()
+    pool(x)
+    q = x["q"][:, 0].contiguous()
+    outs = {s: decode(x, q, x["clen"], s) for s in (1, 2, 3, 8, 33, 0)}
+    torch.cuda.synchronize()
+    kh, vh, _ = oracle.pool(f64(x["k"]), f64(x["v"]), x["P"], x["T"], x["N"], x["w"], 0, 0, f64(x["u"]))
+    ref, _ = oracle.decode(f64(q), kh, vh, x["clen"], x["D"] ** -0.5)
+    for s, o in outs.items():
+        assert rel_err(f64(o), f64(outs[1])) <= TOL["bf16"], s
+        assert rel_err(f64(o), ref) <= TOL["bf16"], s
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_constant_values_give_constant_outputs(mode):
+    x = setup(ones_v=True, P=(0, 3, 9), T=(40, 13, 100), N=(3, 0, 5))
+    pool(x)
+    out = prefill(x, mode)
+    d = decode(x, x["q"][:, 1].contiguous(), x["clen"])
+    torch.cuda.synchronize()
+    for b in range(x["B"]):
+        R = x["rows"][b]
+        o = out[b, :R].float()
+        if mode == 0 and x["P"][b] == 0:  # rows before the first window closes see nothing
+            assert torch.all(o[:x["w"] - 1] == 0)
+            o = o[x["w"] - 1:]
+        # P is rounded to bf16 before the P.V product: |o - 1| is a few ulp
+        assert torch.all((o - 1.0).abs() <= 1e-2), (b, mode)
+    assert torch.all(d.float() == 1.0)  # decode sums p and p*1 identically
+
+
+def test_decode_equals_prefill_row():
+    x = setup()
+    pool(x)
+    out = prefill(x)
+    last = [r - 1 for r in x["rows"]]
+    q = torch.stack([x["q"][b, last[b]] for b in range(x["B"])]).contiguous()
+    d = decode(x, q, x["clen"])
+    torch.cuda.synchronize()
+    for b in range(x["B"]):
+        assert rel_err(f64(d[b]), f64(out[b, last[b]])) <= TOL["bf16"]
+
+
+def test_page_placement_does_not_matter():
+    a = setup(shuffle=True)
+    b = setup(shuffle=False)
+    pool(a)
+    pool(b)
+    pa, pb = prefill(a), prefill(b)
+    qa = a["q"][:, 2].contiguous()
+    da, db = decode(a, qa, a["clen"]), decode(b, qa, b["clen"])
+    torch.cuda.synchronize()
+    for s in range(a["B"]):
+        ka, va = gather(a["cache"], s, a["clen"][s])
+        kb, vb = gather(b["cache"], s, b["clen"][s])
+        assert torch.equal(ka, kb) and torch.equal(va, vb)
+    assert torch.equal(pa, pb) and torch.equal(da, db)
+
+
+def test_runs_are_bitwise_repeatable():
+    x = setup()
+    pool(x)
+    p1 = prefill(x)
+    q = x["q"][:, 3].contiguous()
+    d1 = decode(x, q, x["clen"], 5)
+    pool(x)
+    p2 = prefill(x)
+    d2 = decode(x, q, x["clen"], 5)
+    torch.cuda.synchronize()
+    assert torch.equal(p1, p2) and torch.equal(d1, d2)
+
+
+def test_errors_with_device_buffers_write_nothing():
+    x = setup()
+    cache = x["cache"]
+    # one allocation holding raw K and, overlapping its second half, the K pool
+    nk, npool = x["k"].numel(), cache.k_pages.numel()
+    big = torch.zeros(nk // 2 + npool + nk, dtype=x["dtype"], device=DEV)
+    raw = big[:nk].view_as(x["k"])
+    raw.copy_(x["k"])
+    pool_view = big[nk // 2:nk // 2 + npool].view_as(cache.k_pages)
+    aliased = skv.PagedKV(pool_view, cache.v_pages, cache.block_table)
+    before = big.clone()
+    with pytest.raises(skv.SpeechKVError) as e:
+        skv.speechkv_pool_kv(raw, x["v"], x["spans"], x["w"], x["u"], 0, 0, aliased)
+    assert e.value.status == skv.ERR_ALIAS
+    torch.cuda.synchronize()
+    assert torch.equal(big, before)
+    before = cache.k_pages.clone()
+    # workspace too small for the requested splits
+    out = torch.zeros(x["B"], x["Hq"], x["D"], dtype=x["dtype"], device=DEV)
+    tiny = torch.empty(4, dtype=torch.float32, device=DEV)
+    with pytest.raises(skv.SpeechKVError) as e:
+        skv.speechkv_decode_attn(x["q"][:, 0].contiguous(), cache,
+                                 torch.tensor(x["clen"], dtype=torch.int32, device=DEV),
+                                 max(x["clen"]), out, num_splits=4, workspace=tiny)
+    assert e.value.status == skv.ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.equal(cache.k_pages, before) and not out.any()

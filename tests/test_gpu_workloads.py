@@ -1,0 +1,129 @@
+"""GPU parity on the five synthetic workloads, at their full sizes.
+
+tiny fp32 (1 layer, b=1), 30 s layer (b=32) and prefill (b=8, 1596 queries
+over 471 keys) are checked on every output; the 28-layer 60 s stack (b=64) and
+the 10-minute decode (b=16, w in {2,4,8}) are run whole, in the launch
+configuration the benchmark times, and checked on sampled (layer, step,
+sequence) outputs the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import TOL, f64, gather, oracle_decode_for, oracle_pool_for, oracle_prefill_for, rel_err
+from paper_2607_06827_amd import inputs
+from paper_2607_06827_amd.workload import Job
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def check_pool(job, i, bs, errs):
+    for b in bs:
+        kh, vh, clen = oracle_pool_for(job, i, b)
+        L = int(clen[0])
+        gk, gv = gather(job.caches[i], b, L)
+        errs.append(("pool_k", job.layers[i], b, rel_err(f64(gk), kh[0, :L])))
+        errs.append(("pool_v", job.layers[i], b, rel_err(f64(gv), vh[0, :L])))
+
+
+def check_prefill(job, i, bs, errs):
+    ref, ref_lse = oracle_prefill_for(job, i, bs)
+    R = job.wl.prefill_len
+    got = f64(job.prefill_out[bs])
+    errs.append(("prefill", job.layers[i], tuple(bs), rel_err(got[:, :R], ref[:, :R])))
+
+
+def check_decode(job, i, b, steps, errs):
+    pooled = oracle_pool_for(job, i, b)
+    for s in steps:
+        ref, _ = oracle_decode_for(job, i, b, s, pooled)
+        got = f64(job.decode_out_at(i, s)[b])
+        errs.append(("decode", job.layers[i], (b, s), rel_err(got, ref)))
+
+
+def assert_ok(errs, tol, name):
+    worst = max(errs, key=lambda e: e[-1])
+    print(f"{name}: {len(errs)} checks, worst {worst}", flush=True)
+    bad = [e for e in errs if not e[-1] <= tol]
+    assert not bad, f"{name}: {len(bad)} checks above {tol}: {bad[:8]}"
+
+
+def test_tiny_fp32_everything():
+    wl = inputs.TINY_F32
+    job = Job(wl, keep_decode=True)
+    job.run()
+    torch.cuda.synchronize()
+    errs = []
+    check_pool(job, 0, [0], errs)
+    check_prefill(job, 0, [0], errs)
+    check_decode(job, 0, 0, range(wl.decode_steps), errs)
+    assert_ok(errs, TOL["f32"], wl.name)
+
+
+def test_layer_30s_everything():
+    wl = inputs.LAYER_30S
+    job = Job(wl, keep_decode=True)
+    job.run()
+    torch.cuda.synchronize()
+    errs = []
+    bs = list(range(wl.batch))
+    check_pool(job, 0, bs, errs)
+    check_prefill(job, 0, bs, errs)
+    # every decode step of every sequence, batched through the oracle
+    kh, vh, clen = oracle.pool(f64(job.k_raw[0]), f64(job.v_raw[0]), [wl.prefix_len] * wl.batch,
+                               [wl.speech_len] * wl.batch, [0] * wl.batch, wl.w, 0, job.l0,
+                               f64(job.gate[0]))
+    L0 = int(clen[0])
+    K = np.concatenate([kh[:, :L0], f64(job.k_new[0]).transpose(1, 0, 2, 3)], axis=1)
+    V = np.concatenate([vh[:, :L0], f64(job.v_new[0]).transpose(1, 0, 2, 3)], axis=1)
+    for s in range(wl.decode_steps):
+        ref, _ = oracle.decode(f64(job.q_dec[0][s]), K, V, [L0 + s + 1] * wl.batch, job.scale)
+        errs.append(("decode", 0, s, rel_err(f64(job.decode_out_at(0, s)), ref)))
+    assert_ok(errs, TOL["bf16"], wl.name)
+
+
+def test_prefill_1500_everything():
+    wl = inputs.PREFILL_1500
+    job = Job(wl)
+    job.run()
+    torch.cuda.synchronize()
+    errs = []
+    bs = list(range(wl.batch))
+    check_pool(job, 0, bs, errs)
+    assert job.prefill_clen[0] == 471
+    check_prefill(job, 0, bs, errs)
+    assert_ok(errs, TOL["bf16"], wl.name)
+
+
+def test_stack_60s_sampled():
+    wl = inputs.STACK_60S
+    job = Job(wl, keep_decode=True)
+    errs = []
+    # prefill outputs share one buffer across layers: check a few layers as they run
+    for l in (0, 13, 14, 27):
+        job.run_prefill(layers=[l])
+        torch.cuda.synchronize()
+        check_prefill(job, job.layers.index(l), [5], errs)
+    job.run()
+    torch.cuda.synchronize()
+    for i in range(wl.num_layers):
+        for b in (0, 37, 63):
+            check_decode(job, i, b, (0, 63, 127), errs)
+        check_pool(job, i, [37], errs)
+    assert_ok(errs, TOL["bf16"], wl.name)
+
+
+@pytest.mark.parametrize("w", [2, 4, 8])
+def test_long_10min_sampled(w):
+    wl = inputs.LONG_10MIN.with_(w=w)
+    job = Job(wl, layers=[0, 13, 14, 27], with_prefill=False, keep_decode=True)
+    job.run()
+    torch.cuda.synchronize()
+    errs = []
+    for i in range(len(job.layers)):
+        for b in (0, 9, 15):
+            check_decode(job, i, b, (0, 127, 255), errs)
+        check_pool(job, i, [9], errs)
+    assert_ok(errs, TOL["bf16"], f"{wl.name}-w{w}")
