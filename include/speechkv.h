@@ -180,7 +180,7 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
  * max_cache_len  host bound on cache_len (sizes the split-K grid).
  * k_new, v_new   device [batch][num_kv_heads][head_dim] of cache->dtype, or
  *                both NULL.
- * scale          logit scale, 1/sqrt(head_dim) in the paper.
+ * scale          logit scale, finite and > 0; 1/sqrt(head_dim) in the paper.
  * num_splits     number of key ranges each (sequence, KV head) is split into
  *                (split-K); 0 selects speechkv_decode_num_splits().  With more
  *                than one split the partial results are merged by a
@@ -223,7 +223,7 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
  * q_len          rows allocated per sequence (>= max_total_len).
  * spans, w, layer, l0  as for speechkv_pool_kv (they define nW and tau).
  * mask_mode      SPEECHKV_MASK_WINDOW_END or SPEECHKV_MASK_WINDOW_START.
- * scale          logit scale, 1/sqrt(head_dim) in the paper.
+ * scale          logit scale, finite and > 0; 1/sqrt(head_dim) in the paper.
  * lse            device fp32 [batch][num_q_heads][q_len] receiving the
  *                natural-log log-sum-exp of each row's scaled logits, or NULL.
  * Errors: INVALID_ARG, UNSUPPORTED, HIP.

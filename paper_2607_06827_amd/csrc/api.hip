@@ -83,12 +83,14 @@ int64_t speechkv_compressed_len(int32_t prefix_len, int32_t speech_len, int32_t 
 
 int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t max_cache_len) {
   if (batch < 1 || num_kv_heads < 1 || max_cache_len < 0) return -1;
-  // Aim at about 1024 blocks (4 per CU on 256 CUs) while keeping at least
-  // 128 keys per split, so that each block streams >= 64 KB of bf16 K/V and
-  // the partials stay a small fraction of the traffic.
+  // A decode block has 8 waves; about 512 blocks (2 per CU on 256 CUs) keep
+  // every CU streaming in one round.  Split a (sequence, KV head) only when
+  // there are fewer pairs than that, and keep at least 16 groups of 4 keys
+  // (two per wave) in every split.
   const int64_t units = (int64_t)batch * num_kv_heads;
-  int64_t s = (1024 + units - 1) / units;
-  const int64_t by_len = (max_cache_len + 127) / 128;
+  int64_t s = (512 + units - 1) / units;
+  const int64_t groups = ((int64_t)max_cache_len + 3) / 4;
+  const int64_t by_len = groups / 16;
   if (s > by_len) s = by_len;
   if (s > 64) s = 64;
   if (s < 1) s = 1;
@@ -182,7 +184,7 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
   if (batch < 1 || batch > kMaxGrid || max_cache_len < 0 || num_splits < 0 || num_splits > kMaxGrid)
     return SPEECHKV_ERR_INVALID_ARG;
   if ((k_new == nullptr) != (v_new == nullptr)) return SPEECHKV_ERR_INVALID_ARG;
-  if (!(scale == scale)) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || scale > 3.0e38f) return SPEECHKV_ERR_INVALID_ARG;  // finite, > 0
   if ((int64_t)max_cache_len > (int64_t)cache->max_pages_per_seq * cache->page_size)
     return SPEECHKV_ERR_INVALID_ARG;
   const int group = group_of(num_q_heads, cache->num_kv_heads);
@@ -236,7 +238,7 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int
   if (mask_mode != SPEECHKV_MASK_WINDOW_END && mask_mode != SPEECHKV_MASK_WINDOW_START)
     return SPEECHKV_ERR_INVALID_ARG;
   if (spans->max_total_len > q_len) return SPEECHKV_ERR_INVALID_ARG;
-  if (!(scale == scale)) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || scale > 3.0e38f) return SPEECHKV_ERR_INVALID_ARG;  // finite, > 0
   if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
   const int group = group_of(num_q_heads, cache->num_kv_heads);
   if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;

@@ -94,6 +94,7 @@ constexpr int kDppQuadXor1 = 0xB1;    // quad_perm [1,0,3,2]
 constexpr int kDppQuadXor2 = 0x4E;    // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141; // lane i <- 7 - i within 8
 constexpr int kDppMirror = 0x140;     // lane i <- 15 - i within 16
+constexpr int kDppRowRor8 = 0x128;    // lane i <- (i + 8) mod 16 within 16 (= i ^ 8)
 
 template <int kLanes>
 __device__ __forceinline__ float group_sum(float x) {

@@ -152,7 +152,8 @@ def test_bad_spans(skw):
     (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(clen=None), E_ARG), (dict(batch=0), E_ARG),
     (dict(hq=3), E_ARG), (dict(hq=6), E_UNS), (dict(hq=32), E_UNS), (dict(max_len=-1), E_ARG),
     (dict(max_len=129), E_ARG), (dict(kn=FAKE), E_ARG), (dict(splits=-1), E_ARG),
-    (dict(scale=float("nan")), E_ARG), (dict(q=FAKE + 8), E_ARG),
+    (dict(scale=float("nan")), E_ARG), (dict(scale=0.0), E_ARG), (dict(scale=-0.1), E_ARG),
+    (dict(scale=float("inf")), E_ARG), (dict(q=FAKE + 8), E_ARG),
     (dict(splits=4), E_WS), (dict(splits=4, ws=FAKE + (14 << 24), ws_bytes=64), E_WS),
 ])
 def test_decode_rejects(kw, code):
@@ -162,7 +163,8 @@ def test_decode_rejects(kw, code):
 @pytest.mark.parametrize("kw,code", [
     (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(q_len=59), E_ARG), (dict(mode=2), E_ARG),
     (dict(w=0), E_ARG), (dict(hq=6), E_UNS), (dict(hq=5), E_ARG), (dict(lse=FAKE + 2), E_ARG),
-    (dict(scale=float("nan")), E_ARG), (dict(batch=0), E_ARG),
+    (dict(scale=float("nan")), E_ARG), (dict(scale=0.0), E_ARG), (dict(scale=-1.0), E_ARG),
+    (dict(batch=0), E_ARG),
 ])
 def test_prefill_rejects(kw, code):
     assert prefill(**kw) == code
