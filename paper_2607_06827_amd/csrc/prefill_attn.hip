@@ -6,9 +6,9 @@
 // Mask.  Key c is visible from full-resolution position tau(c): prefix keys at
 // their own position, pooled window i at its last frame (WINDOW_END) or first
 // frame (WINDOW_START), suffix key m at P + T + m.  tau is increasing, so row
-// p sees the prefix [0, n_vis(p)) of the cache and a query tile needs only the
-// key tiles below n_vis of its last row; rows are masked per element inside
-// the last tiles.
+// p sees the prefix [0, n_vis(p)) of the cache: a query tile needs only the
+// key tiles below n_vis of its last row, and only the tiles that straddle the
+// n_vis of some row of a wave are masked element by element.
 //
 // Tiling (wave64, 32x32 MFMA).  A block owns one (sequence, KV head) and 32*RB
 // query rows for all G query heads of the group (G*RB waves, RB = max(1, 4/G)),
@@ -16,13 +16,20 @@
 // query rows in registers and, per 32-key tile, computes
 //     S^T = K Q^T            (keys x queries; A = K tile, B = Q^T)
 // so that the C layout puts one query per lane column.  The online softmax
-// then runs per lane (row max exchanged with the partner lane l^32), and the
+// then runs per lane (row max exchanged with the partner lane l^32 by a
+// permlane swap, rescaling only when the max grows by more than 2^8), and the
 // probabilities already sit in the B-operand layout of
 //     O^T += V^T P^T          (A = V^T tile from LDS, B = P^T)
-// with the key order of the C layout carried into the V^T reads.  V is
-// transposed while it is staged into LDS.  bf16 uses
+// with the key order of the C layout carried into the V^T reads.  bf16 uses
 // v_mfma_f32_32x32x16_bf16 (8 elements per lane per operand), fp32 uses
 // v_mfma_f32_32x32x2_f32 (1 element), both accumulating in fp32.
+//
+// K/V tiles are double-buffered in LDS: the next tile's global loads are in
+// flight while the current one is multiplied, and one barrier per tile
+// separates the phases.  V is transposed while it is staged; the V^T row
+// stride (18 words) and the key-pair-fastest lane order put the 64 lanes of a
+// staging store, and the 32 lanes of an operand read, on distinct banks.  The
+// output tile goes back through LDS so that rows leave as 16-byte stores.
 //
 // Blocks are remapped so that the eight XCDs each run a contiguous range of
 // (sequence, head, tile) items: tiles of one (b, g) share that XCD's L2 copy
@@ -34,16 +41,24 @@ namespace skv {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned short u16x8_t __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Running maxima may lag the true maximum by up to 2^kSlack in the exponent
+// before the accumulators are rescaled; the final division by the weight sum
+// makes the choice of reference exact.
+constexpr float kSlack = 8.f;
 
 template <typename T>
 struct Mfma;
 
 template <>
 struct Mfma<bf16_bits> {
-  static constexpr int kPack = 8;  // elements per lane per operand
+  static constexpr int kPack = 8;   // elements per lane per operand
+  static constexpr int kRowV = 36;  // V^T row stride in elements (18 words)
   typedef bf16x8_t Frag;
   static __device__ __forceinline__ f32x16_t mma(Frag a, Frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -59,18 +74,24 @@ struct Mfma<bf16_bits> {
     u16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(Frag, v);
   }
-  static __device__ __forceinline__ float round_p(float p) { return bf16_to_f32(f32_to_bf16(p)); }
+  // round-to-nearest-even pack of 8 probabilities (v_cvt_pk_bf16_f32)
   static __device__ __forceinline__ Frag pack_p(const float* p) {
-    u16x8_t v;
+    Frag f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = (unsigned short)f32_to_bf16(p[i]);
-    return __builtin_bit_cast(Frag, v);
+    for (int i = 0; i < 8; ++i) f[i] = (__bf16)p[i];
+    return f;
+  }
+  // four output values of one row, rounded to bf16, stored as 8 bytes
+  static __device__ __forceinline__ void store4(bf16_bits* dst, float a, float b, float c, float d) {
+    bf16x4_t v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    *reinterpret_cast<bf16x4_t*>(dst) = v;
   }
 };
 
 template <>
 struct Mfma<float> {
   static constexpr int kPack = 1;
+  static constexpr int kRowV = 40;
   typedef float Frag;
   static __device__ __forceinline__ f32x16_t mma(Frag a, Frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
@@ -81,8 +102,10 @@ struct Mfma<float> {
   static __device__ __forceinline__ Frag load_vt(const float* row, int kk, int hg) {
     return row[8 * (kk / 4) + 4 * hg + (kk % 4)];
   }
-  static __device__ __forceinline__ float round_p(float p) { return p; }
   static __device__ __forceinline__ Frag pack_p(const float* p) { return p[0]; }
+  static __device__ __forceinline__ void store4(float* dst, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
+  }
 };
 
 // Number of compressed keys visible from full-resolution row p.
@@ -104,11 +127,24 @@ struct PrefillShape {
   static constexpr int kRows = 32 * kRowBlocks;
 };
 
+__device__ __forceinline__ float partner_max(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+
+__device__ __forceinline__ float partner_sum(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto p = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
 template <typename T, int D, int G>
 __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(PrefillArgs a) {
   typedef Mfma<T> M;
   typedef typename M::Frag Frag;
   constexpr int kThreads = PrefillShape<G>::kThreads;
+  constexpr int kWaves = PrefillShape<G>::kWaves;
   constexpr int kRows = PrefillShape<G>::kRows;
   constexpr int kKeys = 32;                       // keys per tile
   constexpr int kPack = M::kPack;
@@ -117,11 +153,16 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   constexpr int kElems16 = 16 / (int)sizeof(T);   // elements per 16-byte chunk
   constexpr int kChunksPerRow = D / kElems16;
   constexpr int kRowK = D + kElems16;             // padded K row (elements)
-  constexpr int kRowV = kKeys + (sizeof(T) == 2 ? 8 : 4);  // padded V^T row
+  constexpr int kRowV = M::kRowV;                 // padded V^T row (elements)
+  constexpr int kItems = (kKeys / 2) * kChunksPerRow;  // staging work: (key pair, chunk)
+  constexpr int kItemsPerThread = (kItems + kThreads - 1) / kThreads;
+  constexpr int kTileK = kKeys * kRowK, kTileV = D * kRowV;
+  constexpr int kRowO = D + kElems16;             // padded output row (elements)
   constexpr float kLn2 = 0.6931471805599453f;
+  // the output tiles of all waves go through the staging buffers when they fit
+  constexpr bool kStageOut = kWaves * 32 * kRowO <= 2 * (kTileK + kTileV);
 
-  __shared__ __attribute__((aligned(16))) T s_k[kKeys * kRowK];
-  __shared__ __attribute__((aligned(16))) T s_vt[D * kRowV];
+  __shared__ __attribute__((aligned(16))) T s_buf[2 * (kTileK + kTileV)];
 
   // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
   const int nblk = gridDim.x, bid = blockIdx.x;
@@ -146,9 +187,12 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = g * G + wave % G;
   const int col = lane & 31, hg = lane >> 5;
-  const int p = p0 + (wave / G) * 32 + col;
+  const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
+  const int p = wrow0 + col;
   const bool qvalid = p < rows;
   const int nvis = qvalid ? visible_keys(p, P, T_, nW, w, a.mask_mode) : 0;
+  // keys every valid row of the wave sees (n_vis grows with the row)
+  const int nvis_lo = wrow0 < rows ? min(visible_keys(wrow0, P, T_, nW, w, a.mask_mode), clen) : 0;
   const int hq = a.num_q_heads;
   const int slot_mask = (1 << a.pv.page_shift) - 1;
 
@@ -168,84 +212,114 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const T* kpool = static_cast<const T*>(a.k_pages);
   const T* vpool = static_cast<const T*>(a.v_pages);
   const int ntiles = (kmax + kKeys - 1) / kKeys;
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int kb = kt * kKeys;
-    // stage K (row-major) and V (transposed) for keys [kb, kb + 32); two keys
-    // per work item so that V^T pairs are written as one LDS word
-    for (int idx = tid; idx < (kKeys / 2) * kChunksPerRow; idx += kThreads) {
-      const int pair = idx / kChunksPerRow, ch = idx % kChunksPerRow;
-      uint4 vv[2];
+
+  // staging registers: keys (2 pair, 2 pair + 1) of chunk c, for K and V
+  uint4 rk[kItemsPerThread][2], rv[kItemsPerThread][2];
+  auto fetch = [&](int kt) {
 #pragma unroll
-      for (int rr = 0; rr < 2; ++rr) {
-        const int key = kb + 2 * pair + rr;
-        int64_t page = -1;
-        if (key < kmax) page = page_of(a.table, b, key, a.pv);
-        uint4 kv = make_uint4(0, 0, 0, 0);
-        vv[rr] = kv;
-        if (page >= 0) {
-          const int64_t off = page_row<D>(page, g, key & slot_mask, a.pv) + ch * kElems16;
-          kv = *reinterpret_cast<const uint4*>(kpool + off);
-          vv[rr] = *reinterpret_cast<const uint4*>(vpool + off);
+    for (int it = 0; it < kItemsPerThread; ++it) {
+      const int idx = tid + it * kThreads;
+      const int pair = idx % (kKeys / 2), ch = idx / (kKeys / 2);
+      const int key = kt * kKeys + 2 * pair;  // both keys of a pair share a page
+      int64_t page = -1;
+      if (idx < kItems && key < kmax) page = page_of(a.table, b, key, a.pv);
+      rk[it][0] = rk[it][1] = rv[it][0] = rv[it][1] = make_uint4(0, 0, 0, 0);
+      if (page >= 0) {
+        const T* kp = kpool + page_row<D>(page, g, key & slot_mask, a.pv) + ch * kElems16;
+        const T* vp = vpool + (kp - kpool);
+        rk[it][0] = *reinterpret_cast<const uint4*>(kp);
+        rv[it][0] = *reinterpret_cast<const uint4*>(vp);
+        if (key + 1 < kmax) {
+          rk[it][1] = *reinterpret_cast<const uint4*>(kp + D);
+          rv[it][1] = *reinterpret_cast<const uint4*>(vp + D);
         }
-        *reinterpret_cast<uint4*>(&s_k[(2 * pair + rr) * kRowK + ch * kElems16]) = kv;
       }
-      const uint32_t w0[4] = {vv[0].x, vv[0].y, vv[0].z, vv[0].w};
-      const uint32_t w1[4] = {vv[1].x, vv[1].y, vv[1].z, vv[1].w};
+    }
+  };
+  auto stage = [&](int buf) {
+    T* sk = s_buf + buf * (kTileK + kTileV);
+    T* sv = sk + kTileK;
+#pragma unroll
+    for (int it = 0; it < kItemsPerThread; ++it) {
+      const int idx = tid + it * kThreads;
+      if (idx >= kItems) continue;
+      const int pair = idx % (kKeys / 2), ch = idx / (kKeys / 2);
+#pragma unroll
+      for (int rr = 0; rr < 2; ++rr)
+        *reinterpret_cast<uint4*>(&sk[(2 * pair + rr) * kRowK + ch * kElems16]) = rk[it][rr];
+      const uint32_t w0[4] = {rv[it][0].x, rv[it][0].y, rv[it][0].z, rv[it][0].w};
+      const uint32_t w1[4] = {rv[it][1].x, rv[it][1].y, rv[it][1].z, rv[it][1].w};
       if (sizeof(T) == 2) {
-        // element e of a chunk is half e%2 of word e/2; keys (2*pair, 2*pair+1)
+        // element e of a chunk is half e%2 of word e/2; keys (2 pair, 2 pair+1)
         // of one element form one 32-bit LDS word of V^T
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const uint32_t lo = e % 2 ? w0[e / 2] >> 16 : w0[e / 2] & 0xffffu;
           const uint32_t hi = e % 2 ? w1[e / 2] >> 16 : w1[e / 2] & 0xffffu;
-          *reinterpret_cast<uint32_t*>(&s_vt[(ch * 8 + e) * kRowV + 2 * pair]) = lo | (hi << 16);
+          *reinterpret_cast<uint32_t*>(&sv[(ch * 8 + e) * kRowV + 2 * pair]) = lo | (hi << 16);
         }
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          *reinterpret_cast<uint2*>(&s_vt[(ch * 4 + e) * kRowV + 2 * pair]) = make_uint2(w0[e], w1[e]);
+          *reinterpret_cast<uint2*>(&sv[(ch * 4 + e) * kRowV + 2 * pair]) = make_uint2(w0[e], w1[e]);
       }
     }
-    __syncthreads();
+  };
+
+  if (ntiles > 0) {
+    fetch(0);
+    stage(0);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int kb = kt * kKeys;
+    if (kt + 1 < ntiles) fetch(kt + 1);  // in flight during this tile
+    const T* sk = s_buf + (kt & 1) * (kTileK + kTileV);
+    const T* sv = sk + kTileK;
 
     // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
     f32x16_t st;
 #pragma unroll
     for (int i = 0; i < 16; ++i) st[i] = 0.f;
-    const T* krow = &s_k[col * kRowK + hg * kPack];
+    const T* krow = &sk[col * kRowK + hg * kPack];
 #pragma unroll
     for (int kc = 0; kc < kQChunks; ++kc) st = M::mma(M::load(krow + kc * kStep), qf[kc], st);
 
     float pr[16];
     float mt = neg_inf();
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
-      pr[i] = key < nvis ? st[i] * a.scale_log2 : neg_inf();
-      mt = fmaxf(mt, pr[i]);
-    }
-    mt = fmaxf(mt, xor_shuffle(mt, 32));
-    const float mn = fmaxf(m_run, mt);
-    if (mn != neg_inf()) {
-      const float corr = fast_exp2(m_run - mn);
-      float sum = 0.f;
+    const bool masked = kb + kKeys > nvis_lo;  // uniform over the wave
+    if (masked) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        // the P.V product takes P in the element type: normalise by the sum
-        // of exactly those values so that the weights sum to one
-        pr[i] = M::round_p(fast_exp2(pr[i] - mn));
-        sum += pr[i];
+        const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
+        pr[i] = key < nvis ? st[i] : neg_inf();
+        mt = fmaxf(mt, pr[i]);
       }
-      l_run = l_run * corr + sum;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        pr[i] = st[i];
+        mt = fmaxf(mt, pr[i]);
+      }
+    }
+    mt = partner_max(mt) * a.scale_log2;  // the scale is > 0
+    if (mt > m_run + kSlack) {
+      const float corr = fast_exp2(m_run - mt);
+      l_run *= corr;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= corr;
-      m_run = mn;
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) pr[i] = 0.f;
+      m_run = mt;
     }
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_run));
+      if (masked) pr[i] = m_run == neg_inf() ? 0.f : pr[i];  // nothing visible yet
+      sum += pr[i];
+    }
+    l_run += sum;
 
     // O^T += V^T P^T over the 32 keys of the tile
 #pragma unroll
@@ -253,36 +327,54 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
       const Frag pf = M::pack_p(pr + kk * kPack);
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const Frag vf = M::load_vt(&s_vt[(db * 32 + col) * kRowV], kk, hg);
+        const Frag vf = M::load_vt(&sv[(db * 32 + col) * kRowV], kk, hg);
         o[db] = M::mma(vf, pf, o[db]);
       }
     }
+    if (kt + 1 < ntiles) stage((kt + 1) & 1);
     __syncthreads();
   }
 
-  const float l_tot = l_run + xor_shuffle(l_run, 32);
-  if (!qvalid) return;
+  const float l_tot = partner_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  T* orow = static_cast<T*>(a.out) + (((int64_t)b * a.q_len + p) * hq + h) * D;
+  if (hg == 0 && a.lse && qvalid)
+    a.lse[((int64_t)b * hq + h) * a.q_len + p] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : neg_inf();
+
+  if (!kStageOut) {  // direct stores of the C layout: four values per row
+    if (qvalid) {
+      T* orow = static_cast<T*>(a.out) + (((int64_t)b * a.q_len + p) * hq + h) * D;
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) {
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-    for (int ig = 0; ig < 4; ++ig) {
-      const int d0 = db * 32 + 8 * ig + 4 * hg;
-      if (sizeof(T) == 2) {
-        u16x4_t v;
+        for (int ig = 0; ig < 4; ++ig)
+          M::store4(orow + db * 32 + 8 * ig + 4 * hg, o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
+                    o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+    }
+    return;
+  }
+  // output: through LDS, one 32 x D tile per wave, then 16-byte row stores
+  // (the barrier after the last tile has freed the staging buffers)
+  T* so = s_buf + wave * 32 * kRowO;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) v[t] = (unsigned short)f32_to_bf16(o[db][4 * ig + t] * inv);
-        *reinterpret_cast<u16x4_t*>(reinterpret_cast<bf16_bits*>(orow) + d0) = v;
-      } else {
-        float4 v = make_float4(o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
-                               o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
-        *reinterpret_cast<float4*>(reinterpret_cast<float*>(orow) + d0) = v;
-      }
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int ig = 0; ig < 4; ++ig)
+      M::store4(&so[col * kRowO + db * 32 + 8 * ig + 4 * hg], o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
+                o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+  __syncthreads();
+  constexpr int kLanesPerRow = D / kElems16;      // 16-byte chunks per row
+  constexpr int kRowsPerPass = 64 / kLanesPerRow;
+  const int rsub = lane / kLanesPerRow, cch = lane % kLanesPerRow;
+#pragma unroll
+  for (int r0 = 0; r0 < 32; r0 += kRowsPerPass) {
+    const int rr = r0 + rsub;
+    const int out_row = wrow0 + rr;
+    if (out_row < rows) {
+      const uint4 v = *reinterpret_cast<const uint4*>(&so[rr * kRowO + cch * kElems16]);
+      *reinterpret_cast<uint4*>(static_cast<T*>(a.out) + (((int64_t)b * a.q_len + out_row) * hq + h) * D +
+                                cch * kElems16) = v;
     }
   }
-  if (hg == 0 && a.lse)
-    a.lse[((int64_t)b * hq + h) * a.q_len + p] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : neg_inf();
 }
 
 template <typename T, int D>
