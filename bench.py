@@ -66,6 +66,33 @@ def time_graph(g, reps):
     return start.elapsed_time(end) / reps  # ms
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_stack60s_traffic.md")
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2607_06827_amd", "csrc", f)
+                  for f in ("decode_attn.hip", "common.hpp", "kernels.hpp")]
+
+
+def decode_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in DECODE_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary, or None
+    when it is missing or was taken on a different decode kernel source."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    vals = dict(line.split(":", 1) for line in text.splitlines()
+                if line.startswith(("traffic_bytes_per_launch:", "decode_source_sha256:")))
+    if vals.get("decode_source_sha256", "").strip() != decode_source_hash():
+        return None
+    return float(vals["traffic_bytes_per_launch"])
+
+
 def decode_launch_stats(job):
     """Algorithmic bytes and launch count of the decode part of one step."""
     total = sum(job.decode_bytes(s) for s in range(job.wl.decode_steps))
@@ -149,6 +176,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-full", action="store_true", help="skip the uncompressed run")
     ap.add_argument("--num-splits", type=int, default=0)
+    ap.add_argument("--traffic", action="store_true",
+                    help="counter-collection run: two decode steps of the job launched eagerly, "
+                         "then a plain 1 GiB device copy that calibrates the byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the decode, "
@@ -167,6 +197,16 @@ def main():
     job = Job(wl, num_splits=args.num_splits)
     torch.cuda.synchronize()
     log(f"inputs and caches ready in {time.perf_counter() - t0:.1f} s")
+    if args.traffic:
+        job.run()  # the step's launches, eagerly: 28 pool, 28 prefill, 128 x 28 decode
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)  # 1 GiB read + 1 GiB written by one copy kernel
+        torch.cuda.synchronize()
+        dec_bytes, launches = decode_launch_stats(job)
+        print(json.dumps({"traffic_run": True, "copy_bytes": 1 << 30,
+                          "decode_bytes_per_launch": dec_bytes / launches, "decode_launches": launches}))
+        return
     pooled = measure(job, args.steps, args.warmup, "pooled (l0=14, w=4)")
 
     full = None
@@ -199,7 +239,7 @@ def main():
                    "head_dim": wl.head_dim, "page_size": wl.page_size,
                    "tokens_per_step": wl.batch * wl.decode_steps},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(),
                      "kernel": "decode_kernel (+ split merge)",
                      "avg_launch_us": avg_launch_ms * 1e3,
                      "bytes_per_launch": dec_bytes / launches},

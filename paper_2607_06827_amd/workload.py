@@ -139,14 +139,16 @@ class Job:
             self.run_decode_step(s, stream)
 
     # ------------------------------------------------------------- accounting
-    def decode_bytes(self, step: int) -> int:
-        """Algorithmic HBM bytes of one decode step over all layers: every
-        cached K and V row once, plus q, the new K/V and out."""
+    def decode_bytes_layer(self, i: int, step: int) -> int:
+        """Algorithmic HBM bytes of one decode launch (layer index i): every
+        cached K and V row read once, q read, out written, and the new token's
+        K/V read and written once."""
         wl = self.wl
         e = 2 if wl.dtype == "bf16" else 4
         row = wl.num_kv_heads * wl.head_dim * e
-        total = 0
-        for i in range(len(self.layers)):
-            L = self.prefill_clen[i] + step + 1
-            total += wl.batch * (2 * row * L + 2 * wl.num_q_heads * wl.head_dim * e + 2 * row)
-        return total
+        L = self.prefill_clen[i] + step + 1
+        return wl.batch * (2 * row * (L - 1) + 2 * wl.num_q_heads * wl.head_dim * e + 4 * row)
+
+    def decode_bytes(self, step: int) -> int:
+        """Algorithmic HBM bytes of one decode step over all layers."""
+        return sum(self.decode_bytes_layer(i, step) for i in range(len(self.layers)))
