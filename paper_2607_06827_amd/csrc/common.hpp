@@ -88,9 +88,11 @@ struct Chunk<float> {
 // below every lane of a 16-lane row (8-lane group for kLanes = 8) holds the
 // row's sum.
 
+// Every pattern used here reads a lane of the same row that exists, so the
+// "old" operand never shows and bound_ctrl only spares a register copy.
 template <int kCtrl>
 __device__ __forceinline__ float dpp(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, false));
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), kCtrl, 0xf, 0xf, true));
 }
 
 constexpr int kDppQuadXor1 = 0xB1;    // quad_perm [1,0,3,2]
@@ -98,6 +100,12 @@ constexpr int kDppQuadXor2 = 0x4E;    // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141; // lane i <- 7 - i within 8
 constexpr int kDppMirror = 0x140;     // lane i <- 15 - i within 16
 constexpr int kDppRowRor8 = 0x128;    // lane i <- (i + 8) mod 16 within 16 (= i ^ 8)
+constexpr int kDppRowBcast0 = 0x150;  // row_newbcast:n (+ n): lane n of each row to the row
+
+// s_waitcnt immediate (CDNA layout: vmcnt bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8) that waits for every outstanding vector-memory operation and
+// leaves the other counters alone
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 template <int kLanes>
 __device__ __forceinline__ float group_sum(float x) {

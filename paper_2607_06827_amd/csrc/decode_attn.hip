@@ -11,30 +11,39 @@
 // log-sum-exp reduction in fixed split order.
 //
 // Key ranges are cut from the host-known bound on the cache length, so the
-// block-table entries, the queries and the cache length are all requested at
-// once and the first K/V loads wait on a single memory round trip.  The wave's
-// table entries sit one per lane and are read back with readlane, so every
-// load address is a wave-uniform page base plus a fixed per-lane offset.
+// block-table entries, the queries, the cache length and the new token's K/V
+// are all requested at once and the first K/V loads wait on a single memory
+// round trip.  The wave's table entries sit one per lane and are read back
+// with readlane, so every load address is a wave-uniform page base (SGPRs)
+// plus a fixed 32-bit per-lane offset.
 //
-// Lane layout: kLanes lanes per key row, E elements per lane in 16-byte
-// pieces (bf16 rows of 128 with G <= 2: 8 lanes x 16 elements, otherwise
-// D/8 lanes x 8), so kRows = 64 / kLanes consecutive keys of one page form a
-// "group" that the wave reads with E*elt/16 wave-wide loads, each covering
-// whole 128-byte lines of one (page, head) block.  A wave streams its
-// groups in batches of U loads of K and of V, double-buffered so that the next
-// batch is in flight while the current one is reduced.  Batches of groups that
-// lie wholly inside the cache take a branch-free path with non-temporal loads
-// (the cache is read once per step); the last partial group and the newest
-// token go through a masked tail.  q.k is a v_dot2_f32_bf16 partial (fma for
-// fp32) reduced over the row's lanes with DPP; each lane row keeps its own
-// online-softmax sum against a reference max shared by the whole wave (moved,
-// with a rescale, only when a ballot shows some row exceeding it by 2^8), so
-// the rows' states add up at the end (DPP / permlane swaps) and the waves'
-// states merge through LDS.
+// Lane layout: kLanes = D/8 lanes per key row, 8 elements (16 bytes of bf16,
+// 32 of fp32) per lane, so kRows = 64 / kLanes consecutive keys of one page
+// form a "group" that the wave reads with one wave-wide load per 16 bytes,
+// each covering whole 128-byte lines of one (page, head) block.  A wave
+// streams its groups in batches of U groups of K and of V, kDepth batches in
+// flight, branch-free, with non-temporal loads (the cache is read once per
+// step).  The masked tail of the range (at most one batch: the leftover
+// groups and the group holding key L-1) is requested beside the first full
+// batch, so no round trip follows the stream.
+//
+// bf16 rows of 128 (16 lanes) take pairs of groups at a time: the 2G partial
+// q.k sums of a lane (v_dot2_f32_bf16 over bf16 pairs) are reduced over the
+// row "transposed", so that each lane ends with one full logit and the
+// exponent, the growth test and the weight cost one operation per lane; the
+// weights of the two keys a lane row holds are rounded to bf16 as a pair (as
+// in an MFMA P.V) and every accumulator takes both products with one
+// v_dot2_f32_bf16.  Other shapes and the masked tail reduce each logit over
+// its row with DPP and accumulate P.V in fp32.  Each lane row keeps its own
+// online-softmax sums against a reference max shared by the whole wave
+// (moved, with a rescale, only when a ballot shows some logit exceeding it by
+// 2^8), so the rows' states add up at the end (DPP / permlane swaps) and the
+// waves' states merge through LDS in one step.
 //
 // If k_new/v_new are given, the wave whose range holds slot L-1 stores them
-// there, and that key is read from k_new/v_new directly.
-// The kernel moves each K/V byte once: it is bound by HBM bandwidth.
+// there as soon as the page is known, and that key is read from k_new/v_new
+// directly.  The kernel moves each K/V byte once: it is bound by HBM
+// bandwidth.
 #include "kernels.hpp"
 
 namespace skv {
@@ -61,6 +70,7 @@ struct Row {
   uint4 v[kVec];
   // element index inside the row of element k of piece i for lane j
   static __device__ __forceinline__ int elem(int i, int j, int k) { return (i * kLanes + j) * kElems + k; }
+  // base is wave-uniform, lane_off a 32-bit per-lane offset
   __device__ __forceinline__ void stream(const char* base, uint32_t lane_off) {
 #pragma unroll
     for (int i = 0; i < kVec; ++i) v[i] = stream_load(base + lane_off + 16 * kLanes * i);
@@ -118,10 +128,78 @@ struct QSlice {
   }
 };
 
-template <int kLanes>
-__device__ __forceinline__ float row_sum(float x) {
+// Row sums of n independent values (rows of kLanes lanes), step by step.
+template <int kLanes, int n>
+__device__ __forceinline__ void row_sums(float* x) {
   static_assert(kLanes == 8 || kLanes == 16, "rows of 8 or 16 lanes");
-  return group_sum<kLanes>(x);
+#pragma unroll
+  for (int i = 0; i < n; ++i) x[i] += dpp<kDppQuadXor1>(x[i]);
+#pragma unroll
+  for (int i = 0; i < n; ++i) x[i] += dpp<kDppQuadXor2>(x[i]);
+#pragma unroll
+  for (int i = 0; i < n; ++i) x[i] += dpp<kDppHalfMirror>(x[i]);
+  if (kLanes == 16) {
+#pragma unroll
+    for (int i = 0; i < n; ++i) x[i] += dpp<kDppMirror>(x[i]);
+  }
+}
+
+// Transposed row sums over rows of 16 lanes: n partial sums per lane in, one
+// full row sum per lane out, in about n + log2(16/n) + ... steps instead of
+// 4 n.  Each level halves the values a lane carries: the lane keeps the half
+// picked by one bit of its lane index and adds the partner's copy of that
+// half (the partner differs in that bit, so it kept the other half).  The
+// levels pair lanes i^8 (row_ror:8), i^7 (row_half_mirror), i^2 and i^1
+// (quad permutes); together they cover all 16 lanes of the row.  Lane i ends
+// with value number  b3 n/2 + b2 n/4 + b1 n/8 + b0 n/16  (bits of i within
+// its row, terms below 1 dropped).
+template <int kCtrl, int kBit, int c>
+__device__ __forceinline__ void halve_values(float* x, int lane) {
+  const bool up = (lane >> kBit) & 1;
+#pragma unroll
+  for (int t = 0; t < c / 2; ++t) {
+    const float keep = up ? x[t + c / 2] : x[t];
+    const float send = up ? x[t] : x[t + c / 2];
+    x[t] = keep + dpp<kCtrl>(send);
+  }
+}
+
+template <int n>
+__device__ __forceinline__ float transpose_sum16(float* x, int lane) {
+  static_assert(n == 1 || n == 2 || n == 4 || n == 8 || n == 16, "power of two up to 16");
+  if constexpr (n >= 2) halve_values<kDppRowRor8, 3, n>(x, lane);
+  else x[0] += dpp<kDppRowRor8>(x[0]);
+  if constexpr (n >= 4) halve_values<kDppHalfMirror, 2, n / 2>(x, lane);
+  else x[0] += dpp<kDppHalfMirror>(x[0]);
+  if constexpr (n >= 8) halve_values<kDppQuadXor2, 1, n / 4>(x, lane);
+  else x[0] += dpp<kDppQuadXor2>(x[0]);
+  if constexpr (n >= 16) halve_values<kDppQuadXor1, 0, n / 8>(x, lane);
+  else x[0] += dpp<kDppQuadXor1>(x[0]);
+  return x[0];
+}
+
+// Lane k of each 16-lane row, to every lane of that row (k a constant once
+// the caller's loop is unrolled).
+__device__ __forceinline__ uint32_t row_bcast(uint32_t x, int k) {
+  const int v = (int)x;
+  switch (k) {
+    case 0: return (uint32_t)__builtin_amdgcn_mov_dpp(v, kDppRowBcast0 + 0, 0xf, 0xf, true);
+    case 2: return (uint32_t)__builtin_amdgcn_mov_dpp(v, kDppRowBcast0 + 2, 0xf, 0xf, true);
+    case 4: return (uint32_t)__builtin_amdgcn_mov_dpp(v, kDppRowBcast0 + 4, 0xf, 0xf, true);
+    default: return (uint32_t)__builtin_amdgcn_mov_dpp(v, kDppRowBcast0 + 6, 0xf, 0xf, true);
+  }
+}
+
+// Maximum over all 64 lanes (any values), the same in every lane.
+__device__ __forceinline__ float full_wave_max(float x) {
+  x = fmaxf(x, dpp<kDppQuadXor1>(x));
+  x = fmaxf(x, dpp<kDppQuadXor2>(x));
+  x = fmaxf(x, dpp<kDppHalfMirror>(x));
+  x = fmaxf(x, dpp<kDppMirror>(x));
+  auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
 }
 
 // Running maxima may lag the true maximum by up to 2^kSlack in the exponent
@@ -138,6 +216,7 @@ struct DecodeWave {
   typedef Row<T, E, kLanes> R;
   QSlice<T, E, kLanes> qs[G];
   float scale_log2;
+  int lane;
   float m[G], l[G], acc[G][E];  // online softmax state of this lane row (log2 units)
 
   __device__ __forceinline__ void init() {
@@ -167,16 +246,30 @@ struct DecodeWave {
   // are the same in every lane of the wave; they move (and the accumulators
   // are rescaled) only when some row's logits exceed them by more than
   // kSlack, decided by a wave-wide ballot.
+  // bf16 rows of 16 lanes, pairs of groups, up to 4 heads: the unmasked
+  // batches take consume_paired
+  static constexpr bool kPaired = sizeof(T) == 2 && kLanes == 16 && G <= 4;
+
   template <int N, bool kMasked>
   __device__ __forceinline__ void consume(const R* kc, const R* vc, const bool* valid) {
+    if constexpr (kPaired && !kMasked && N == 2) {
+      consume_paired(kc, vc);
+      return;
+    }
     float s[N][G];  // unscaled logits; the scale is > 0
 #pragma unroll
-    for (int u = 0; u < N; ++u) {
+    for (int u = 0; u < N; ++u)
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        s[u][h] = row_sum<kLanes>(qs[h].dot(kc[u]));
-        if (kMasked && !valid[u]) s[u][h] = neg_inf();
-      }
+      for (int h = 0; h < G; ++h) s[u][h] = qs[h].dot(kc[u]);
+    // row sums, one DPP step at a time over all N*G independent chains so that
+    // no step waits on the step just before it
+    row_sums<kLanes, N * G>(&s[0][0]);
+    if (kMasked) {
+#pragma unroll
+      for (int u = 0; u < N; ++u)
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+          if (!valid[u]) s[u][h] = neg_inf();
     }
     float mx[G];
     bool grow = false;
@@ -215,6 +308,72 @@ struct DecodeWave {
       }
     }
   }
+
+  // Two unmasked bf16 groups (keys r of groups u = 0, 1 in lane row r).
+  // The 2 G partial q.k sums of a lane are reduced transposed, so that lane
+  // (bits b3 b2 b1 b0 of its index in the row) holds the logit of key u = b3
+  // for head h = (b2 b1 b0) / (8 / G): the exponent, the growth test and the
+  // weight are then one operation per lane for the whole batch.  The weight
+  // pair (key 0, key 1) of each head is rounded to bf16 as one pair (as in an
+  // MFMA P.V), broadcast over the row, and every accumulator takes both
+  // products with one v_dot2_f32_bf16 on the element pair (key 0, key 1) of
+  // the row; the weight sum uses the same rounded pair.
+  __device__ __forceinline__ void consume_paired(const R* kc, const R* vc) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    constexpr int kHeadStride = 8 / G;  // lanes between heads within a half row
+    float x[2 * G];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int h = 0; h < G; ++h) x[u * G + h] = qs[h].dot(kc[u]);
+    const float sl = transpose_sum16<2 * G>(x, lane);
+    const int hl = (lane & 7) / kHeadStride;  // this lane's head
+    float ml = m[0];
+#pragma unroll
+    for (int h = 1; h < G; ++h) ml = hl == h ? m[h] : ml;
+    float t = __builtin_fmaf(sl, scale_log2, -ml);
+    if (__builtin_amdgcn_ballot_w64(t > kSlack)) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float M = full_wave_max(hl == h ? sl * scale_log2 : neg_inf());
+        if (M > m[h] + kSlack) {
+          const float corr = fast_exp2(m[h] - M);
+          l[h] *= corr;
+#pragma unroll
+          for (int i = 0; i < E; ++i) acc[h][i] *= corr;
+          m[h] = M;
+        }
+      }
+      ml = m[0];
+#pragma unroll
+      for (int h = 1; h < G; ++h) ml = hl == h ? m[h] : ml;
+      t = __builtin_fmaf(sl, scale_log2, -ml);
+    }
+    const float pw = fast_exp2(t);
+    // lanes of key 0 pack (own, key-1 partner); row_newbcast spreads head h's
+    // pair from lane h * kHeadStride to its row
+    const uint32_t pk = pack_bf16x2(pw, dpp<kDppRowRor8>(pw));
+    uint32_t lo[E / 2], hi[E / 2];  // (key 0, key 1) of elements 2w and 2w+1
+#pragma unroll
+    for (int w = 0; w < E / 2; ++w) {
+      const uint32_t a = vc[0].word(w), b = vc[1].word(w);
+      lo[w] = __builtin_amdgcn_perm(b, a, 0x05040100u);
+      hi[w] = __builtin_amdgcn_perm(b, a, 0x07060302u);
+    }
+    const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3f803f80u);  // (1, 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const bf16x2_t pp = __builtin_bit_cast(bf16x2_t, row_bcast(pk, h * kHeadStride));
+      l[h] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l[h], false);
+#pragma unroll
+      for (int w = 0; w < E / 2; ++w) {
+        acc[h][2 * w] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, lo[w]), pp,
+                                                        acc[h][2 * w], false);
+        acc[h][2 * w + 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, hi[w]), pp,
+                                                            acc[h][2 * w + 1], false);
+      }
+    }
+  }
 };
 
 // Sum a value over the lane rows of the wave (lane ^ K for K = 8, 16, 32).
@@ -243,6 +402,11 @@ __device__ __forceinline__ void sum_rows(float* l, float (*acc)[E]) {
   }
 }
 
+#ifndef SKV_DECODE_DEPTH
+#define SKV_DECODE_DEPTH 2
+#endif
+constexpr int kDepth = SKV_DECODE_DEPTH;  // load batches in flight per wave
+
 template <typename T, int D, int G, int NW, int U, int E>
 __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(DecodeArgs a) {
   typedef DecodeWave<T, D, G, E> W;
@@ -253,8 +417,6 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   __shared__ float s_acc[NW][G][D];
   __shared__ float s_m[NW][G];
   __shared__ float s_l[NW][G];
-  __shared__ float s_w[NW][G];  // per-wave merge weights
-  __shared__ float s_den[G];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
@@ -282,12 +444,16 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   const int32_t* table = a.table + (int64_t)b * a.pv.max_pages;
   int tbl = -1;
   if (g_begin < g_end && first_page + lane < a.pv.max_pages) tbl = table[first_page + lane];
+  const int64_t num_pages = a.pv.num_pages;
+  auto checked = [num_pages](int page) { return (page >= 0 && page < num_pages) ? page : -1; };
+  tbl = checked(tbl);
 
   W st;
 #pragma unroll
   for (int h = 0; h < G; ++h)
     st.qs[h].q.load(static_cast<const T*>(a.q) + ((int64_t)b * hq + g * G + h) * D, j);
   st.scale_log2 = a.scale_log2;
+  st.lane = lane;
   st.init();
 
   T* kpool = static_cast<T*>(a.k_pages);
@@ -296,27 +462,23 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   const int last = L - 1;
   const int64_t new_row = ((int64_t)b * heads + g) * D;
   // byte offset of this lane's first piece inside a group (consecutive rows)
-  const uint32_t lane_off = (uint32_t)((r * D + R::elem(0, j, 0)) * sizeof(T));
+  uint32_t lane_off = (uint32_t)((r * D + R::elem(0, j, 0)) * sizeof(T));
 
-  // the wave holding slot L-1 stores the newest token's K/V there
-  if (has_new && L > 0 && g_begin * kRows <= last && last < g_end * kRows && r == 0) {
-    const int64_t page = page_of(a.table, b, last, a.pv);
-    if (page >= 0) {
-      const int64_t off = page_row<D>(page, g, last & slot_mask, a.pv);
-      R kc, vc;
-      kc.load(static_cast<const T*>(a.k_new) + new_row, j);
-      vc.load(static_cast<const T*>(a.v_new) + new_row, j);
-      kc.store(kpool + off, j);
-      vc.store(vpool + off, j);
-    }
+  // lanes of row 0 of the wave whose range holds slot L-1 will store the new
+  // token's K/V; request it with the other prologue loads
+  const bool stores_new = has_new && L > 0 && g_begin * kRows <= last && last < g_end * kRows && r == 0;
+  R kn, vn;
+  if (stores_new) {
+    kn.load(static_cast<const T*>(a.k_new) + new_row, j);
+    vn.load(static_cast<const T*>(a.v_new) + new_row, j);
   }
 
   // page of group grp (wave-uniform), or -1 when the table entry is bad
   auto group_page = [&](int grp) -> int {
     const int pg = (grp * kRows) >> shift;
     const int idx = pg - first_page;
-    const int page = idx < 64 ? __builtin_amdgcn_readlane(tbl, idx) : table[min(pg, a.pv.max_pages - 1)];
-    return (page >= 0 && page < a.pv.num_pages) ? page : -1;
+    if (idx < 64) return __builtin_amdgcn_readlane(tbl, idx);  // checked when loaded
+    return checked(table[min(pg, a.pv.max_pages - 1)]);
   };
   auto group_base = [&](int page, int grp) -> int64_t {
     return ((((int64_t)page * heads + g) << shift) + ((grp * kRows) & slot_mask)) * D;
@@ -335,34 +497,21 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
       const int page = group_page(gs + u);
       ok = ok && page >= 0;
       const int64_t base = group_base(page >= 0 ? page : 0, gs + u) * (int64_t)sizeof(T);
+      // An empty asm that "redefines" the 32-bit lane offset in place, next
+      // to the loads, keeps the compiler from hoisting a 64-bit per-lane
+      // address out of the loop: the loads take the uniform-base +
+      // 32-bit-offset (saddr) form with no per-lane address arithmetic.
+      asm volatile("" : "+v"(lane_off));
       kc[u].stream(reinterpret_cast<const char*>(kpool) + base, lane_off);
       vc[u].stream(reinterpret_cast<const char*>(vpool) + base, lane_off);
     }
     return ok;
   };
 
-  R k0[U], v0[U], k1[U], v1[U];
-  bool all_ok = true;
-  if (nbatch > 0) all_ok = issue_full(g_begin, k0, v0);
-  for (int bi = 0; bi < nbatch; bi += 2) {
-    const int gs = g_begin + bi * U;
-    const bool more = bi + 1 < nbatch;
-    if (more) all_ok = issue_full(gs + U, k1, v1) && all_ok;
-    st.template consume<U, false>(k0, v0, nullptr);
-    if (more) {
-      if (bi + 2 < nbatch) all_ok = issue_full(gs + 2 * U, k0, v0) && all_ok;
-      st.template consume<U, false>(k1, v1, nullptr);
-    }
-  }
-  // A block-table entry out of range (a caller error) was read as page 0:
-  // drop what the unmasked path accumulated rather than mix in that page.
-  if (!all_ok) st.init();
-
-  // masked tail: the remaining groups of the range that hold keys < L
+  // Masked batch starting at group gs: keys >= L (and groups past the tail)
+  // are invalid; key L-1 comes from k_new when given.
   const int g_tail_end = min(g_end, (L + kRows - 1) / kRows);
-  for (int gs = g_begin + nbatch * U; gs < g_tail_end; gs += U) {
-    R kc[U], vc[U];
-    bool valid[U];
+  auto load_masked = [&](int gs, R* kc, R* vc, bool* valid) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int grp = gs + u;
@@ -393,7 +542,72 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
         vc[u].zero();
       }
     }
-    st.template consume<U, true>(kc, vc, valid);
+  };
+
+  // Software pipeline over the nbatch unmasked batches, kDepth buffers deep:
+  // while batch k is reduced, batches k+1 .. k+kDepth-1 are in flight.  The
+  // steady-state loop issues unconditionally (so the wait before each
+  // reduction covers only the batch being reduced); buffer indices are
+  // compile-time constants throughout, so the buffers stay in registers.
+  R kb[kDepth][U], vb[kDepth][U];
+  bool all_ok = true;
+  // The prologue loads (block-table entries, queries) are needed before the
+  // first batch anyway; waiting for them here once keeps the compiler from
+  // re-waiting on them, conservatively, at the head of every loop iteration.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+
+  // The wave holding slot L-1 stores the newest token's K/V there (loaded in
+  // the prologue); no load of this launch reads that slot from the cache (key
+  // L-1 comes from k_new), so the store can go out at once.
+  if (stores_new) {
+    const int page = group_page(last / kRows);
+    if (page >= 0) {
+      const int64_t off = group_base(page, last / kRows) + (int64_t)(last % kRows) * D;
+      kn.store(kpool + off, j);
+      vn.store(vpool + off, j);
+    }
+  }
+  // The masked tail (at most U groups: the leftover full groups of the
+  // batching plus the one group holding key L-1) is loaded now, beside the
+  // first full batch, so that its round trip is not added after the stream.
+  const int tail_begin = g_begin + nbatch * U;
+  R kt[U], vt[U];
+  bool tvalid[U];
+  load_masked(tail_begin, kt, vt, tvalid);
+#pragma unroll
+  for (int d = 0; d < kDepth - 1; ++d)
+    if (d < nbatch) all_ok = issue_full(g_begin + d * U, kb[d], vb[d]) && all_ok;
+  int bi = 0;
+  for (; bi + 2 * kDepth - 2 < nbatch; bi += kDepth) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      constexpr int kAhead = kDepth - 1;
+      all_ok = issue_full(g_begin + (bi + d + kAhead) * U, kb[(d + kAhead) % kDepth],
+                          vb[(d + kAhead) % kDepth]) && all_ok;
+      st.template consume<U, false>(kb[d], vb[d], nullptr);
+    }
+  }
+  // drain: fewer than 2 kDepth - 1 batches are left, the first kDepth - 1 of
+  // them already in flight
+#pragma unroll
+  for (int d = 0; d < 2 * kDepth - 2; ++d) {
+    if (bi + d < nbatch) {
+      if (bi + d + kDepth - 1 < nbatch)
+        all_ok = issue_full(g_begin + (bi + d + kDepth - 1) * U, kb[(d + kDepth - 1) % kDepth],
+                            vb[(d + kDepth - 1) % kDepth]) && all_ok;
+      st.template consume<U, false>(kb[d % kDepth], vb[d % kDepth], nullptr);
+    }
+  }
+  // A block-table entry out of range (a caller error) was read as page 0:
+  // drop what the unmasked path accumulated rather than mix in that page.
+  if (!all_ok) st.init();
+
+  // masked tail: its first batch was loaded up front; any further batches
+  // (none with the group accounting above, kept for safety) load here
+  st.template consume<U, true>(kt, vt, tvalid);
+  for (int gs = tail_begin + U; gs < g_tail_end; gs += U) {
+    load_masked(gs, kt, vt, tvalid);
+    st.template consume<U, true>(kt, vt, tvalid);
   }
 
   // the lane rows share the reference maxima: their states simply add up
@@ -413,38 +627,24 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
     }
   }
   __syncthreads();
-  // per-head merge weights of the waves, once
-  if (tid < G) {
-    const int h = tid;
+
+  // One thread per (head, element) merges the waves: each derives its head's
+  // weights from the waves' maxima itself, so one barrier suffices.
+  for (int idx = tid; idx < G * D; idx += NW * 64) {
+    const int h = idx / D, e = idx % D;
     float M = neg_inf();
 #pragma unroll
     for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][h]);
-    float den = 0.f;
+    float num = 0.f, den = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
       const float mw = s_m[w][h];
       const float f = (mw == neg_inf()) ? 0.f : fast_exp2(mw - M);
-      s_w[w][h] = f;
+      num += f * s_acc[w][h][e];
       den += f * s_l[w][h];
     }
-    s_den[h] = den;
-    if (a.num_splits > 1) {
-      const int64_t ws = ((int64_t)b * hq + g * G + h) * a.num_splits + split;
-      a.ws_ml[ws * 2] = M;
-      a.ws_ml[ws * 2 + 1] = den;
-    }
-  }
-  __syncthreads();
-
-  // one thread per (head, element)
-  for (int idx = tid; idx < G * D; idx += NW * 64) {
-    const int h = idx / D, e = idx % D;
-    float num = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) num += s_w[w][h] * s_acc[w][h][e];
     const int64_t row = (int64_t)b * hq + g * G + h;
     if (a.num_splits == 1) {
-      const float den = s_den[h];
       const float o = den > 0.f ? num / den : 0.f;
       if (sizeof(T) == 2)
         static_cast<bf16_bits*>(a.out)[row * D + e] = (bf16_bits)f32_to_bf16(o);
@@ -452,6 +652,11 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
         static_cast<float*>(a.out)[row * D + e] = o;
     } else {
       a.ws_o[(row * a.num_splits + split) * D + e] = num;
+      if (e == 0) {
+        const int64_t ws = row * a.num_splits + split;
+        a.ws_ml[ws * 2] = M;
+        a.ws_ml[ws * 2 + 1] = den;
+      }
     }
   }
 }
