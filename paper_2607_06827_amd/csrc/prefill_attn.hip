@@ -34,6 +34,8 @@
 // Blocks are remapped so that the eight XCDs each run a contiguous range of
 // (sequence, head, tile) items: tiles of one (b, g) share that XCD's L2 copy
 // of the compressed K/V.  Heavy tiles (late rows) are issued first.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace skv {
@@ -190,7 +192,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
   const int p = wrow0 + col;
   const bool qvalid = p < rows;
-  const int nvis = qvalid ? visible_keys(p, P, T_, nW, w, a.mask_mode) : 0;
+  const int nvis = qvalid ? min(visible_keys(p, P, T_, nW, w, a.mask_mode), clen) : 0;
   // keys every valid row of the wave sees (n_vis grows with the row)
   const int nvis_lo = wrow0 < rows ? min(visible_keys(wrow0, P, T_, nW, w, a.mask_mode), clen) : 0;
   const int hq = a.num_q_heads;
@@ -213,42 +215,62 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const T* vpool = static_cast<const T*>(a.v_pages);
   const int ntiles = (kmax + kKeys - 1) / kKeys;
 
-  // staging registers: keys (2 pair, 2 pair + 1) of chunk c, for K and V
-  uint4 rk[kItemsPerThread][2], rv[kItemsPerThread][2];
-  auto fetch = [&](int kt) {
+  // Staging pipeline, branch-free so that every wait covers exactly the loads
+  // it needs: the block-table entries of tile t are loaded at the start of
+  // tile t-3, the K/V rows of tile t at the start of tile t-2 (two register
+  // sets), and tile t is written to LDS at the end of tile t-1 (two LDS
+  // buffers).  Each thread owns staging items (key pair, 16-byte chunk);
+  // both keys of a pair share a page (page_size >= 8).  Tiles past the last
+  // one load clamped, in-range addresses and are never read.
+  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
+  const int64_t num_pages = a.pv.num_pages;
+  const int shift = a.pv.page_shift;
+  int pg[2][kItemsPerThread];  // table entries, by tile parity
+  uint4 rk[2][kItemsPerThread][2], rv[2][kItemsPerThread][2];  // by tile parity
+  uint32_t okm[2][kItemsPerThread];  // bit r: key 2 pair + r valid
+  auto item_key = [&](int kt, int it) {
+    const int idx = tid + it * kThreads;
+    return kt * kKeys + 2 * (idx % (kKeys / 2));
+  };
+  auto table_load = [&](int kt, int* pgs) {
+#pragma unroll
+    for (int it = 0; it < kItemsPerThread; ++it)
+      pgs[it] = table_row[min(item_key(kt, it) >> shift, a.pv.max_pages - 1)];
+  };
+  auto fetch = [&](int kt, const int* pgs, uint4 (*rks)[2], uint4 (*rvs)[2], uint32_t* oks) {
 #pragma unroll
     for (int it = 0; it < kItemsPerThread; ++it) {
       const int idx = tid + it * kThreads;
-      const int pair = idx % (kKeys / 2), ch = idx / (kKeys / 2);
-      const int key = kt * kKeys + 2 * pair;  // both keys of a pair share a page
-      int64_t page = -1;
-      if (idx < kItems && key < kmax) page = page_of(a.table, b, key, a.pv);
-      rk[it][0] = rk[it][1] = rv[it][0] = rv[it][1] = make_uint4(0, 0, 0, 0);
-      if (page >= 0) {
-        const T* kp = kpool + page_row<D>(page, g, key & slot_mask, a.pv) + ch * kElems16;
-        const T* vp = vpool + (kp - kpool);
-        rk[it][0] = *reinterpret_cast<const uint4*>(kp);
-        rv[it][0] = *reinterpret_cast<const uint4*>(vp);
-        if (key + 1 < kmax) {
-          rk[it][1] = *reinterpret_cast<const uint4*>(kp + D);
-          rv[it][1] = *reinterpret_cast<const uint4*>(vp + D);
-        }
-      }
+      const int ch = (idx / (kKeys / 2)) % kChunksPerRow;
+      const int key = item_key(kt, it);
+      const int page = pgs[it];
+      const bool ok = key < kmax && page >= 0 && page < num_pages;
+      oks[it] = (ok ? 1u : 0u) | (ok && key + 1 < kmax ? 2u : 0u);
+      const T* kp = kpool + page_row<D>(ok ? page : 0, g, key & slot_mask, a.pv) + ch * kElems16;
+      const T* vp = vpool + (kp - kpool);
+      rks[it][0] = *reinterpret_cast<const uint4*>(kp);
+      rvs[it][0] = *reinterpret_cast<const uint4*>(vp);
+      rks[it][1] = *reinterpret_cast<const uint4*>(kp + D);
+      rvs[it][1] = *reinterpret_cast<const uint4*>(vp + D);
     }
   };
-  auto stage = [&](int buf) {
+  auto stage = [&](int buf, const uint4 (*rks)[2], const uint4 (*rvs)[2], const uint32_t* oks) {
     T* sk = s_buf + buf * (kTileK + kTileV);
     T* sv = sk + kTileK;
+    const uint4 z = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int it = 0; it < kItemsPerThread; ++it) {
       const int idx = tid + it * kThreads;
       if (idx >= kItems) continue;
       const int pair = idx % (kKeys / 2), ch = idx / (kKeys / 2);
-#pragma unroll
-      for (int rr = 0; rr < 2; ++rr)
-        *reinterpret_cast<uint4*>(&sk[(2 * pair + rr) * kRowK + ch * kElems16]) = rk[it][rr];
-      const uint32_t w0[4] = {rv[it][0].x, rv[it][0].y, rv[it][0].z, rv[it][0].w};
-      const uint32_t w1[4] = {rv[it][1].x, rv[it][1].y, rv[it][1].z, rv[it][1].w};
+      // rows of keys past the visible range (or of a bad table entry) are
+      // zero: their V would otherwise meet a zero weight as 0 * garbage
+      const uint4 k0 = (oks[it] & 1u) ? rks[it][0] : z, k1 = (oks[it] & 2u) ? rks[it][1] : z;
+      const uint4 v0 = (oks[it] & 1u) ? rvs[it][0] : z, v1 = (oks[it] & 2u) ? rvs[it][1] : z;
+      *reinterpret_cast<uint4*>(&sk[(2 * pair) * kRowK + ch * kElems16]) = k0;
+      *reinterpret_cast<uint4*>(&sk[(2 * pair + 1) * kRowK + ch * kElems16]) = k1;
+      const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
+      const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
       if (sizeof(T) == 2) {
         // element e of a chunk is half e%2 of word e/2; keys (2 pair, 2 pair+1)
         // of one element form one 32-bit LDS word of V^T
@@ -266,73 +288,88 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
     }
   };
 
-  if (ntiles > 0) {
-    fetch(0);
-    stage(0);
-  }
+  // prologue: tables of tiles 0..2, K/V of tiles 0 and 1, tile 0 into LDS
+  table_load(0, pg[0]);
+  table_load(1, pg[1]);
+  fetch(0, pg[0], rk[0], rv[0], okm[0]);
+  table_load(2, pg[0]);
+  fetch(1, pg[1], rk[1], rv[1], okm[1]);
+  stage(0, rk[0], rv[0], okm[0]);
   __syncthreads();
-  for (int kt = 0; kt < ntiles; ++kt) {
+
+  // one tile of the steady state; kPar = kt & 1 (compile-time register sets)
+  auto tile_step = [&](int kt, auto par) {
+    constexpr int kPar = decltype(par)::value;
+    constexpr int kOther = 1 - kPar;
+    table_load(kt + 3, pg[kOther]);                          // tile kt+3: parity of kt+1
+    fetch(kt + 2, pg[kPar], rk[kPar], rv[kPar], okm[kPar]);  // tile kt+2: parity of kt
     const int kb = kt * kKeys;
-    if (kt + 1 < ntiles) fetch(kt + 1);  // in flight during this tile
-    const T* sk = s_buf + (kt & 1) * (kTileK + kTileV);
+    const T* sk = s_buf + kPar * (kTileK + kTileV);
     const T* sv = sk + kTileK;
+    if (kt < ntiles) {  // (the loop runs an even number of steps)
+      // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
+      f32x16_t st;
+  #pragma unroll
+      for (int i = 0; i < 16; ++i) st[i] = 0.f;
+      const T* krow = &sk[col * kRowK + hg * kPack];
+  #pragma unroll
+      for (int kc = 0; kc < kQChunks; ++kc) st = M::mma(M::load(krow + kc * kStep), qf[kc], st);
 
-    // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
-    f32x16_t st;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) st[i] = 0.f;
-    const T* krow = &sk[col * kRowK + hg * kPack];
-#pragma unroll
-    for (int kc = 0; kc < kQChunks; ++kc) st = M::mma(M::load(krow + kc * kStep), qf[kc], st);
-
-    float pr[16];
-    float mt = neg_inf();
-    const bool masked = kb + kKeys > nvis_lo;  // uniform over the wave
-    if (masked) {
-#pragma unroll
+      float pr[16];
+      float mt = neg_inf();
+      const bool masked = kb + kKeys > nvis_lo;  // uniform over the wave
+      if (masked) {
+  #pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
+          pr[i] = key < nvis ? st[i] : neg_inf();
+          mt = fmaxf(mt, pr[i]);
+        }
+      } else {
+  #pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pr[i] = st[i];
+          mt = fmaxf(mt, pr[i]);
+        }
+      }
+      mt = partner_max(mt) * a.scale_log2;  // the scale is > 0
+      if (mt > m_run + kSlack) {
+        const float corr = fast_exp2(m_run - mt);
+        l_run *= corr;
+  #pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+        m_run = mt;
+      }
+      float sum = 0.f;
+  #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
-        pr[i] = key < nvis ? st[i] : neg_inf();
-        mt = fmaxf(mt, pr[i]);
+        pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_run));
+        if (masked) pr[i] = m_run == neg_inf() ? 0.f : pr[i];  // nothing visible yet
+        sum += pr[i];
       }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        pr[i] = st[i];
-        mt = fmaxf(mt, pr[i]);
-      }
-    }
-    mt = partner_max(mt) * a.scale_log2;  // the scale is > 0
-    if (mt > m_run + kSlack) {
-      const float corr = fast_exp2(m_run - mt);
-      l_run *= corr;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) o[db][i] *= corr;
-      m_run = mt;
-    }
-    float sum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_run));
-      if (masked) pr[i] = m_run == neg_inf() ? 0.f : pr[i];  // nothing visible yet
-      sum += pr[i];
-    }
-    l_run += sum;
+      l_run += sum;
 
-    // O^T += V^T P^T over the 32 keys of the tile
-#pragma unroll
-    for (int kk = 0; kk < kKeys / kStep; ++kk) {
-      const Frag pf = M::pack_p(pr + kk * kPack);
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        const Frag vf = M::load_vt(&sv[(db * 32 + col) * kRowV], kk, hg);
-        o[db] = M::mma(vf, pf, o[db]);
+      // O^T += V^T P^T over the 32 keys of the tile
+  #pragma unroll
+      for (int kk = 0; kk < kKeys / kStep; ++kk) {
+        const Frag pf = M::pack_p(pr + kk * kPack);
+  #pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const Frag vf = M::load_vt(&sv[(db * 32 + col) * kRowV], kk, hg);
+          o[db] = M::mma(vf, pf, o[db]);
+        }
       }
     }
-    if (kt + 1 < ntiles) stage((kt + 1) & 1);
+    stage(kOther, rk[kOther], rv[kOther], okm[kOther]);  // tile kt+1 (never read past the end)
     __syncthreads();
+  };
+  // two steps per iteration so that the register sets are compile-time; the
+  // loads and stores of a step past the last tile are harmless
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    tile_step(kt, std::integral_constant<int, 0>());
+    tile_step(kt + 1, std::integral_constant<int, 1>());
   }
 
   const float l_tot = partner_sum(l_run);
