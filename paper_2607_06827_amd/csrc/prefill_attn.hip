@@ -198,11 +198,6 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const int hq = a.num_q_heads;
   const int slot_mask = (1 << a.pv.page_shift) - 1;
 
-  // this lane's query row, as the B operand of S^T = K Q^T
-  Frag qf[kQChunks];
-  const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + p) * hq + h) * D;
-#pragma unroll
-  for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = qvalid ? M::load(qrow + kc * kStep + hg * kPack) : M::zero();
 
   f32x16_t o[D / 32];
 #pragma unroll
@@ -288,14 +283,28 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
     }
   };
 
-  // prologue: tables of tiles 0..2, K/V of tiles 0 and 1, tile 0 into LDS
+  // prologue: tables of tiles 0..2, K/V of tiles 0 and 1, then this lane's
+  // query row (the B operand of S^T = K Q^T), then tile 0 into LDS.  The
+  // memory counter is in order: issued after the first fetches, the query
+  // loads arrive while tile 0 is in flight instead of delaying it.
   table_load(0, pg[0]);
   table_load(1, pg[1]);
   fetch(0, pg[0], rk[0], rv[0], okm[0]);
   table_load(2, pg[0]);
   fetch(1, pg[1], rk[1], rv[1], okm[1]);
+  // (rows past the end read row 0 of the sequence: finite, never stored)
+  __builtin_amdgcn_sched_barrier(0);  // keep this issue order
+  Frag qf[kQChunks];
+  const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + (qvalid ? p : 0)) * hq + h) * D;
+#pragma unroll
+  for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = M::load(qrow + kc * kStep + hg * kPack);
+  __builtin_amdgcn_sched_barrier(0);
   stage(0, rk[0], rv[0], okm[0]);
   __syncthreads();
+  // tile 0 needs the queries, and every load of the prologue was issued
+  // before them; one wait here leaves nothing of the prologue pending at the
+  // loop head, where it would make every iteration's waits conservative
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 
   // one tile of the steady state; kPar = kt & 1 (compile-time register sets)
   auto tile_step = [&](int kt, auto par) {
