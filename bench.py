@@ -14,9 +14,14 @@ full resolution) is measured beside it.
 
 Also reported: the decode kernel's achieved HBM bandwidth against the 8 TB/s
 peak (algorithmic bytes: every cached K/V row once, plus q, the new K/V and
-the output), and the fp64 CPU oracle timed on a bounded sample of the same job.
+the output); the pooling kernel's achieved HBM bandwidth (raw K/V read once,
+cache rows written once) and the prefill attention's achieved bf16 TFLOP/s
+against the 2.5 PFLOP/s dense MFMA peak (FLOPs of the visible (row, key) pairs
+only), each from a graph of that kernel alone; and the fp64 CPU oracle timed
+on a bounded sample of the same job.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-full]
+    python bench.py --traffic [--workload NAME]   # eager launches for counter runs
 """
 from __future__ import annotations
 
@@ -32,6 +37,7 @@ if ROOT not in sys.path:
 
 METRIC = "decode-attn achieved HBM GB/s & tokens/s/GPU, 60s audio b=64, pooled vs full KV"
 HBM_PEAK_GBPS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
 
 
 def log(msg):
@@ -104,13 +110,20 @@ def measure(job, steps, warmup, label):
     g_step = capture(job.run)
     g_dec = capture(lambda: [job.run_decode_step(s) for s in range(job.wl.decode_steps)])
     g_pre = capture(job.run_prefill)
+    g_pool = capture(job.run_pool)
+    g_attn = capture(job.run_prefill_attn)
     for _ in range(warmup):
         g_step.replay()
     ms_step = time_graph(g_step, steps)
     ms_dec = time_graph(g_dec, max(2, steps))
     ms_pre = time_graph(g_pre, max(2, steps))
+    ms_pool = time_graph(g_pool, max(2, steps))
+    ms_attn = time_graph(g_attn, max(2, steps))
     dec_bytes, launches = decode_launch_stats(job)
     wl = job.wl
+    nl = len(job.layers)
+    pool_bytes = sum(job.pool_bytes_layer(i) for i in range(nl))
+    attn_flops = sum(job.prefill_flops_layer(i) for i in range(nl))
     res = {
         "ms_per_step": ms_step,
         "tokens_per_s": wl.batch * wl.decode_steps / (ms_step * 1e-3),
@@ -120,10 +133,21 @@ def measure(job, steps, warmup, label):
         "decode_bytes_per_step": dec_bytes,
         "decode_launches": launches,
         "prefill_ms": ms_pre,
+        "pool": {"avg_launch_us": ms_pool / nl * 1e3,
+                 "achieved_gbps": pool_bytes / (ms_pool * 1e-3) / 1e9,
+                 "bytes_per_launch": pool_bytes / nl},
+        "prefill_attn": {"avg_launch_us": ms_attn / nl * 1e3,
+                         "achieved_tflops": attn_flops / (ms_attn * 1e-3) / 1e12,
+                         "flops_per_launch": attn_flops / nl},
     }
+    res["pool"]["frac_of_hbm_peak"] = res["pool"]["achieved_gbps"] / HBM_PEAK_GBPS
+    res["prefill_attn"]["frac_of_bf16_mfma_peak"] = (res["prefill_attn"]["achieved_tflops"]
+                                                     / BF16_MFMA_PEAK_TFLOPS)
     log(f"{label}: step {ms_step:.3f} ms, decode {ms_dec:.3f} ms "
-        f"({res['decode_gbps']:.0f} GB/s), prefill+pool {ms_pre:.3f} ms")
-    del g_step, g_dec, g_pre
+        f"({res['decode_gbps']:.0f} GB/s), prefill+pool {ms_pre:.3f} ms "
+        f"(pool {ms_pool:.3f} ms, {res['pool']['achieved_gbps']:.0f} GB/s; "
+        f"attention {ms_attn:.3f} ms, {res['prefill_attn']['achieved_tflops']:.0f} TFLOP/s)")
+    del g_step, g_dec, g_pre, g_pool, g_attn
     return res
 
 
@@ -177,8 +201,10 @@ def main():
     ap.add_argument("--no-full", action="store_true", help="skip the uncompressed run")
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--traffic", action="store_true",
-                    help="counter-collection run: two decode steps of the job launched eagerly, "
+                    help="counter-collection run: the job's launches issued eagerly once, "
                          "then a plain 1 GiB device copy that calibrates the byte counters")
+    ap.add_argument("--workload", default=None,
+                    help="with --traffic: run this workload (by name) instead of the benchmark's")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the decode, "
@@ -191,6 +217,15 @@ def main():
     from paper_2607_06827_amd.workload import Job
 
     wl = inputs.STACK_60S
+    if args.workload:
+        if not args.traffic:
+            print("--workload applies to --traffic runs only", file=sys.stderr)
+            sys.exit(2)
+        named = {x.name: x for x in inputs.WORKLOADS}
+        if args.workload not in named:
+            print(f"unknown workload {args.workload}; one of {sorted(named)}", file=sys.stderr)
+            sys.exit(2)
+        wl = named[args.workload]
     torch.cuda.set_device(0)
     log(f"building {wl.name} on {torch.cuda.get_device_name(0)}")
     t0 = time.perf_counter()
@@ -204,8 +239,12 @@ def main():
         dst.copy_(src)  # 1 GiB read + 1 GiB written by one copy kernel
         torch.cuda.synchronize()
         dec_bytes, launches = decode_launch_stats(job)
-        print(json.dumps({"traffic_run": True, "copy_bytes": 1 << 30,
-                          "decode_bytes_per_launch": dec_bytes / launches, "decode_launches": launches}))
+        nl = len(job.layers)
+        print(json.dumps({"traffic_run": True, "workload": wl.name, "copy_bytes": 1 << 30,
+                          "decode_bytes_per_launch": dec_bytes / max(launches, 1), "decode_launches": launches,
+                          "pool_bytes_per_launch": sum(job.pool_bytes_layer(i) for i in range(nl)) / nl,
+                          "prefill_flops_per_launch": sum(job.prefill_flops_layer(i) for i in range(nl)) / nl,
+                          "layers": nl}))
         return
     pooled = measure(job, args.steps, args.warmup, "pooled (l0=14, w=4)")
 
@@ -246,6 +285,8 @@ def main():
         "decode": {"pooled_tokens_per_s": pooled["decode_tokens_per_s"],
                    "pooled_gbps": pooled["decode_gbps"], "pooled_ms_per_step": pooled["decode_ms"]},
         "prefill_ms": pooled["prefill_ms"],
+        "pool": pooled["pool"],
+        "prefill_attn": pooled["prefill_attn"],
     }
     if full:
         result["full_kv"] = {"tokens_per_s": full["tokens_per_s"], "ms_per_step": full["ms_per_step"],

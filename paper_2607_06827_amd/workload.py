@@ -20,6 +20,20 @@ from .speechkv import (PagedKV, Spans, speechkv_compressed_len, speechkv_decode_
                        speechkv_pool_kv, speechkv_prefill_attn)
 
 
+def visible_pairs(P: int, T: int, N: int, w: int) -> int:
+    """Sum over the P + T + N full-resolution rows of the number of compressed
+    keys each row may attend to, under the causal mask over compressed
+    positions (Sec. III-B, Eq. 5) with a pooled window visible from its last
+    frame: prefix row p sees p + 1 keys, speech frame t sees the prefix and the
+    windows that end at or before it, text row m after the speech sees all
+    of those plus the text up to itself.  Used to count algorithmic FLOPs."""
+    nW = -(-T // w)
+    total = P * (P + 1) // 2
+    total += sum((P + nW) if t == T - 1 else (P + (t + 1) // w) for t in range(T))
+    total += sum(P + nW + m + 1 for m in range(N))
+    return total
+
+
 class Job:
     """All buffers of one workload on one device.
 
@@ -117,6 +131,20 @@ class Job:
                 speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.w, l,
                                       self.l0, self.prefill_out, scale=self.scale, stream=stream)
 
+    def run_pool(self, stream=None):
+        """Pooling of every layer (writes the caches)."""
+        wl = self.wl
+        for i, l in enumerate(self.layers):
+            speechkv_pool_kv(self.k_raw[i], self.v_raw[i], self.spans, wl.w, self.gate[i], l,
+                             self.l0, self.caches[i], self.cache_len_out[i], stream=stream)
+
+    def run_prefill_attn(self, stream=None):
+        """Prefill attention of every layer over caches already pooled."""
+        wl = self.wl
+        for i, l in enumerate(self.layers):
+            speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.w, l,
+                                  self.l0, self.prefill_out, scale=self.scale, stream=stream)
+
     def decode_out_at(self, i: int, step: int) -> torch.Tensor:
         return self.decode_out[i * self.wl.decode_steps + step if self.keep_decode else 0]
 
@@ -152,3 +180,25 @@ class Job:
     def decode_bytes(self, step: int) -> int:
         """Algorithmic HBM bytes of one decode step over all layers."""
         return sum(self.decode_bytes_layer(i, step) for i in range(len(self.layers)))
+
+    def pool_bytes_layer(self, i: int) -> int:
+        """Algorithmic HBM bytes of one pooling launch (layer index i): every
+        raw K and V row read once, every cache row written once (pooled
+        windows and copied text alike), the gate vectors read."""
+        wl = self.wl
+        e = 2 if wl.dtype == "bf16" else 4
+        row = wl.num_kv_heads * wl.head_dim * e
+        return wl.batch * 2 * row * (wl.prefill_len + self.prefill_clen[i]) + row
+
+    def prefill_visible_pairs(self, i: int) -> int:
+        """(row, visible key) pairs of one sequence's prefill at layer index i."""
+        wl = self.wl
+        w = wl.w if self.layers[i] >= self.l0 else 1
+        return visible_pairs(wl.prefix_len, wl.speech_len, wl.suffix_len, w)
+
+    def prefill_flops_layer(self, i: int) -> int:
+        """Algorithmic FLOPs of one prefill attention launch: q.k and p.v for
+        every (row, visible key) pair of every query head, 2 FLOPs per
+        multiply-add (the masked-out pairs are not counted)."""
+        wl = self.wl
+        return 4 * wl.batch * wl.num_q_heads * wl.head_dim * self.prefill_visible_pairs(i)
