@@ -124,6 +124,7 @@ def measure(job, steps, warmup, label):
     nl = len(job.layers)
     pool_bytes = sum(job.pool_bytes_layer(i) for i in range(nl))
     attn_flops = sum(job.prefill_flops_layer(i) for i in range(nl))
+    attn_bytes = sum(job.prefill_bytes_layer(i) for i in range(nl))
     res = {
         "ms_per_step": ms_step,
         "tokens_per_s": wl.batch * wl.decode_steps / (ms_step * 1e-3),
@@ -143,6 +144,10 @@ def measure(job, steps, warmup, label):
     res["pool"]["frac_of_hbm_peak"] = res["pool"]["achieved_gbps"] / HBM_PEAK_GBPS
     res["prefill_attn"]["frac_of_bf16_mfma_peak"] = (res["prefill_attn"]["achieved_tflops"]
                                                      / BF16_MFMA_PEAK_TFLOPS)
+    # roofline fraction: the larger of the MFMA and HBM floors over the measured time
+    t_floor = max(attn_flops / (BF16_MFMA_PEAK_TFLOPS * 1e12), attn_bytes / (HBM_PEAK_GBPS * 1e9))
+    res["prefill_attn"]["bytes_per_launch"] = attn_bytes / nl
+    res["prefill_attn"]["roofline_frac"] = t_floor / (ms_attn * 1e-3)
     log(f"{label}: step {ms_step:.3f} ms, decode {ms_dec:.3f} ms "
         f"({res['decode_gbps']:.0f} GB/s), prefill+pool {ms_pre:.3f} ms "
         f"(pool {ms_pool:.3f} ms, {res['pool']['achieved_gbps']:.0f} GB/s; "

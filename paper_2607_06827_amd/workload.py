@@ -196,6 +196,15 @@ class Job:
         w = wl.w if self.layers[i] >= self.l0 else 1
         return visible_pairs(wl.prefix_len, wl.speech_len, wl.suffix_len, w)
 
+    def prefill_bytes_layer(self, i: int) -> int:
+        """Algorithmic HBM bytes of one prefill attention launch: Q read and O
+        written once, the compressed K and V read once."""
+        wl = self.wl
+        e = 2 if wl.dtype == "bf16" else 4
+        q = wl.batch * wl.prefill_len * wl.num_q_heads * wl.head_dim * e
+        kv = wl.batch * self.prefill_clen[i] * wl.num_kv_heads * wl.head_dim * e
+        return 2 * q + 2 * kv
+
     def prefill_flops_layer(self, i: int) -> int:
         """Algorithmic FLOPs of one prefill attention launch: q.k and p.v for
         every (row, visible key) pair of every query head, 2 FLOPs per
