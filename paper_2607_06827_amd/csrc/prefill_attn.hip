@@ -20,16 +20,18 @@
 // permlane swap, rescaling only when the max grows by more than 2^8), and the
 // probabilities already sit in the B-operand layout of
 //     O^T += V^T P^T          (A = V^T tile from LDS, B = P^T)
-// with the key order of the C layout carried into the V^T reads.  bf16 uses
+// with the key order of the C layout carried into the V reads.  bf16 uses
 // v_mfma_f32_32x32x16_bf16 (8 elements per lane per operand), fp32 uses
 // v_mfma_f32_32x32x2_f32 (1 element), both accumulating in fp32.
 //
-// K/V tiles are double-buffered in LDS: the next tile's global loads are in
-// flight while the current one is multiplied, and one barrier per tile
-// separates the phases.  V is transposed while it is staged; the V^T row
-// stride (18 words) and the key-pair-fastest lane order put the 64 lanes of a
-// staging store, and the 32 lanes of an operand read, on distinct banks.  The
-// output tile goes back through LDS so that rows leave as 16-byte stores.
+// K and V tiles are both staged row-major in LDS, double-buffered, behind a
+// branch-free pipeline: block-table entries three tiles ahead, K/V rows two
+// tiles ahead (whole 256-byte rows per wave-wide load), LDS one tile ahead,
+// one barrier per tile.  The bf16 V^T operand comes from the row-major V
+// tile through the gfx950 LDS transpose read (ds_read_b64_tr_b16), so no
+// register transpose is needed at staging; row strides put every staging
+// write and operand read on distinct banks.  The output tile goes back
+// through LDS so that rows leave as 16-byte stores.
 //
 // Blocks are remapped so that the eight XCDs each run a contiguous range of
 // (sequence, head, tile) items: tiles of one (b, g) share that XCD's L2 copy
@@ -57,10 +59,13 @@ constexpr float kSlack = 8.f;
 template <typename T>
 struct Mfma;
 
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t* lds_s16x4_ptr;
+
 template <>
 struct Mfma<bf16_bits> {
-  static constexpr int kPack = 8;   // elements per lane per operand
-  static constexpr int kRowV = 36;  // V^T row stride in elements (18 words)
+  static constexpr int kPack = 8;    // elements per lane per operand
+  static constexpr int kRowV = 160;  // V row stride in elements (80 words = 16 mod 64 banks)
   typedef bf16x8_t Frag;
   static __device__ __forceinline__ f32x16_t mma(Frag a, Frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -69,11 +74,21 @@ struct Mfma<bf16_bits> {
     return __builtin_bit_cast(Frag, *reinterpret_cast<const u16x8_t*>(p));
   }
   static __device__ __forceinline__ Frag zero() { return __builtin_bit_cast(Frag, u16x8_t{0, 0, 0, 0, 0, 0, 0, 0}); }
-  // keys 8*(i/4) + 4*hg + (i%4) for i = 8kk .. 8kk+7: two runs of four
-  static __device__ __forceinline__ Frag load_vt(const bf16_bits* row, int kk, int hg) {
-    u16x4_t lo = *reinterpret_cast<const u16x4_t*>(row + 16 * kk + 4 * hg);
-    u16x4_t hi = *reinterpret_cast<const u16x4_t*>(row + 16 * kk + 8 + 4 * hg);
-    u16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  // A operand of O^T += V^T P^T for keys 16kk.. and head-dim block db, read
+  // from the row-major V tile with the gfx950 LDS transpose read.  In MFMA
+  // order lane (m = lane%32, h = lane/32) needs column m's keys 16kk + 4h +
+  // {0..3} and 16kk + 8 + 4h + {0..3} (the key order of the S^T C layout).
+  // ds_read_b64_tr_b16 gives lane i of a 16-lane group element (row 4r +
+  // i/4, column i%4) of the 16 x 4 block its lanes point at, so lane j of
+  // group g points at key 16kk + 4(g/2) + j/4 (+8 for the second read),
+  // elements 32db + 16(g%2) + 4(j%4) .. +3.
+  static __device__ __forceinline__ Frag load_v(const bf16_bits* sv, int kk, int db, int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const bf16_bits* p = sv + (16 * kk + 4 * (g >> 1) + (j >> 2)) * kRowV + 32 * db + 16 * (g & 1) + 4 * (j & 3);
+    const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)p);
+    const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(p + 8 * kRowV));
+    const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
+                       (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
     return __builtin_bit_cast(Frag, v);
   }
   // round-to-nearest-even pack of 8 probabilities (v_cvt_pk_bf16_f32)
@@ -93,16 +108,19 @@ struct Mfma<bf16_bits> {
 template <>
 struct Mfma<float> {
   static constexpr int kPack = 1;
-  static constexpr int kRowV = 40;
+  static constexpr int kRowV = 160;  // V row stride in elements (160 words = 32 mod 64 banks)
   typedef float Frag;
   static __device__ __forceinline__ f32x16_t mma(Frag a, Frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ Frag load(const float* p) { return *p; }
   static __device__ __forceinline__ Frag zero() { return 0.f; }
-  // key 8*(kk/4) + 4*hg + (kk%4)
-  static __device__ __forceinline__ Frag load_vt(const float* row, int kk, int hg) {
-    return row[8 * (kk / 4) + 4 * hg + (kk % 4)];
+  // A operand of O^T += V^T P^T: lane (m = lane%32, hg = lane/32) takes key
+  // 8*(kk/4) + 4*hg + (kk%4) (the key order of the S^T C layout), column m
+  // of head-dim block db, from the row-major V tile
+  static __device__ __forceinline__ Frag load_v(const float* sv, int kk, int db, int lane) {
+    const int hg = lane >> 5, m = lane & 31;
+    return sv[(8 * (kk / 4) + 4 * hg + (kk % 4)) * kRowV + 32 * db + m];
   }
   static __device__ __forceinline__ Frag pack_p(const float* p) { return p[0]; }
   static __device__ __forceinline__ void store4(float* dst, float a, float b, float c, float d) {
@@ -156,9 +174,9 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   constexpr int kChunksPerRow = D / kElems16;
   constexpr int kRowK = D + kElems16;             // padded K row (elements)
   constexpr int kRowV = M::kRowV;                 // padded V^T row (elements)
-  constexpr int kItems = (kKeys / 2) * kChunksPerRow;  // staging work: (key pair, chunk)
+  constexpr int kItems = kKeys * kChunksPerRow;  // staging work: (key, 16-byte chunk)
   constexpr int kItemsPerThread = (kItems + kThreads - 1) / kThreads;
-  constexpr int kTileK = kKeys * kRowK, kTileV = D * kRowV;
+  constexpr int kTileK = kKeys * kRowK, kTileV = kKeys * kRowV;
   constexpr int kRowO = D + kElems16;             // padded output row (elements)
   constexpr float kLn2 = 0.6931471805599453f;
   // the output tiles of all waves go through the staging buffers when they fit
@@ -214,72 +232,50 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   // it needs: the block-table entries of tile t are loaded at the start of
   // tile t-3, the K/V rows of tile t at the start of tile t-2 (two register
   // sets), and tile t is written to LDS at the end of tile t-1 (two LDS
-  // buffers).  Each thread owns staging items (key pair, 16-byte chunk);
-  // both keys of a pair share a page (page_size >= 8).  Tiles past the last
-  // one load clamped, in-range addresses and are never read.
+  // buffers).  Each thread owns staging items (key, 16-byte chunk), chunks
+  // fastest, so each wave-wide load reads whole rows and each LDS row write
+  // covers all banks once.  K and V are both staged row-major.  Tiles past
+  // the last one load clamped, in-range addresses and are never read.
   const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
   const int64_t num_pages = a.pv.num_pages;
   const int shift = a.pv.page_shift;
   int pg[2][kItemsPerThread];  // table entries, by tile parity
-  uint4 rk[2][kItemsPerThread][2], rv[2][kItemsPerThread][2];  // by tile parity
-  uint32_t okm[2][kItemsPerThread];  // bit r: key 2 pair + r valid
-  auto item_key = [&](int kt, int it) {
-    const int idx = tid + it * kThreads;
-    return kt * kKeys + 2 * (idx % (kKeys / 2));
-  };
+  uint4 rk[2][kItemsPerThread], rv[2][kItemsPerThread];  // by tile parity
+  uint32_t okm[2];  // bit it: item it holds a valid key
+  auto item_key = [&](int it) { return (tid + it * kThreads) / kChunksPerRow; };  // key within the tile
+  auto item_chunk = [&](int it) { return (tid + it * kThreads) % kChunksPerRow; };
   auto table_load = [&](int kt, int* pgs) {
 #pragma unroll
     for (int it = 0; it < kItemsPerThread; ++it)
-      pgs[it] = table_row[min(item_key(kt, it) >> shift, a.pv.max_pages - 1)];
+      pgs[it] = table_row[min((kt * kKeys + item_key(it)) >> shift, a.pv.max_pages - 1)];
   };
-  auto fetch = [&](int kt, const int* pgs, uint4 (*rks)[2], uint4 (*rvs)[2], uint32_t* oks) {
+  auto fetch = [&](int kt, const int* pgs, uint4* rks, uint4* rvs, uint32_t& oks) {
+    oks = 0;
 #pragma unroll
     for (int it = 0; it < kItemsPerThread; ++it) {
-      const int idx = tid + it * kThreads;
-      const int ch = (idx / (kKeys / 2)) % kChunksPerRow;
-      const int key = item_key(kt, it);
+      const int key = kt * kKeys + item_key(it);
       const int page = pgs[it];
       const bool ok = key < kmax && page >= 0 && page < num_pages;
-      oks[it] = (ok ? 1u : 0u) | (ok && key + 1 < kmax ? 2u : 0u);
-      const T* kp = kpool + page_row<D>(ok ? page : 0, g, key & slot_mask, a.pv) + ch * kElems16;
-      const T* vp = vpool + (kp - kpool);
-      rks[it][0] = *reinterpret_cast<const uint4*>(kp);
-      rvs[it][0] = *reinterpret_cast<const uint4*>(vp);
-      rks[it][1] = *reinterpret_cast<const uint4*>(kp + D);
-      rvs[it][1] = *reinterpret_cast<const uint4*>(vp + D);
+      oks |= ok ? 1u << it : 0u;
+      const int64_t off = page_row<D>(ok ? page : 0, g, key & slot_mask, a.pv) + item_chunk(it) * kElems16;
+      rks[it] = *reinterpret_cast<const uint4*>(kpool + off);
+      rvs[it] = *reinterpret_cast<const uint4*>(vpool + off);
     }
   };
-  auto stage = [&](int buf, const uint4 (*rks)[2], const uint4 (*rvs)[2], const uint32_t* oks) {
+  auto stage = [&](int buf, const uint4* rks, const uint4* rvs, uint32_t oks) {
     T* sk = s_buf + buf * (kTileK + kTileV);
     T* sv = sk + kTileK;
-    const uint4 z = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int it = 0; it < kItemsPerThread; ++it) {
-      const int idx = tid + it * kThreads;
-      if (idx >= kItems) continue;
-      const int pair = idx % (kKeys / 2), ch = idx / (kKeys / 2);
+      if (tid + it * kThreads >= kItems) continue;
+      const int key = item_key(it), ch = item_chunk(it);
       // rows of keys past the visible range (or of a bad table entry) are
       // zero: their V would otherwise meet a zero weight as 0 * garbage
-      const uint4 k0 = (oks[it] & 1u) ? rks[it][0] : z, k1 = (oks[it] & 2u) ? rks[it][1] : z;
-      const uint4 v0 = (oks[it] & 1u) ? rvs[it][0] : z, v1 = (oks[it] & 2u) ? rvs[it][1] : z;
-      *reinterpret_cast<uint4*>(&sk[(2 * pair) * kRowK + ch * kElems16]) = k0;
-      *reinterpret_cast<uint4*>(&sk[(2 * pair + 1) * kRowK + ch * kElems16]) = k1;
-      const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
-      const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
-      if (sizeof(T) == 2) {
-        // element e of a chunk is half e%2 of word e/2; keys (2 pair, 2 pair+1)
-        // of one element form one 32-bit LDS word of V^T
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t lo = e % 2 ? w0[e / 2] >> 16 : w0[e / 2] & 0xffffu;
-          const uint32_t hi = e % 2 ? w1[e / 2] >> 16 : w1[e / 2] & 0xffffu;
-          *reinterpret_cast<uint32_t*>(&sv[(ch * 8 + e) * kRowV + 2 * pair]) = lo | (hi << 16);
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          *reinterpret_cast<uint2*>(&sv[(ch * 4 + e) * kRowV + 2 * pair]) = make_uint2(w0[e], w1[e]);
-      }
+      // (masked word by word, so that the rows stay in registers)
+      const uint32_t m = 0u - ((oks >> it) & 1u);
+      const uint4 kv = rks[it], vv = rvs[it];
+      *reinterpret_cast<uint4*>(&sk[key * kRowK + ch * kElems16]) = make_uint4(kv.x & m, kv.y & m, kv.z & m, kv.w & m);
+      *reinterpret_cast<uint4*>(&sv[key * kRowV + ch * kElems16]) = make_uint4(vv.x & m, vv.y & m, vv.z & m, vv.w & m);
     }
   };
 
@@ -366,7 +362,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
         const Frag pf = M::pack_p(pr + kk * kPack);
   #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const Frag vf = M::load_vt(&sv[(db * 32 + col) * kRowV], kk, hg);
+          const Frag vf = M::load_v(sv, kk, db, lane);
           o[db] = M::mma(vf, pf, o[db]);
         }
       }
