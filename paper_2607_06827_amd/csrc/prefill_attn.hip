@@ -419,6 +419,284 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   }
 }
 
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) void* global_void_ptr;
+
+// bf16 prefill with the K/V tiles moved straight from the paged cache into
+// LDS by the gfx950 direct loads (global_load_lds_dwordx4): no staging
+// registers, no staging writes.  A wave-wide direct load fills 1 KB of LDS
+// in lane order, so tile rows are unpadded (D elements) and 16-byte chunks
+// are XOR-swizzled within a row instead: chunk c of row r sits at position
+// c ^ swz(r), with swz_k(r) = r mod 16 (the QK reads of 16 rows at one
+// chunk hit distinct banks) and swz_v(r) = (r mod 4) * 4 (the transposed PV
+// reads of 4 rows x 4 chunks hit distinct banks).  The loading lane picks the
+// global chunk that belongs at its LDS position.  Keys past the visible range
+// load a visible row (finite data that the mask gives zero weight).
+//
+// Pipeline: the block-table entries of tile t load at step t-2, its rows go
+// to LDS at step t-1 (two buffers, each a separate LDS array so that the
+// compiler knows the in-flight direct loads never touch the buffer being
+// read), and every step ends with a full wait and a barrier.
+template <int D>
+struct LdsSwz {
+  static constexpr int kChunks = D / 8;  // 16-byte chunks per row
+  static __device__ __forceinline__ int k(int row) { return row & (kChunks >= 16 ? 15 : kChunks - 1); }
+  static __device__ __forceinline__ int v(int row) { return (row % (kChunks / 4)) << 2; }
+};
+
+// Waves per SIMD the compiler must fit: three where the registers allow it
+// without spilling (it measured faster than two at the same tile sizes).
+template <int D, int G>
+constexpr int lds_kernel_waves() { return D == 128 && G == 4 ? 2 : 3; }
+
+template <int D, int G>
+__global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>())) void prefill_kernel_lds(PrefillArgs a) {
+  typedef bf16_bits T;
+  typedef Mfma<T> M;
+  typedef M::Frag Frag;
+  typedef LdsSwz<D> Swz;
+  constexpr int kThreads = PrefillShape<G>::kThreads;
+  constexpr int kWaves = PrefillShape<G>::kWaves;
+  constexpr int kRows = PrefillShape<G>::kRows;
+  constexpr int kKeys = 32;                        // keys per tile
+  constexpr int kPack = M::kPack;
+  constexpr int kStep = 2 * kPack;                 // head-dim elements per QK MFMA
+  constexpr int kQChunks = D / kStep;
+  constexpr int kChunks = Swz::kChunks;
+  constexpr int kRowsPerLoad = 64 / kChunks;       // rows one wave-wide direct load fills
+  constexpr int kLoads = kKeys / kRowsPerLoad;     // direct loads per tile and matrix
+  constexpr int kLoadsPerWave = kLoads >= kWaves ? kLoads / kWaves : 1;
+  static_assert(kLoads % kWaves == 0 || kWaves % kLoads == 0, "loads must split evenly over waves");
+  constexpr int kTile = kKeys * D;                 // elements of one tile
+  constexpr float kLn2 = 0.6931471805599453f;
+  (void)kThreads;
+
+  __shared__ __attribute__((aligned(16))) T s_k0[kTile];
+  __shared__ __attribute__((aligned(16))) T s_k1[kTile];
+  __shared__ __attribute__((aligned(16))) T s_v0[kTile];
+  __shared__ __attribute__((aligned(16))) T s_v1[kTile];
+
+  // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int tile = a.num_tiles - 1 - item % a.num_tiles;
+  const int g = (item / a.num_tiles) % heads;
+  const int b = item / a.num_tiles / heads;
+
+  const int P = max(a.prefix_len[b], 0);
+  const int T_ = max(a.speech_len[b], 0);
+  const int N = max(a.suffix_len[b], 0);
+  const int w = a.w_eff;
+  const int nW = (T_ + w - 1) / w;
+  const int rows = min(P + T_ + N, a.q_len);
+  const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
+  const int p0 = tile * kRows;
+  if (p0 >= rows) return;
+  const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
+  const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = g * G + wave % G;
+  const int col = lane & 31, hg = lane >> 5;
+  const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
+  const int p = wrow0 + col;
+  const bool qvalid = p < rows;
+  const int nvis = qvalid ? min(visible_keys(p, P, T_, nW, w, a.mask_mode), clen) : 0;
+  // keys every valid row of the wave sees (n_vis grows with the row)
+  const int nvis_lo = wrow0 < rows ? min(visible_keys(wrow0, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int hq = a.num_q_heads;
+  const int slot_mask = (1 << a.pv.page_shift) - 1;
+  const int shift = a.pv.page_shift;
+  const int64_t num_pages = a.pv.num_pages;
+  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
+  const T* kpool = static_cast<const T*>(a.k_pages);
+  const T* vpool = static_cast<const T*>(a.v_pages);
+  const int ntiles = (kmax + kKeys - 1) / kKeys;
+  // this wave's direct loads: load i fills rows [row0(i), +kRowsPerLoad) of a tile
+  const bool loads = kLoads >= kWaves || wave < kLoads;
+  auto load_row0 = [&](int i) { return (kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * kRowsPerLoad; };
+  const int lrow = lane / kChunks, lpos = lane % kChunks;  // row within the load, LDS chunk position
+
+  f32x16_t o[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  float m_run = neg_inf(), l_run = 0.f;
+
+  int pg[2][kLoadsPerWave];  // block-table entries, by tile parity
+  auto table_load = [&](int kt, int* pgs) {
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int key = min(kt * kKeys + load_row0(i) + lrow, kclamp);
+      pgs[i] = table_row[min(key >> shift, a.pv.max_pages - 1)];
+    }
+  };
+  auto tile_load = [&](int kt, const int* pgs, T* sk, T* sv) {
+    if (!loads) return;
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int row = load_row0(i) + lrow;
+      const int key = min(kt * kKeys + row, kclamp);
+      const int e = pgs[i];
+      const int page = (e >= 0 && e < num_pages) ? e : 0;  // a bad entry reads an in-range page
+      const int64_t off = page_row<D>(page, g, key & slot_mask, a.pv);
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(kpool + off + ((lpos ^ Swz::k(row)) << 3)),
+                                       (lds_void_ptr)(sk + load_row0(i) * D), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(vpool + off + ((lpos ^ Swz::v(row)) << 3)),
+                                       (lds_void_ptr)(sv + load_row0(i) * D), 16, 0, 0);
+    }
+  };
+
+  // prologue: tables of tiles 0 and 1, tile 0 into LDS, then this lane's query
+  // row (issued after the tile: the memory counter is in order)
+  table_load(0, pg[0]);
+  table_load(1, pg[1]);
+  tile_load(0, pg[0], s_k0, s_v0);
+  __builtin_amdgcn_sched_barrier(0);
+  Frag qf[kQChunks];
+  {
+    const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + (qvalid ? p : 0)) * hq + h) * D;
+#pragma unroll
+    for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = M::load(qrow + kc * kStep + hg * kPack);
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __syncthreads();
+
+  // one step; kPar = kt & 1 selects buffers and table registers at compile time
+  auto tile_step = [&](int kt, auto par) {
+    constexpr int kPar = decltype(par)::value;
+    T* const sk = kPar ? s_k1 : s_k0;
+    T* const sv = kPar ? s_v1 : s_v0;
+    T* const sk_next = kPar ? s_k0 : s_k1;
+    T* const sv_next = kPar ? s_v0 : s_v1;
+    table_load(kt + 2, pg[kPar]);                     // parity of kt+2 = kt
+    tile_load(kt + 1, pg[1 - kPar], sk_next, sv_next);  // into the buffer tile kt-1 used
+    if (kt < ntiles) {  // (the loop runs an even number of steps)
+      const int kb = kt * kKeys;
+      // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
+      f32x16_t st;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) st[i] = 0.f;
+      const T* krow = sk + col * D;
+      const int kswz = Swz::k(col);
+#pragma unroll
+      for (int kc = 0; kc < kQChunks; ++kc)
+        st = M::mma(M::load(krow + (((2 * kc + hg) ^ kswz) << 3)), qf[kc], st);
+
+      float pr[16];
+      float mt = neg_inf();
+      const bool masked = kb + kKeys > nvis_lo;  // uniform over the wave
+      if (masked) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
+          pr[i] = key < nvis ? st[i] : neg_inf();
+          mt = fmaxf(mt, pr[i]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pr[i] = st[i];
+          mt = fmaxf(mt, pr[i]);
+        }
+      }
+      mt = partner_max(mt) * a.scale_log2;  // the scale is > 0
+      if (mt > m_run + kSlack) {
+        const float corr = fast_exp2(m_run - mt);
+        l_run *= corr;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+        m_run = mt;
+      }
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_run));
+        if (masked) pr[i] = m_run == neg_inf() ? 0.f : pr[i];  // nothing visible yet
+        sum += pr[i];
+      }
+      l_run += sum;
+
+      // O^T += V^T P^T over the 32 keys of the tile; the A operand comes
+      // through the LDS transpose read (see Mfma<bf16_bits>::load_v) from
+      // the swizzled rows
+      const int vg = lane >> 4, vj = lane & 15;
+#pragma unroll
+      for (int kk = 0; kk < kKeys / kStep; ++kk) {
+        const Frag pf = M::pack_p(pr + kk * kPack);
+        const int r0 = 16 * kk + 4 * (vg >> 1) + (vj >> 2);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const int e = 32 * db + 16 * (vg & 1) + 4 * (vj & 3);  // first element of the lane's run
+          const T* plo = sv + r0 * D + ((((e >> 3) ^ Swz::v(r0)) << 3) | (e & 4));
+          const T* phi = sv + (r0 + 8) * D + ((((e >> 3) ^ Swz::v(r0 + 8)) << 3) | (e & 4));
+          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)plo);
+          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)phi);
+          const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2],
+                             (unsigned short)lo[3], (unsigned short)hi[0], (unsigned short)hi[1],
+                             (unsigned short)hi[2], (unsigned short)hi[3]};
+          o[db] = M::mma(__builtin_bit_cast(Frag, v), pf, o[db]);
+        }
+      }
+    }
+    // the next tile's rows (and the table entries after them) have landed in
+    // every wave's part of the buffer once each wave's counter is at zero
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+  };
+  // two steps per iteration so that buffers and registers are compile-time;
+  // the loads of a step past the last tile are in range and never read
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    tile_step(kt, std::integral_constant<int, 0>());
+    tile_step(kt + 1, std::integral_constant<int, 1>());
+  }
+
+  const float l_tot = partner_sum(l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (hg == 0 && a.lse && qvalid)
+    a.lse[((int64_t)b * hq + h) * a.q_len + p] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : neg_inf();
+
+  if constexpr (kWaves > 4) {  // direct stores of the C layout: four values per row
+    if (qvalid) {
+      T* orow = static_cast<T*>(a.out) + (((int64_t)b * a.q_len + p) * hq + h) * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int ig = 0; ig < 4; ++ig)
+          M::store4(orow + db * 32 + 8 * ig + 4 * hg, o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
+                    o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+    }
+  } else {
+    // output: one 32 x D tile per wave through one of the (now idle) tile
+    // buffers, rows swizzled like K, then 16-byte row stores
+    T* so = wave == 0 ? s_k0 : wave == 1 ? s_k1 : wave == 2 ? s_v0 : s_v1;
+    const int oswz = Swz::k(col);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int ig = 0; ig < 4; ++ig)
+        M::store4(so + col * D + (((4 * db + ig) ^ oswz) << 3) + 4 * hg, o[db][4 * ig] * inv,
+                  o[db][4 * ig + 1] * inv, o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+    __syncthreads();  // (the same wave reads its tile back: orders its LDS traffic)
+    constexpr int kRowsPerPass = 64 / kChunks;
+#pragma unroll
+    for (int r0 = 0; r0 < 32; r0 += kRowsPerPass) {
+      const int rr = r0 + lane / kChunks, cch = lane % kChunks;
+      const int out_row = wrow0 + rr;
+      if (out_row < rows) {
+        const uint4 v = *reinterpret_cast<const uint4*>(so + rr * D + ((cch ^ Swz::k(rr)) << 3));
+        *reinterpret_cast<uint4*>(static_cast<T*>(a.out) + (((int64_t)b * a.q_len + out_row) * hq + h) * D +
+                                  cch * 8) = v;
+      }
+    }
+  }
+}
+
 template <typename T, int D>
 hipError_t launch_prefill_d(const PrefillArgs& a, int group, int batch, hipStream_t s) {
   const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
@@ -427,6 +705,17 @@ hipError_t launch_prefill_d(const PrefillArgs& a, int group, int batch, hipStrea
     case 2: return launch_struct(prefill_kernel<T, D, 2>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
     case 4: return launch_struct(prefill_kernel<T, D, 4>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
     default: return launch_struct(prefill_kernel<T, D, 8>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
+  }
+}
+
+template <int D>
+hipError_t launch_prefill_lds(const PrefillArgs& a, int group, int batch, hipStream_t s) {
+  const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
+  switch (group) {
+    case 1: return launch_struct(prefill_kernel_lds<D, 1>, dim3(items), dim3(PrefillShape<1>::kThreads), s, a);
+    case 2: return launch_struct(prefill_kernel_lds<D, 2>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
+    case 4: return launch_struct(prefill_kernel_lds<D, 4>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
+    default: return launch_struct(prefill_kernel_lds<D, 8>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
   }
 }
 
@@ -444,8 +733,8 @@ int prefill_rows_per_tile(int group) {
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int group, int batch,
                           hipStream_t s) {
   if (dtype == 1) {
-    if (head_dim == 128) return launch_prefill_d<bf16_bits, 128>(a, group, batch, s);
-    return launch_prefill_d<bf16_bits, 64>(a, group, batch, s);
+    if (head_dim == 128) return launch_prefill_lds<128>(a, group, batch, s);
+    return launch_prefill_lds<64>(a, group, batch, s);
   }
   if (head_dim == 128) return launch_prefill_d<float, 128>(a, group, batch, s);
   return launch_prefill_d<float, 64>(a, group, batch, s);
