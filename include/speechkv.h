@@ -16,6 +16,8 @@
  *   speechkv_pool_kv       prefill-time pooling into the paged cache (Eq. 4)
  *   speechkv_decode_attn   one-query-per-sequence attention over the cache (Eq. 5)
  *   speechkv_prefill_attn  full-resolution queries over the cache (Eq. 5 + mask)
+ *   speechkv_pool_hidden   the same pooling applied to whole hidden states
+ *                          (HS Compression, Sec. IV-A method (4))
  *
  * Conventions shared by every call
  * --------------------------------
@@ -161,6 +163,47 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
                      const float* gate_u, int32_t layer, int32_t l0,
                      const speechkv_paged_kv* cache, int32_t* cache_len_out,
                      void* stream);
+
+/*
+ * speechkv_pool_hidden - learned window pooling of whole hidden states: the HS
+ * Compression variant (Sec. IV-A, method (4)), which applies the pooling of
+ * Eq. 4 to the entire hidden state at layer l0, so that all later layers,
+ * queries included, run on the shortened sequence.  (Attention over that
+ * sequence is plain causal attention: speechkv_prefill_attn and
+ * speechkv_decode_attn with w = 1 over a cache built from it.)
+ *
+ * For every sequence b, with P, T, N its span lengths and nW = ceil(T / w):
+ *   out row c in [0, P)          <- h row c                    (bitwise copy)
+ *   out row P + i, i in [0, nW)  <- sum_j alpha_j * h row j over the window
+ *       j in [P + i*w, min(P + (i+1)*w, P + T)), alpha = softmax_j(gate_u .
+ *       h row j) over that window (a one-frame window is copied bitwise)
+ *   out row P + nW + m, m in [0, N) <- h row P + T + m         (bitwise copy)
+ * As in speechkv_pool_kv the gate bias cancels and only u is taken.
+ *
+ * h              device, element type dtype.  Element (b, s, e) is at index
+ *                b*stride_b + s*stride_s + e; e (the hidden axis) is
+ *                contiguous.  Strides in elements, keeping rows 16-byte aligned.
+ * batch, raw_len sequences (>= 1) and rows per sequence in h (>= 1).  Caller
+ *                obligation: prefix+speech+suffix <= raw_len.
+ * hidden         hidden size, one of 512, 1024, 2048, 4096.
+ * dtype          SPEECHKV_DTYPE_F32 or SPEECHKV_DTYPE_BF16 (h and out alike).
+ * spans          host pointer to the span description.
+ * w              window size (>= 1).
+ * gate_u         device fp32 [hidden], or NULL for the zero gate.
+ * out            device, [batch] sequences of out_capacity rows: element
+ *                (b, c, e) at b*out_stride_b + c*out_stride_s + e.  Must not
+ *                overlap h.  Rows past P + nW + N are not written.
+ * out_capacity   rows per sequence in out; must be >= spans->max_total_len.
+ * out_len        device int32 [batch] receiving P + nW + N, or NULL.
+ * Errors: INVALID_ARG, UNSUPPORTED (dtype or hidden), ALIAS (out overlaps h),
+ *         HIP.
+ */
+int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s,
+                         int32_t batch, int32_t raw_len, int32_t hidden,
+                         int32_t dtype, const speechkv_spans* spans, int32_t w,
+                         const float* gate_u, void* out, int64_t out_stride_b,
+                         int64_t out_stride_s, int32_t out_capacity,
+                         int32_t* out_len, void* stream);
 
 /*
  * speechkv_decode_attn - one decoding step of attention over the compressed

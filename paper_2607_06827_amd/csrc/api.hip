@@ -173,6 +173,48 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b, int
   return status_of(skv::launch_pool(a, cache->dtype, D, batch, static_cast<hipStream_t>(stream)));
 }
 
+int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s, int32_t batch,
+                         int32_t raw_len, int32_t hidden, int32_t dtype, const speechkv_spans* spans,
+                         int32_t w, const float* gate_u, void* out, int64_t out_stride_b,
+                         int64_t out_stride_s, int32_t out_capacity, int32_t* out_len, void* stream) {
+  if (!h || !out) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_spans(spans);
+  if (st) return st;
+  if (dtype != SPEECHKV_DTYPE_F32 && dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
+  if (!skv::pool_hidden_supported(hidden)) return SPEECHKV_ERR_UNSUPPORTED;
+  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || w < 1) return SPEECHKV_ERR_INVALID_ARG;
+  if (stride_b < 0 || stride_s < 0 || out_stride_b < 0 || out_stride_s < 0) return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > raw_len || out_capacity < spans->max_total_len || out_capacity < 1)
+    return SPEECHKV_ERR_INVALID_ARG;
+  const int esz = elt_size(dtype);
+  const int64_t per16 = 16 / esz;
+  if (stride_b % per16 || stride_s % per16 || out_stride_b % per16 || out_stride_s % per16)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (!aligned16(h) || !aligned16(out) || (gate_u && !aligned16(gate_u))) return SPEECHKV_ERR_INVALID_ARG;
+  const int64_t in_bytes =
+      ((int64_t)(batch - 1) * stride_b + (int64_t)(raw_len - 1) * stride_s + hidden) * esz;
+  const int64_t out_bytes =
+      ((int64_t)(batch - 1) * out_stride_b + (int64_t)(out_capacity - 1) * out_stride_s + hidden) * esz;
+  if (overlaps(h, in_bytes, out, out_bytes)) return SPEECHKV_ERR_ALIAS;
+  skv::PoolHiddenArgs a;
+  a.h = h;
+  a.stride_b = stride_b;
+  a.stride_s = stride_s;
+  a.raw_len = raw_len;
+  a.prefix_len = spans->prefix_len;
+  a.speech_len = spans->speech_len;
+  a.suffix_len = spans->suffix_len;
+  a.w = w;
+  a.gate = gate_u;
+  a.out = out;
+  a.out_stride_b = out_stride_b;
+  a.out_stride_s = out_stride_s;
+  a.out_cap = out_capacity;
+  a.out_len = out_len;
+  a.max_out = spans->max_total_len;
+  return status_of(skv::launch_pool_hidden(a, dtype, hidden, batch, static_cast<hipStream_t>(stream)));
+}
+
 int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
                          const speechkv_paged_kv* cache, const int32_t* cache_len,
                          int32_t max_cache_len, const void* k_new, const void* v_new, float scale,

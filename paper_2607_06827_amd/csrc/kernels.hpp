@@ -27,6 +27,24 @@ struct PoolArgs {
   int max_out;             // bound on the compressed length (grid size)
 };
 
+// Window pooling of whole hidden states (HS Compression, Sec. IV-A method
+// (4); the pooling of Eq. 4 applied to the hidden state).
+struct PoolHiddenArgs {
+  const void* h;
+  int64_t stride_b, stride_s;  // elements
+  int raw_len;
+  const int32_t* prefix_len;
+  const int32_t* speech_len;
+  const int32_t* suffix_len;
+  int w;
+  const float* gate;  // [hidden] or null (zero gate)
+  void* out;
+  int64_t out_stride_b, out_stride_s;  // elements
+  int out_cap;        // rows per sequence in out
+  int32_t* out_len;   // may be null
+  int max_out;        // bound on the compressed length (grid size)
+};
+
 // Split-K decode attention (Sec. III-B, Eq. 5; Sec. III-C).
 struct DecodeArgs {
   const void* q;
@@ -67,6 +85,9 @@ struct PrefillArgs {
 
 // dtype: 0 = fp32, 1 = bf16.  Each launcher returns the launch status.
 hipError_t launch_pool(const PoolArgs& a, int dtype, int head_dim, int batch, hipStream_t s);
+bool pool_hidden_supported(int hidden);
+hipError_t launch_pool_hidden(const PoolHiddenArgs& a, int dtype, int hidden, int batch,
+                              hipStream_t s);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group, int batch,
                          hipStream_t s);
 hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, int head_dim, int num_q_heads,

@@ -54,6 +54,9 @@ _vp, _i32, _i64, _f32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ct
 _lib.speechkv_pool_kv.argtypes = [_vp, _vp, _i64, _i64, _i64, _i32, _i32, ctypes.POINTER(_Spans),
                                   _i32, _vp, _i32, _i32, ctypes.POINTER(_PagedKV), _vp, _vp]
 _lib.speechkv_pool_kv.restype = ctypes.c_int
+_lib.speechkv_pool_hidden.argtypes = [_vp, _i64, _i64, _i32, _i32, _i32, _i32, ctypes.POINTER(_Spans),
+                                      _i32, _vp, _vp, _i64, _i64, _i32, _vp, _vp]
+_lib.speechkv_pool_hidden.restype = ctypes.c_int
 _lib.speechkv_decode_attn.argtypes = [_vp, _i32, _i32, ctypes.POINTER(_PagedKV), _vp, _i32, _vp,
                                       _vp, _f32, _i32, _vp, _vp, _sz, _vp]
 _lib.speechkv_decode_attn.restype = ctypes.c_int
@@ -160,6 +163,22 @@ def speechkv_pool_kv(k_raw: torch.Tensor, v_raw: torch.Tensor, spans: Spans, w: 
                                k_raw.shape[1], ctypes.byref(s), w, _ptr(gate_u), layer, l0,
                                ctypes.byref(c), _ptr(cache_len_out), _stream(stream))
     _check(st, "speechkv_pool_kv")
+
+
+def speechkv_pool_hidden(h: torch.Tensor, spans: Spans, w: int, gate_u: Optional[torch.Tensor],
+                         out: torch.Tensor, out_len: Optional[torch.Tensor] = None,
+                         stream=None) -> None:
+    """h: [B, S_raw, hidden], out: [B, S_out, hidden], both with a contiguous last axis."""
+    if h.dim() != 3 or out.dim() != 3 or h.stride(2) != 1 or out.stride(2) != 1:
+        raise ValueError("h and out must be [B, S, hidden] with a contiguous last axis")
+    if h.dtype != out.dtype or h.shape[0] != out.shape[0] or h.shape[2] != out.shape[2]:
+        raise ValueError("h and out must agree in dtype, batch and hidden size")
+    s = spans._c()
+    st = _lib.speechkv_pool_hidden(h.data_ptr(), h.stride(0), h.stride(1), h.shape[0], h.shape[1],
+                                   h.shape[2], _dtype_code(h.dtype), ctypes.byref(s), w,
+                                   _ptr(gate_u), out.data_ptr(), out.stride(0), out.stride(1),
+                                   out.shape[1], _ptr(out_len), _stream(stream))
+    _check(st, "speechkv_pool_hidden")
 
 
 def speechkv_decode_attn(q: torch.Tensor, cache: PagedKV, cache_len: torch.Tensor,

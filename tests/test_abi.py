@@ -26,6 +26,7 @@ def declared_functions():
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
+                          "speechkv_pool_hidden",
                           "speechkv_compressed_len", "speechkv_decode_num_splits",
                           "speechkv_decode_workspace_bytes", "speechkv_status_string",
                           "speechkv_version"}
@@ -128,6 +129,34 @@ E_ARG, E_UNS, E_WS, E_ALIAS = skv.ERR_INVALID_ARG, skv.ERR_UNSUPPORTED, skv.ERR_
 ])
 def test_pool_rejects(kw, code):
     assert pool(**kw) == code
+
+
+HID = FAKE + (14 << 24)
+
+
+def pool_hidden(s=None, **kw):
+    a = dict(h=HID, sb=60 * 2048, ss=2048, batch=2, raw_len=60, hidden=2048, dtype=skv.DTYPE_BF16,
+             w=4, gate=None, out=HID + (4 << 20), ob=60 * 2048, os=2048, cap=60, olen=None)
+    a.update(kw)
+    s = s or spans()
+    return lib.speechkv_pool_hidden(a["h"], a["sb"], a["ss"], a["batch"], a["raw_len"], a["hidden"],
+                                    a["dtype"], ctypes.byref(s), a["w"], a["gate"], a["out"], a["ob"],
+                                    a["os"], a["cap"], a["olen"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h=None), E_ARG), (dict(out=None), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=0), E_ARG),
+    (dict(w=0), E_ARG), (dict(sb=-8), E_ARG), (dict(ss=3), E_ARG), (dict(os=5), E_ARG),
+    (dict(h=HID + 4), E_ARG), (dict(gate=FAKE + 4), E_ARG), (dict(raw_len=50), E_ARG),
+    (dict(cap=59), E_ARG), (dict(hidden=768), E_UNS), (dict(hidden=128), E_UNS), (dict(dtype=7), E_UNS),
+    (dict(out=HID + 2048 * 2), E_ALIAS),
+])
+def test_pool_hidden_rejects(kw, code):
+    assert pool_hidden(**kw) == code
+
+
+def test_pool_hidden_rejects_bad_spans():
+    assert pool_hidden(s=spans(prefix_len=None)) == E_ARG
 
 
 @pytest.mark.parametrize("ckw,code", [
