@@ -17,8 +17,9 @@ peak (algorithmic bytes: every cached K/V row once, plus q, the new K/V and
 the output); the pooling kernel's achieved HBM bandwidth (raw K/V read once,
 cache rows written once) and the prefill attention's achieved bf16 TFLOP/s
 against the 2.5 PFLOP/s dense MFMA peak (FLOPs of the visible (row, key) pairs
-only), each from a graph of that kernel alone; and the fp64 CPU oracle timed
-on a bounded sample of the same job.
+only), each from a graph of that kernel alone; HS Compression's pooling of
+the whole hidden state (hidden 2048) on the same batch and spans, in GB/s;
+and the fp64 CPU oracle timed on a bounded sample of the same job.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-full]
     python bench.py --traffic [--workload NAME]   # eager launches for counter runs
@@ -156,6 +157,21 @@ def measure(job, steps, warmup, label):
     return res
 
 
+def measure_hs_pool(wl, steps):
+    """HS Compression's hidden-state pooling on the same batch and spans."""
+    from paper_2607_06827_amd.workload import HiddenPoolJob
+
+    hj = HiddenPoolJob(wl)
+    g = capture(hj.run)
+    ms = time_graph(g, max(20, steps))
+    gbps = hj.bytes() / (ms * 1e-3) / 1e9
+    log(f"hs pool (hidden {hj.hidden}): {ms * 1e3:.1f} us, {gbps:.0f} GB/s")
+    res = {"hidden": hj.hidden, "avg_launch_us": ms * 1e3, "bytes_per_launch": hj.bytes(),
+           "achieved_gbps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBPS}
+    del g, hj
+    return res
+
+
 def cpu_baseline(job, budget_s=15.0):
     """The fp64 oracle on whole sequences of the same job (all layers: pool,
     prefill attention, every decode step), one sequence at a time until about
@@ -206,8 +222,8 @@ def main():
     ap.add_argument("--no-full", action="store_true", help="skip the uncompressed run")
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--traffic", action="store_true",
-                    help="counter-collection run: the job's launches issued eagerly once, "
-                         "then a plain 1 GiB device copy that calibrates the byte counters")
+                    help="counter-collection run: the job's launches and one HS pooling launch "
+                         "issued eagerly once, then a plain 1 GiB device copy that calibrates the byte counters")
     ap.add_argument("--workload", default=None,
                     help="with --traffic: run this workload (by name) instead of the benchmark's")
     args = ap.parse_args()
@@ -239,6 +255,9 @@ def main():
     log(f"inputs and caches ready in {time.perf_counter() - t0:.1f} s")
     if args.traffic:
         job.run()  # the step's launches, eagerly: 28 pool, 28 prefill, 128 x 28 decode
+        from paper_2607_06827_amd.workload import HiddenPoolJob
+        hj = HiddenPoolJob(wl)
+        hj.run()  # one HS Compression pooling launch of the same batch
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)  # 1 GiB read + 1 GiB written by one copy kernel
@@ -249,7 +268,7 @@ def main():
                           "decode_bytes_per_launch": dec_bytes / max(launches, 1), "decode_launches": launches,
                           "pool_bytes_per_launch": sum(job.pool_bytes_layer(i) for i in range(nl)) / nl,
                           "prefill_flops_per_launch": sum(job.prefill_flops_layer(i) for i in range(nl)) / nl,
-                          "layers": nl}))
+                          "hs_pool_bytes_per_launch": hj.bytes(), "layers": nl}))
         return
     pooled = measure(job, args.steps, args.warmup, "pooled (l0=14, w=4)")
 
@@ -259,6 +278,9 @@ def main():
         full = measure(fjob, args.steps, args.warmup, "full KV")
         del fjob
         torch.cuda.empty_cache()
+
+    hs_pool = measure_hs_pool(wl, args.steps)
+    torch.cuda.empty_cache()
 
     dec_bytes, launches = decode_launch_stats(job)
     avg_launch_ms = pooled["decode_ms"] / launches
@@ -292,6 +314,7 @@ def main():
         "prefill_ms": pooled["prefill_ms"],
         "pool": pooled["pool"],
         "prefill_attn": pooled["prefill_attn"],
+        "hs_pool": hs_pool,
     }
     if full:
         result["full_kv"] = {"tokens_per_s": full["tokens_per_s"], "ms_per_step": full["ms_per_step"],

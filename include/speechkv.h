@@ -193,7 +193,11 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
  * out            device, [batch] sequences of out_capacity rows: element
  *                (b, c, e) at b*out_stride_b + c*out_stride_s + e.  Must not
  *                overlap h.  Rows past P + nW + N are not written.
- * out_capacity   rows per sequence in out; must be >= spans->max_total_len.
+ * out_capacity   rows per sequence in out (>= 1).  Caller obligation:
+ *                out_capacity >= P + nW + N of every sequence (the compressed
+ *                length, not the raw one).  Rows at or past out_capacity are
+ *                never written; out_len still receives the full length, so a
+ *                short buffer shows there.
  * out_len        device int32 [batch] receiving P + nW + N, or NULL.
  * Errors: INVALID_ARG, UNSUPPORTED (dtype or hidden), ALIAS (out overlaps h),
  *         HIP.

@@ -184,8 +184,7 @@ int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s, int3
   if (!skv::pool_hidden_supported(hidden)) return SPEECHKV_ERR_UNSUPPORTED;
   if (batch < 1 || batch > kMaxGrid || raw_len < 1 || w < 1) return SPEECHKV_ERR_INVALID_ARG;
   if (stride_b < 0 || stride_s < 0 || out_stride_b < 0 || out_stride_s < 0) return SPEECHKV_ERR_INVALID_ARG;
-  if (spans->max_total_len > raw_len || out_capacity < spans->max_total_len || out_capacity < 1)
-    return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > raw_len || out_capacity < 1) return SPEECHKV_ERR_INVALID_ARG;
   const int esz = elt_size(dtype);
   const int64_t per16 = 16 / esz;
   if (stride_b % per16 || stride_s % per16 || out_stride_b % per16 || out_stride_s % per16)
@@ -211,7 +210,8 @@ int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s, int3
   a.out_stride_s = out_stride_s;
   a.out_cap = out_capacity;
   a.out_len = out_len;
-  a.max_out = spans->max_total_len;
+  // no output row at or past min(max_total_len, out_capacity) is written
+  a.max_out = spans->max_total_len < out_capacity ? spans->max_total_len : out_capacity;
   return status_of(skv::launch_pool_hidden(a, dtype, hidden, batch, static_cast<hipStream_t>(stream)));
 }
 

@@ -143,7 +143,9 @@ __global__ __launch_bounds__(256) void pool_hidden_kernel(PoolHiddenArgs a) {
 
 template <typename T>
 hipError_t launch_pool_hidden_t(const PoolHiddenArgs& a, int hidden, int batch, hipStream_t s) {
-  const dim3 grid((a.max_out + 3) / 4, batch);
+  // at least one block per sequence: block 0 writes out_len even when every span is empty
+  const int blocks = (a.max_out + 3) / 4;
+  const dim3 grid((unsigned)(blocks > 0 ? blocks : 1), batch);
   switch (hidden / 512) {
     case 1: return launch_struct(pool_hidden_kernel<T, 1>, grid, dim3(256), s, a);
     case 2: return launch_struct(pool_hidden_kernel<T, 2>, grid, dim3(256), s, a);

@@ -17,7 +17,7 @@ import torch
 from . import inputs
 from .speechkv import (PagedKV, Spans, speechkv_compressed_len, speechkv_decode_attn,
                        speechkv_decode_num_splits, speechkv_decode_workspace_bytes,
-                       speechkv_pool_kv, speechkv_prefill_attn)
+                       speechkv_pool_hidden, speechkv_pool_kv, speechkv_prefill_attn)
 
 
 def visible_pairs(P: int, T: int, N: int, w: int) -> int:
@@ -211,3 +211,38 @@ class Job:
         multiply-add (the masked-out pairs are not counted)."""
         wl = self.wl
         return 4 * wl.batch * wl.num_q_heads * wl.head_dim * self.prefill_visible_pairs(i)
+
+
+class HiddenPoolJob:
+    """HS Compression (Sec. IV-A, method (4)) of one workload: the hidden state
+    entering layer l0 ([B, P + T + N, hidden], hidden = q_heads x head_dim,
+    2048 for Qwen3-1.7B) pooled with the Eq. 4 window softmax into the
+    shortened sequence every later layer runs on."""
+
+    def __init__(self, wl: inputs.Workload, device="cuda"):
+        self.wl = wl
+        self.hidden = wl.num_q_heads * wl.head_dim
+        B, S = wl.batch, wl.prefill_len
+        self.h = inputs.normal((B, S, self.hidden), wl.seed * 100 + 71, device=device,
+                               dtype=wl.torch_dtype)
+        self.gate = inputs.normal((self.hidden,), wl.seed * 100 + 72, device=device,
+                                  scale=self.hidden ** -0.5)
+        self.out_rows = speechkv_compressed_len(wl.prefix_len, wl.speech_len, wl.suffix_len,
+                                                wl.w, 1, 0)
+        self.out = torch.empty(B, self.out_rows, self.hidden, dtype=wl.torch_dtype,
+                               device=device)
+        self.out_len = torch.empty(B, dtype=torch.int32, device=device)
+        i32 = lambda v: torch.full((B,), v, dtype=torch.int32, device=device)
+        self.spans = Spans(i32(wl.prefix_len), i32(wl.speech_len), i32(wl.suffix_len),
+                           wl.speech_len, S)
+
+    def run(self, stream=None):
+        speechkv_pool_hidden(self.h, self.spans, self.wl.w, self.gate, self.out, self.out_len,
+                             stream)
+
+    def bytes(self) -> int:
+        """Algorithmic HBM bytes of one launch: every input row read once,
+        every output row written once, the gate read."""
+        e = self.h.element_size()
+        return self.wl.batch * self.hidden * e * (self.wl.prefill_len + self.out_rows) \
+            + self.hidden * 4

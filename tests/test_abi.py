@@ -148,7 +148,7 @@ def pool_hidden(s=None, **kw):
     (dict(h=None), E_ARG), (dict(out=None), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=0), E_ARG),
     (dict(w=0), E_ARG), (dict(sb=-8), E_ARG), (dict(ss=3), E_ARG), (dict(os=5), E_ARG),
     (dict(h=HID + 4), E_ARG), (dict(gate=FAKE + 4), E_ARG), (dict(raw_len=50), E_ARG),
-    (dict(cap=59), E_ARG), (dict(hidden=768), E_UNS), (dict(hidden=128), E_UNS), (dict(dtype=7), E_UNS),
+    (dict(cap=0), E_ARG), (dict(hidden=768), E_UNS), (dict(hidden=128), E_UNS), (dict(dtype=7), E_UNS),
     (dict(out=HID + 2048 * 2), E_ALIAS),
 ])
 def test_pool_hidden_rejects(kw, code):

@@ -28,7 +28,8 @@ def f64(t):
     return t.detach().to("cpu", torch.float64).numpy()
 
 
-def run_hidden(P, T, N, w, hidden, dtype="bf16", gate_scale=1.0, zero_gate=False, seed=0):
+def run_hidden(P, T, N, w, hidden, dtype="bf16", gate_scale=1.0, zero_gate=False, seed=0,
+               cap=None):
     dt = torch.bfloat16 if dtype == "bf16" else torch.float32
     B = len(P)
     rows = [p + t + n for p, t, n in zip(P, T, N)]
@@ -40,7 +41,8 @@ def run_hidden(P, T, N, w, hidden, dtype="bf16", gate_scale=1.0, zero_gate=False
     out_len = torch.full((B,), -1, dtype=torch.int32, device="cuda")
     i32 = lambda x: torch.tensor(x, dtype=torch.int32, device="cuda")
     spans = skv.Spans(i32(P), i32(T), i32(N), max(T) if T else 0, max(rows))
-    skv.speechkv_pool_hidden(h, spans, w, u, out, out_len)
+    # out_capacity = cap rows: a view of the first cap rows of each sequence
+    skv.speechkv_pool_hidden(h, spans, w, u, out if cap is None else out[:, :cap], out_len)
     torch.cuda.synchronize()
     # oracle: one head of width `hidden`, a compressed layer
     ref, _, clen = oracle.pool(f64(h).reshape(B, S, 1, hidden), f64(h).reshape(B, S, 1, hidden),
@@ -133,3 +135,32 @@ def test_hs_compression_path():
     oo = f64(o)
     for b in range(B):
         assert rel_err(oo[b, :L[b]], ro[b, :L[b]]) <= TOL["bf16"]
+
+
+def test_pool_hidden_tight_capacity():
+    """An output buffer of exactly the longest compressed length is enough."""
+    P, T, N, w, hidden = [3, 9], [41, 30], [2, 7], 4, 1024
+    L = [p + -(-t // w) + n for p, t, n in zip(P, T, N)]
+    h, out, out_len, ref, clen = run_hidden(P, T, N, w, hidden, cap=max(L))
+    check(P, T, N, w, hidden, "bf16", out, out_len, ref, clen, h)
+
+
+def test_pool_hidden_short_capacity_writes_nothing_past_it():
+    """Rows at or past out_capacity stay untouched; out_len keeps the full
+    compressed length, which is how a caller sees the short buffer."""
+    P, T, N, w, hidden, cap = [6, 2], [57, 12], [5, 1], 4, 512, 10
+    h, out, out_len, ref, clen = run_hidden(P, T, N, w, hidden, cap=cap)
+    assert out_len.cpu().tolist() == [int(c) for c in clen]
+    o = f64(out)
+    for b in range(len(P)):
+        n = min(int(clen[b]), cap)
+        assert rel_err(o[b, :n], ref[b, :n]) <= TOL["bf16"]
+        assert np.all(np.isnan(o[b, n:]))
+
+
+def test_pool_hidden_all_spans_empty():
+    """Every span empty: nothing is written and every length is 0."""
+    P, T, N = [0, 0, 0], [0, 0, 0], [0, 0, 0]
+    h, out, out_len, _, _ = run_hidden(P, T, N, 4, 512)
+    assert out_len.cpu().tolist() == [0, 0, 0]
+    assert torch.isnan(out).all()
