@@ -66,6 +66,11 @@ extern "C" {
 #define SPEECHKV_DTYPE_F32 0
 #define SPEECHKV_DTYPE_BF16 1
 
+/* Largest window size w the pooling and attention calls take, and so the
+ * largest number of rows (raw_len, q_len) is INT32_MAX - SPEECHKV_MAX_WINDOW:
+ * with these bounds no window count ceil(T / w) overflows 32-bit arithmetic. */
+#define SPEECHKV_MAX_WINDOW 65536
+
 /* Mask modes for speech queries against pooled windows (Sec. III-B: each
  * query attends only to positions that precede it; the figure that draws the
  * mask is not part of the text, so two readings are offered).
@@ -146,7 +151,7 @@ typedef struct speechkv_spans {
  * raw_len        rows per sequence in k_raw/v_raw (>= 1).  Caller
  *                obligation: prefix+speech+suffix <= raw_len.
  * spans          host pointer to the span description.
- * w              window size R of the paper (>= 1).
+ * w              window size R of the paper, 1 .. SPEECHKV_MAX_WINDOW.
  * gate_u         device fp32 [num_kv_heads][head_dim], the gate vector of
  *                this layer per KV head, or NULL for the zero gate (uniform
  *                averaging, the paper's initialisation).
@@ -188,7 +193,7 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
  * hidden         hidden size, one of 512, 1024, 2048, 4096.
  * dtype          SPEECHKV_DTYPE_F32 or SPEECHKV_DTYPE_BF16 (h and out alike).
  * spans          host pointer to the span description.
- * w              window size (>= 1).
+ * w              window size, 1 .. SPEECHKV_MAX_WINDOW.
  * gate_u         device fp32 [hidden], or NULL for the zero gate.
  * out            device, [batch] sequences of out_capacity rows: element
  *                (b, c, e) at b*out_stride_b + c*out_stride_s + e.  Must not

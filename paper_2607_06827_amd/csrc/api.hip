@@ -11,6 +11,7 @@
 namespace {
 
 constexpr int kMaxGrid = 65535;
+constexpr int kMaxRows = 2147483647 - SPEECHKV_MAX_WINDOW;  // ceil(T / w) stays in int32
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -132,7 +133,8 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b, int
   int st = check_cache(cache);
   if (st) return st;
   if ((st = check_spans(spans))) return st;
-  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || w < 1 || layer < 0 || l0 < 0)
+  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || raw_len > kMaxRows || w < 1 ||
+      w > SPEECHKV_MAX_WINDOW || layer < 0 || l0 < 0)
     return SPEECHKV_ERR_INVALID_ARG;
   if (stride_b < 0 || stride_s < 0 || stride_h < 0) return SPEECHKV_ERR_INVALID_ARG;
   if (spans->max_total_len > raw_len) return SPEECHKV_ERR_INVALID_ARG;
@@ -182,7 +184,9 @@ int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s, int3
   if (st) return st;
   if (dtype != SPEECHKV_DTYPE_F32 && dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
   if (!skv::pool_hidden_supported(hidden)) return SPEECHKV_ERR_UNSUPPORTED;
-  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || w < 1) return SPEECHKV_ERR_INVALID_ARG;
+  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || raw_len > kMaxRows || w < 1 ||
+      w > SPEECHKV_MAX_WINDOW)
+    return SPEECHKV_ERR_INVALID_ARG;
   if (stride_b < 0 || stride_s < 0 || out_stride_b < 0 || out_stride_s < 0) return SPEECHKV_ERR_INVALID_ARG;
   if (spans->max_total_len > raw_len || out_capacity < 1) return SPEECHKV_ERR_INVALID_ARG;
   const int esz = elt_size(dtype);
@@ -276,7 +280,9 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int
   int st = check_cache(cache);
   if (st) return st;
   if ((st = check_spans(spans))) return st;
-  if (batch < 1 || q_len < 1 || w < 1 || layer < 0 || l0 < 0) return SPEECHKV_ERR_INVALID_ARG;
+  if (batch < 1 || q_len < 1 || q_len > kMaxRows || w < 1 || w > SPEECHKV_MAX_WINDOW ||
+      layer < 0 || l0 < 0)
+    return SPEECHKV_ERR_INVALID_ARG;
   if (mask_mode != SPEECHKV_MASK_WINDOW_END && mask_mode != SPEECHKV_MASK_WINDOW_START)
     return SPEECHKV_ERR_INVALID_ARG;
   if (spans->max_total_len > q_len) return SPEECHKV_ERR_INVALID_ARG;

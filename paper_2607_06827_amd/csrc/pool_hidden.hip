@@ -4,14 +4,20 @@
 // queries included, runs on the shortened sequence (plain causal attention
 // over it is prefill/decode attention with a window of 1).
 //
-// One wave per output row.  Lane l holds elements [(v*64 + l)*8, +8) of the
-// row for v < kVec, so every wave-wide load covers 1 KB (bf16) or 2 KB (fp32)
-// of contiguous memory.  Text rows and one-frame windows are bitwise copies.
-// A window's frames are pooled with an online softmax over their gate logits
-// u . h_j (fp32 dots reduced over the whole wave), in passes of a few frames
-// whose loads are all in flight together, so any w works.
+// Layout: each thread owns 8 consecutive elements (one 16-byte piece for
+// bf16) of a row for each of kVec slices, kTpr threads cover one row, and a
+// 256-thread block handles 256 / kTpr output rows (one row for hidden 2048
+// and 4096, so a row is spread over four waves).  Text rows and one-frame
+// windows are bitwise copies.  A window's frames are pooled with an online
+// softmax over the gate logits u . h_j in passes of four frames: every load
+// of a pass (the gate and all four frames) is issued before the first one is
+// used, each wave reduces its share of the dot products with cross-lane
+// operations, and the per-wave partial logits meet in LDS behind one barrier
+// per pass.  The loads are unconditional (row indices are clamped instead),
+// so no branch forces an early wait for outstanding loads.
 // The kernel moves each input byte once and writes each output byte once: it
-// is bound by HBM bandwidth.
+// is bound by HBM bandwidth.  bf16 rows are read with non-temporal loads
+// (streamed once, they need not stay in the caches).
 #include "kernels.hpp"
 
 namespace skv {
@@ -19,6 +25,8 @@ namespace skv {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kFrames = 4;  // frames per pass
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 // Sum over all 64 lanes, the same in every lane.
 __device__ __forceinline__ float wave_sum(float x) {
@@ -31,16 +39,31 @@ __device__ __forceinline__ float wave_sum(float x) {
   return __uint_as_float(p[0]) + __uint_as_float(p[1]);
 }
 
-template <typename T, int kVec>
+// One streamed 8-element piece of a hidden-state row.
+template <typename T>
+__device__ __forceinline__ void load_piece(Chunk<T>& x, const T* p) {
+  if constexpr (sizeof(T) == 2) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    x.raw = make_uint4(v[0], v[1], v[2], v[3]);
+  } else {
+    x.load(p);
+  }
+}
+
+template <typename T, int kTpr, int kVec, bool kGate>
 __global__ __launch_bounds__(256) void pool_hidden_kernel(PoolHiddenArgs a) {
-  constexpr int kWavesPerBlock = 4;
-  constexpr int kE = kVec * 8;  // elements per lane
-  // frames loaded together per pass: about 16 KB of a bf16 wave in flight
-  constexpr int kFrames = 16 / kVec < 8 ? 16 / kVec : 8;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  constexpr int kRows = 256 / kTpr;  // output rows per block
+  constexpr int kWavesPerRow = kTpr / 64;
+  constexpr int kE = kVec * 8;       // elements per thread
+  __shared__ float s_part[2][4][kFrames];  // [pass parity][wave][frame]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int lr = tid % kTpr;   // thread within its row
+  const int rib = tid / kTpr;  // row within the block
   const int b = blockIdx.y;
-  const int c = blockIdx.x * kWavesPerBlock + wave;  // output row
+  const int cb = blockIdx.x * kRows;
+  const int c = cb + rib;      // output row
 
   const int P = max(a.prefix_len[b], 0);
   const int T_ = max(a.speech_len[b], 0);
@@ -48,69 +71,93 @@ __global__ __launch_bounds__(256) void pool_hidden_kernel(PoolHiddenArgs a) {
   const int w = a.w;
   const int nW = (T_ + w - 1) / w;
   const int L = P + nW + N;
-  if (c == 0 && lane == 0 && a.out_len) a.out_len[b] = L;
-  if (c >= L || c >= a.out_cap) return;
+  if (blockIdx.x == 0 && tid == 0 && a.out_len) a.out_len[b] = L;
+  const int lim = min(L, a.out_cap);
+  if (cb >= lim) return;  // block-uniform
 
   const T* src = static_cast<const T*>(a.h) + (int64_t)b * a.stride_b;
   T* dst = static_cast<T*>(a.out) + (int64_t)b * a.out_stride_b + (int64_t)c * a.out_stride_s;
   auto row = [&](int s) { return src + (int64_t)min(s, a.raw_len - 1) * a.stride_s; };
+  auto elt = [&](int v) { return (v * kTpr + lr) * 8; };
 
-  // source rows of output row c: a text row, or the frames of window c - P
-  int f0, nf;
-  if (c < P) {
-    f0 = c;
-    nf = 1;
-  } else if (c >= P + nW) {
-    f0 = P + T_ + (c - P - nW);
-    nf = 1;
-  } else {
-    f0 = P + (c - P) * w;
-    nf = min(w, P + T_ - f0);
-  }
-  if (nf == 1) {  // bitwise copy
-    const T* s = row(f0);
+  // source rows of output row c: nf = 1 for a text row or a one-frame window
+  // (a copy), nf = 0 past the sequence's end or the buffer's capacity
+  const bool text_before = c < P, text_after = c >= P + nW;
+  const int f0 = text_before ? c : text_after ? P + T_ + (c - P - nW) : P + (c - P) * w;
+  const int nf = c >= lim ? 0 : (text_before || text_after) ? 1 : min(w, P + T_ - f0);
+
+  // block-uniform: does any row of this block pool a window of several frames?
+  const bool block_pools = w > 1 && cb < min(P + nW, lim) && cb + kRows > P;
+  if (!block_pools) {
+    Chunk<T> x[kVec];
 #pragma unroll
-    for (int v = 0; v < kVec; ++v) {
-      Chunk<T> x;
-      x.load(s + (v * 64 + lane) * 8);
-      x.store(dst + (v * 64 + lane) * 8);
-    }
+    for (int v = 0; v < kVec; ++v) load_piece(x[v], row(f0) + elt(v));
+    if (nf == 1)
+#pragma unroll
+      for (int v = 0; v < kVec; ++v) x[v].store(dst + elt(v));
     return;
   }
 
   float u[kE];
+  if constexpr (kGate) {
 #pragma unroll
-  for (int v = 0; v < kVec; ++v)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) u[v * 8 + e] = a.gate ? a.gate[(v * 64 + lane) * 8 + e] : 0.f;
+    for (int v = 0; v < kVec; ++v) {
+      const float4* g = reinterpret_cast<const float4*>(a.gate + elt(v));
+      const float4 g0 = g[0], g1 = g[1];
+      u[v * 8 + 0] = g0.x; u[v * 8 + 1] = g0.y; u[v * 8 + 2] = g0.z; u[v * 8 + 3] = g0.w;
+      u[v * 8 + 4] = g1.x; u[v * 8 + 5] = g1.y; u[v * 8 + 6] = g1.z; u[v * 8 + 7] = g1.w;
+    }
+  }
 
   float m = neg_inf(), l = 0.f, acc[kE];
 #pragma unroll
   for (int e = 0; e < kE; ++e) acc[e] = 0.f;
-  for (int base = 0; base < nf; base += kFrames) {
+  Chunk<T> first[kVec];  // frame 0: the output of a copy row
+  const int passes = (w + kFrames - 1) / kFrames;  // block-uniform
+  for (int p = 0; p < passes; ++p) {
+    const int base = p * kFrames;
     Chunk<T> x[kFrames][kVec];
 #pragma unroll
     for (int f = 0; f < kFrames; ++f) {
-      const T* s = row(f0 + min(base + f, nf - 1));  // frames past the window repeat its last
+      // frames past the window repeat its last one; copy and dead rows re-read their own row
+      const T* s = row(f0 + min(base + f, max(nf, 1) - 1));
 #pragma unroll
-      for (int v = 0; v < kVec; ++v) x[f][v].load(s + (v * 64 + lane) * 8);
+      for (int v = 0; v < kVec; ++v) load_piece(x[f][v], s + elt(v));
+    }
+    if (p == 0)
+#pragma unroll
+      for (int v = 0; v < kVec; ++v) first[v] = x[0][v];
+    if constexpr (kGate) {
+#pragma unroll
+      for (int f = 0; f < kFrames; ++f) {
+        float d = 0.f;
+#pragma unroll
+        for (int v = 0; v < kVec; ++v) {
+          float xf[8];
+          x[f][v].to_float(xf);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) d = __builtin_fmaf(u[v * 8 + e], xf[e], d);
+        }
+        d = wave_sum(d);
+        if (lane == 0) s_part[p & 1][wave][f] = d;
+      }
+      // two parity buffers: a wave that runs ahead writes the other one, and it
+      // cannot come back to this one before every wave has passed the next barrier
+      __syncthreads();
     }
     float logit[kFrames];
 #pragma unroll
     for (int f = 0; f < kFrames; ++f) {
-      float d = 0.f;
+      float d = 0.f;  // the zero gate: every frame weighs the same
+      if constexpr (kGate)
 #pragma unroll
-      for (int v = 0; v < kVec; ++v) {
-        float xf[8];
-        x[f][v].to_float(xf);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) d = __builtin_fmaf(u[v * 8 + e], xf[e], d);
-      }
-      logit[f] = base + f < nf ? wave_sum(d) * kLog2e : neg_inf();  // log2 units
+        for (int k = 0; k < kWavesPerRow; ++k) d += s_part[p & 1][rib * kWavesPerRow + k][f];
+      logit[f] = base + f < nf ? d * kLog2e : neg_inf();  // log2 units
     }
     float mx = m;
 #pragma unroll
     for (int f = 0; f < kFrames; ++f) mx = fmaxf(mx, logit[f]);
+    mx = fmaxf(mx, -1e30f);  // a row without frames keeps finite weights (it is never stored)
     const float corr = fast_exp2(m - mx);  // 0 on the first pass (m = -inf)
     l *= corr;
 #pragma unroll
@@ -118,14 +165,14 @@ __global__ __launch_bounds__(256) void pool_hidden_kernel(PoolHiddenArgs a) {
     m = mx;
 #pragma unroll
     for (int f = 0; f < kFrames; ++f) {
-      const float p = fast_exp2(logit[f] - m);  // 0 for frames past the window
-      l += p;
+      const float pw = fast_exp2(logit[f] - mx);  // 0 for frames past the window
+      l += pw;
 #pragma unroll
       for (int v = 0; v < kVec; ++v) {
         float xf[8];
         x[f][v].to_float(xf);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[v * 8 + e] = __builtin_fmaf(p, xf[e], acc[v * 8 + e]);
+        for (int e = 0; e < 8; ++e) acc[v * 8 + e] = __builtin_fmaf(pw, xf[e], acc[v * 8 + e]);
       }
     }
   }
@@ -135,23 +182,32 @@ __global__ __launch_bounds__(256) void pool_hidden_kernel(PoolHiddenArgs a) {
     float y[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) y[e] = acc[v * 8 + e] * inv;
-    Chunk<T> out;
-    out.from_float(y);
-    out.store(dst + (v * 64 + lane) * 8);
+    Chunk<T> o;
+    o.from_float(y);
+    if (nf == 1) o = first[v];
+    if (nf >= 1) o.store(dst + elt(v));
+  }
+}
+
+template <typename T, bool kGate>
+hipError_t launch_pool_hidden_t(const PoolHiddenArgs& a, int hidden, int batch, hipStream_t s) {
+  auto grid = [&](int rows_per_block) {
+    const int blocks = (a.max_out + rows_per_block - 1) / rows_per_block;
+    // at least one block per sequence: block 0 writes out_len even when every span is empty
+    return dim3((unsigned)(blocks > 0 ? blocks : 1), batch);
+  };
+  switch (hidden) {
+    case 512: return launch_struct(pool_hidden_kernel<T, 64, 1, kGate>, grid(4), dim3(256), s, a);
+    case 1024: return launch_struct(pool_hidden_kernel<T, 128, 1, kGate>, grid(2), dim3(256), s, a);
+    case 2048: return launch_struct(pool_hidden_kernel<T, 256, 1, kGate>, grid(1), dim3(256), s, a);
+    default: return launch_struct(pool_hidden_kernel<T, 256, 2, kGate>, grid(1), dim3(256), s, a);
   }
 }
 
 template <typename T>
-hipError_t launch_pool_hidden_t(const PoolHiddenArgs& a, int hidden, int batch, hipStream_t s) {
-  // at least one block per sequence: block 0 writes out_len even when every span is empty
-  const int blocks = (a.max_out + 3) / 4;
-  const dim3 grid((unsigned)(blocks > 0 ? blocks : 1), batch);
-  switch (hidden / 512) {
-    case 1: return launch_struct(pool_hidden_kernel<T, 1>, grid, dim3(256), s, a);
-    case 2: return launch_struct(pool_hidden_kernel<T, 2>, grid, dim3(256), s, a);
-    case 4: return launch_struct(pool_hidden_kernel<T, 4>, grid, dim3(256), s, a);
-    default: return launch_struct(pool_hidden_kernel<T, 8>, grid, dim3(256), s, a);
-  }
+hipError_t launch_pool_hidden_g(const PoolHiddenArgs& a, int hidden, int batch, hipStream_t s) {
+  return a.gate ? launch_pool_hidden_t<T, true>(a, hidden, batch, s)
+                : launch_pool_hidden_t<T, false>(a, hidden, batch, s);
 }
 
 }  // namespace
@@ -162,8 +218,8 @@ bool pool_hidden_supported(int hidden) {
 
 hipError_t launch_pool_hidden(const PoolHiddenArgs& a, int dtype, int hidden, int batch,
                               hipStream_t s) {
-  if (dtype == 1) return launch_pool_hidden_t<bf16_bits>(a, hidden, batch, s);
-  return launch_pool_hidden_t<float>(a, hidden, batch, s);
+  if (dtype == 1) return launch_pool_hidden_g<bf16_bits>(a, hidden, batch, s);
+  return launch_pool_hidden_g<float>(a, hidden, batch, s);
 }
 
 }  // namespace skv

@@ -32,6 +32,7 @@ DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MASK_WINDOW_END = 0
 MASK_WINDOW_START = 1
+MAX_WINDOW = 65536  # largest window size the pooling and attention calls take
 
 LIBRARY_PATH = _LIB_PATH
 

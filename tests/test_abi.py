@@ -197,3 +197,24 @@ def test_decode_rejects(kw, code):
 ])
 def test_prefill_rejects(kw, code):
     assert prefill(**kw) == code
+
+
+def test_window_and_row_count_bounds():
+    """w beyond SPEECHKV_MAX_WINDOW and row counts whose window count could
+    overflow 32-bit arithmetic are rejected by every pooling and attention call."""
+    big_w = skv.MAX_WINDOW + 1
+    assert pool(w=big_w) == E_ARG
+    assert pool_hidden(w=big_w) == E_ARG
+    assert prefill(w=big_w) == E_ARG
+    too_many = 2**31 - 1 - skv.MAX_WINDOW + 1
+    assert pool(raw_len=too_many) == E_ARG
+    assert pool_hidden(raw_len=too_many) == E_ARG
+    assert prefill(q_len=too_many) == E_ARG
+
+
+def test_binding_constants_match_header():
+    import re
+    defs = dict(re.findall(r"#define SPEECHKV_(\w+) \(?(-?\d+)\)?", open(HEADER).read()))
+    for name in ("OK", "ERR_INVALID_ARG", "ERR_UNSUPPORTED", "ERR_WORKSPACE", "ERR_ALIAS", "ERR_HIP",
+                 "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START", "MAX_WINDOW"):
+        assert int(defs[name]) == getattr(skv, name), name

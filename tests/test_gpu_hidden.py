@@ -79,6 +79,10 @@ CASES = {
     "speech-shorter-than-w": dict(P=[5], T=[3], N=[4], w=8, hidden=512),
     "zero-gate": dict(P=[4], T=[70], N=[3], w=4, hidden=2048, zero_gate=True),
     "sharp-gate": dict(P=[4, 1], T=[70, 33], N=[3, 2], w=4, hidden=2048, gate_scale=10.0),
+    "w5-one-frame-second-pass": dict(P=[2, 0], T=[41, 26], N=[3, 1], w=5, hidden=2048),
+    "w8-h4096-two-passes": dict(P=[3], T=[45], N=[2], w=8, hidden=4096),
+    "zero-gate-w12-h512": dict(P=[5, 2], T=[50, 13], N=[1, 4], w=12, hidden=512, zero_gate=True),
+    "zero-gate-f32-h1024": dict(P=[1], T=[23], N=[2], w=3, hidden=1024, dtype="f32", zero_gate=True),
     "varlen": dict(P=[0, 17, 3, 40], T=[150, 7, 91, 0], N=[9, 33, 0, 1], w=3, hidden=2048),
 }
 
