@@ -6,9 +6,11 @@ does.  It shares no code with the GPU library.
 """
 from .oracle import (  # noqa: F401
     attention,
+    attention_bwd,
     build,
     compressed_len,
     decode,
     num_threads,
     pool,
+    pool_bwd,
 )

@@ -47,6 +47,12 @@ def _load():
     lib.speechkv_oracle_decode.argtypes = [dp, dp, dp, ip, i, i, i, i, i,
                                            ctypes.c_double, dp, dp]
     lib.speechkv_oracle_decode.restype = None
+    lib.speechkv_oracle_attention_bwd.argtypes = [dp, dp, dp, i, i, i, i, i, i, ip, ip, ip, i,
+                                                  i, i, i, ctypes.c_double, dp, dp, dp, dp]
+    lib.speechkv_oracle_attention_bwd.restype = None
+    lib.speechkv_oracle_pool_bwd.argtypes = [dp, dp, i, i, i, i, ip, ip, ip, i, i, i, dp, dp, dp,
+                                             i, dp, dp, dp]
+    lib.speechkv_oracle_pool_bwd.restype = None
     lib.speechkv_oracle_compressed_len.argtypes = [i, i, i, i, i, i]
     lib.speechkv_oracle_compressed_len.restype = i
     lib.speechkv_oracle_num_threads.argtypes = []
@@ -156,3 +162,54 @@ def decode(q, k_hat, v_hat, clen, scale=None):
     lib.speechkv_oracle_decode(_dp(q), _dp(kh), _dp(vh), _ip(clen), B, Hq, Hkv, D, Lc,
                                float(scale), _dp(out), _dp(lse))
     return out, lse
+
+
+def attention_bwd(q, k_hat, v_hat, P, T, N, w, layer, l0, dout, mask_mode=0, scale=None):
+    """Gradient of `attention`'s output against dout: (dq, dk_hat, dv_hat).
+
+    q, dout: [B, Sq, Hq, D]; k_hat, v_hat: [B, Lc, Hkv, D].  Rows that see no
+    key and rows p >= P+T+N get dq = 0; key rows past a compressed length 0.
+    """
+    lib = _load()
+    q, kh, vh, go = _f64(q), _f64(k_hat), _f64(v_hat), _f64(dout)
+    B, Sq, Hq, D = q.shape
+    _, Lc, Hkv, D2 = kh.shape
+    assert D2 == D and vh.shape == kh.shape and go.shape == q.shape and Hq % Hkv == 0
+    P, T, N = _i32(P), _i32(T), _i32(N)
+    assert np.all(P + T + N <= Sq)
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(kh)
+    dv = np.zeros_like(vh)
+    lib.speechkv_oracle_attention_bwd(_dp(q), _dp(kh), _dp(vh), B, Sq, Hq, Hkv, D, Lc, _ip(P),
+                                      _ip(T), _ip(N), w, layer, l0, mask_mode, float(scale),
+                                      _dp(go), _dp(dq), _dp(dk), _dp(dv))
+    return dq, dk, dv
+
+
+def pool_bwd(k_raw, v_raw, P, T, N, w, layer, l0, u, dk_hat, dv_hat):
+    """Gradient of `pool` against (dk_hat, dv_hat): (dk_raw, dv_raw, du).
+
+    k_raw, v_raw: [B, S, Hkv, D]; u: [Hkv, D] or None (the zero gate, whose
+    gradient du is still returned); dk_hat, dv_hat: [B, Lc, Hkv, D].
+    """
+    lib = _load()
+    k, v, gk, gv = _f64(k_raw), _f64(v_raw), _f64(dk_hat), _f64(dv_hat)
+    B, S, H, D = k.shape
+    Lc = gk.shape[1]
+    assert v.shape == k.shape and gk.shape == (B, Lc, H, D) and gv.shape == gk.shape
+    P, T, N = _i32(P), _i32(T), _i32(N)
+    assert np.all(P + T + N <= S)
+    assert Lc >= max(compressed_len(int(P[b]), int(T[b]), int(N[b]), w, layer, l0)
+                     for b in range(B))
+    uu = None if u is None else _f64(u)
+    if uu is not None:
+        assert uu.shape == (H, D)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    du = np.zeros((H, D), np.float64)
+    lib.speechkv_oracle_pool_bwd(_dp(k), _dp(v), B, S, H, D, _ip(P), _ip(T), _ip(N), w, layer,
+                                 l0, _dp(uu) if uu is not None else None, _dp(gk), _dp(gv), Lc,
+                                 _dp(dk), _dp(dv), _dp(du))
+    return dk, dv, du
