@@ -18,6 +18,11 @@
  *   speechkv_prefill_attn  full-resolution queries over the cache (Eq. 5 + mask)
  *   speechkv_pool_hidden   the same pooling applied to whole hidden states
  *                          (HS Compression, Sec. IV-A method (4))
+ * and two more carry its training (Sec. III-C: the pooling runs inside the
+ * forward pass and is optimised jointly with the model):
+ *   speechkv_prefill_attn_bwd  gradients of speechkv_prefill_attn: dQ, dK^, dV^
+ *   speechkv_pool_kv_bwd       gradients of the pooling: raw dK, dV and the
+ *                              gate's du
  *
  * Conventions shared by every call
  * --------------------------------
@@ -285,6 +290,100 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
                           const speechkv_spans* spans, int32_t w, int32_t layer,
                           int32_t l0, int32_t mask_mode, float scale, void* out,
                           float* lse, void* stream);
+
+/*
+ * speechkv_prefill_attn_bwd - gradients of speechkv_prefill_attn with respect
+ * to the queries and the compressed keys and values (training, Sec. III-C;
+ * the chain rule of Eq. 5 under the same mask).
+ *
+ * Given the forward's inputs, its output `out` and log-sum-exp `lse`, and the
+ * gradient `dout` of the output, with P = softmax(scale q k^T) over the keys
+ * each row sees:
+ *   Delta_p = dout_p . out_p,  dZ = P o (dout v^T - Delta)
+ *   dq = scale dZ k^,  dk^ = scale dZ^T q,  dv^ = P^T dout
+ * (key gradients summed over the query heads of each KV head).  P is
+ * recomputed from lse; nothing of size rows x keys is stored.
+ *
+ * q, out, dout   device, element type cache->dtype,
+ *                [batch][q_len][num_q_heads][head_dim], dense.
+ * lse            device fp32 [batch][num_q_heads][q_len], as the forward wrote it.
+ * cache, spans, w, layer, l0, mask_mode, scale  as for the forward call.
+ * dq             device, element type cache->dtype, layout of q.  Rows
+ *                p >= P+T+N are not written; a row that sees no key gets 0.
+ * dk_hat, dv_hat device fp32 [batch][hat_capacity][num_kv_heads][head_dim]:
+ *                row c of sequence b is the gradient of cache slot c.  Rows
+ *                c >= min(P+nW+N, hat_capacity) are not written.  Caller
+ *                obligation: hat_capacity >= P+nW+N for the full gradient.
+ * workspace      device, >= speechkv_prefill_attn_bwd_workspace_bytes bytes,
+ *                16-byte aligned; receives Delta.
+ * Nothing written may overlap an input or another output (ALIAS).
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, ALIAS, HIP.
+ */
+int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads,
+                              int32_t q_len, const speechkv_paged_kv* cache,
+                              const speechkv_spans* spans, int32_t w,
+                              int32_t layer, int32_t l0, int32_t mask_mode,
+                              float scale, const void* out, const float* lse,
+                              const void* dout, void* dq, float* dk_hat,
+                              float* dv_hat, int32_t hat_capacity,
+                              void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* Workspace bytes of speechkv_prefill_attn_bwd (one fp32 per query row and
+ * head), or 0 for invalid arguments.  Host only. */
+size_t speechkv_prefill_attn_bwd_workspace_bytes(int32_t batch,
+                                                 int32_t num_q_heads,
+                                                 int32_t q_len);
+
+/*
+ * speechkv_pool_kv_bwd - gradients of speechkv_pool_kv with respect to the
+ * raw keys, the raw values and the gate vectors (training, Sec. III-C; the
+ * chain rule of Eq. 4).
+ *
+ * For window i of sequence b, KV head g, with frames j, logits s_j = u_g . k_j
+ * and alpha = softmax_j(s):
+ *   dalpha_j = dk^_i . k_j + dv^_i . v_j
+ *   ds_j = alpha_j (dalpha_j - sum_j' alpha_j' dalpha_j')
+ *   dk_j = alpha_j dk^_i + ds_j u_g,   dv_j = alpha_j dv^_i
+ *   du_g = sum over sequences, windows and frames of ds_j k_j
+ * A text row (and a one-frame window) was copied: its gradient is that of the
+ * slot it became.  With w_eff = 1 every raw row gets its slot's gradient and
+ * du = 0.
+ *
+ * k_raw, v_raw   device, element type dtype, strides as for speechkv_pool_kv.
+ * num_kv_heads, head_dim  the raw tensors' heads and head size (64 or 128);
+ *                num_kv_heads * head_dim / 8 must divide 256 (UNSUPPORTED).
+ * spans, w, gate_u, layer, l0  as for the forward call (gate_u NULL: zero gate).
+ * dk_hat, dv_hat device fp32 [batch][hat_capacity][num_kv_heads][head_dim],
+ *                e.g. from speechkv_prefill_attn_bwd.  Caller obligation:
+ *                hat_capacity >= P+nW+N (slots at or past it count as 0).
+ * dk_raw, dv_raw device, element type dtype, the strides of k_raw: receive
+ *                the gradients of rows [0, P+T+N); other rows are not written.
+ * du             device fp32 [num_kv_heads][head_dim] receiving the gate
+ *                gradient, or NULL to skip it.
+ * workspace      device, >= speechkv_pool_kv_bwd_workspace_bytes bytes,
+ *                16-byte aligned, when du is not NULL (per-block partial sums,
+ *                added in a fixed order: the result is deterministic).
+ * Nothing written may overlap an input or another output (ALIAS).
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, ALIAS, HIP.
+ */
+int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw,
+                         int64_t stride_b, int64_t stride_s, int64_t stride_h,
+                         int32_t batch, int32_t raw_len, int32_t num_kv_heads,
+                         int32_t head_dim, int32_t dtype,
+                         const speechkv_spans* spans, int32_t w,
+                         const float* gate_u, int32_t layer, int32_t l0,
+                         const float* dk_hat, const float* dv_hat,
+                         int32_t hat_capacity, void* dk_raw, void* dv_raw,
+                         float* du, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* Workspace bytes of speechkv_pool_kv_bwd with a gate gradient, for
+ * max_total_len = spans->max_total_len, or 0 for invalid or unsupported
+ * arguments.  Host only. */
+size_t speechkv_pool_kv_bwd_workspace_bytes(int32_t batch, int32_t max_total_len,
+                                            int32_t num_kv_heads,
+                                            int32_t head_dim);
 
 /* Length of the compressed sequence, P + ceil(T / w_eff) + N (Sec. III-B,
  * Sec. III-C), or -1 for a negative length, w < 1 or negative layer/l0.

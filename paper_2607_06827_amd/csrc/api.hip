@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "kernels.hpp"
+#include "kernels_bwd.hpp"
 
 namespace {
 
@@ -315,6 +316,169 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int
   a.scale_log2 = scale * 1.4426950408889634f;
   return status_of(skv::launch_prefill(a, cache->dtype, cache->head_dim, group, batch,
                                        static_cast<hipStream_t>(stream)));
+}
+
+size_t speechkv_prefill_attn_bwd_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t q_len) {
+  if (batch < 1 || num_q_heads < 1 || q_len < 1) return 0;
+  return (size_t)batch * num_q_heads * q_len * sizeof(float);
+}
+
+int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                              const speechkv_paged_kv* cache, const speechkv_spans* spans, int32_t w,
+                              int32_t layer, int32_t l0, int32_t mask_mode, float scale,
+                              const void* out, const float* lse, const void* dout, void* dq,
+                              float* dk_hat, float* dv_hat, int32_t hat_capacity, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (!q || !out || !lse || !dout || !dq || !dk_hat || !dv_hat) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_cache(cache);
+  if (st) return st;
+  if ((st = check_spans(spans))) return st;
+  if (batch < 1 || q_len < 1 || q_len > kMaxRows || w < 1 || w > SPEECHKV_MAX_WINDOW ||
+      layer < 0 || l0 < 0 || hat_capacity < 1)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (mask_mode != SPEECHKV_MASK_WINDOW_END && mask_mode != SPEECHKV_MASK_WINDOW_START)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > q_len) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || scale > 3.0e38f) return SPEECHKV_ERR_INVALID_ARG;
+  if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
+  const int group = group_of(num_q_heads, cache->num_kv_heads);
+  if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
+  const size_t need = speechkv_prefill_attn_bwd_workspace_bytes(batch, num_q_heads, q_len);
+  if (!workspace || workspace_bytes < need) return SPEECHKV_ERR_WORKSPACE;
+  if (!aligned16(q) || !aligned16(out) || !aligned16(dout) || !aligned16(dq) || !aligned16(dk_hat) ||
+      !aligned16(dv_hat) || !aligned16(workspace) || (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return SPEECHKV_ERR_INVALID_ARG;
+  const int esz = elt_size(cache->dtype);
+  const int64_t qbytes = (int64_t)batch * q_len * num_q_heads * cache->head_dim * esz;
+  const int64_t hbytes = (int64_t)batch * hat_capacity * cache->num_kv_heads * cache->head_dim * 4;
+  // outputs must not overlap each other or the inputs they are computed from
+  const void* outs[4] = {dq, dk_hat, dv_hat, workspace};
+  const int64_t osz[4] = {qbytes, hbytes, hbytes, (int64_t)need};
+  const void* ins[4] = {q, out, dout, lse};
+  const int64_t isz[4] = {qbytes, qbytes, qbytes, (int64_t)batch * num_q_heads * q_len * 4};
+  for (int i = 0; i < 4; ++i) {
+    for (int k = i + 1; k < 4; ++k)
+      if (overlaps(outs[i], osz[i], outs[k], osz[k])) return SPEECHKV_ERR_ALIAS;
+    for (int k = 0; k < 4; ++k)
+      if (overlaps(outs[i], osz[i], ins[k], isz[k])) return SPEECHKV_ERR_ALIAS;
+    if (overlaps(outs[i], osz[i], cache->k_pages, page_pool_bytes(cache)) ||
+        overlaps(outs[i], osz[i], cache->v_pages, page_pool_bytes(cache)))
+      return SPEECHKV_ERR_ALIAS;
+  }
+  if (spans->max_total_len == 0) return SPEECHKV_OK;
+  const int rows_per_tile = skv::prefill_bwd_rows_per_tile(group);
+  const int64_t q_tiles = (spans->max_total_len + rows_per_tile - 1) / rows_per_tile;
+  const int64_t keys = spans->max_total_len < hat_capacity ? spans->max_total_len : hat_capacity;
+  const int64_t key_tiles = (keys + 31) / 32;
+  if ((int64_t)batch * cache->num_kv_heads * q_tiles > INT32_MAX ||
+      (int64_t)batch * cache->num_kv_heads * key_tiles > INT32_MAX)
+    return SPEECHKV_ERR_INVALID_ARG;
+  skv::PrefillBwdArgs a;
+  a.q = q;
+  a.out = out;
+  a.dout = dout;
+  a.lse = lse;
+  a.k_pages = cache->k_pages;
+  a.v_pages = cache->v_pages;
+  a.table = cache->block_table;
+  a.pv = view_of(cache);
+  a.prefix_len = spans->prefix_len;
+  a.speech_len = spans->speech_len;
+  a.suffix_len = spans->suffix_len;
+  a.w_eff = layer >= l0 ? w : 1;
+  a.mask_mode = mask_mode;
+  a.q_len = q_len;
+  a.num_q_heads = num_q_heads;
+  a.num_q_tiles = (int)q_tiles;
+  a.num_key_tiles = (int)key_tiles;
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.delta = static_cast<float*>(workspace);
+  a.dq = dq;
+  a.dk_hat = dk_hat;
+  a.dv_hat = dv_hat;
+  a.hat_cap = hat_capacity;
+  return status_of(skv::launch_prefill_bwd(a, cache->dtype, cache->head_dim, group, batch,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+size_t speechkv_pool_kv_bwd_workspace_bytes(int32_t batch, int32_t max_total_len,
+                                            int32_t num_kv_heads, int32_t head_dim) {
+  if (batch < 1 || max_total_len < 0 || num_kv_heads < 1) return 0;
+  const int spb = skv::pool_bwd_slots_per_block(num_kv_heads, head_dim);
+  if (spb == 0) return 0;
+  const int64_t blocks = max_total_len > 0 ? (max_total_len + spb - 1) / spb : 1;
+  return (size_t)batch * blocks * num_kv_heads * head_dim * sizeof(float);
+}
+
+int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
+                         int64_t stride_h, int32_t batch, int32_t raw_len, int32_t num_kv_heads,
+                         int32_t head_dim, int32_t dtype, const speechkv_spans* spans, int32_t w,
+                         const float* gate_u, int32_t layer, int32_t l0, const float* dk_hat,
+                         const float* dv_hat, int32_t hat_capacity, void* dk_raw, void* dv_raw,
+                         float* du, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!k_raw || !v_raw || !dk_hat || !dv_hat || !dk_raw || !dv_raw) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_spans(spans);
+  if (st) return st;
+  if (dtype != SPEECHKV_DTYPE_F32 && dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
+  if (head_dim != 64 && head_dim != 128) return SPEECHKV_ERR_UNSUPPORTED;
+  if (num_kv_heads < 1) return SPEECHKV_ERR_INVALID_ARG;
+  const int spb = skv::pool_bwd_slots_per_block(num_kv_heads, head_dim);
+  if (spb == 0) return SPEECHKV_ERR_UNSUPPORTED;
+  if (batch < 1 || batch > kMaxGrid || raw_len < 1 || raw_len > kMaxRows || w < 1 ||
+      w > SPEECHKV_MAX_WINDOW || layer < 0 || l0 < 0 || hat_capacity < 1)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (stride_b < 0 || stride_s < 0 || stride_h < 0) return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > raw_len) return SPEECHKV_ERR_INVALID_ARG;
+  const int esz = elt_size(dtype);
+  const int64_t per16 = 16 / esz;
+  if (stride_b % per16 || stride_s % per16 || stride_h % per16) return SPEECHKV_ERR_INVALID_ARG;
+  if (!aligned16(k_raw) || !aligned16(v_raw) || !aligned16(dk_raw) || !aligned16(dv_raw) ||
+      !aligned16(dk_hat) || !aligned16(dv_hat) || (gate_u && !aligned16(gate_u)) || (du && !aligned16(du)))
+    return SPEECHKV_ERR_INVALID_ARG;
+  const size_t need = du ? speechkv_pool_kv_bwd_workspace_bytes(batch, spans->max_total_len,
+                                                                num_kv_heads, head_dim)
+                         : 0;
+  if (du && (!workspace || workspace_bytes < need || !aligned16(workspace))) return SPEECHKV_ERR_WORKSPACE;
+  const int64_t raw_bytes = ((int64_t)(batch - 1) * stride_b + (int64_t)(raw_len - 1) * stride_s +
+                             (int64_t)(num_kv_heads - 1) * stride_h + head_dim) * esz;
+  const int64_t hbytes = (int64_t)batch * hat_capacity * num_kv_heads * head_dim * 4;
+  const int64_t ubytes = (int64_t)num_kv_heads * head_dim * 4;
+  const void* outs[4] = {dk_raw, dv_raw, du, du ? workspace : nullptr};
+  const int64_t osz[4] = {raw_bytes, raw_bytes, ubytes, (int64_t)need};
+  const void* ins[5] = {k_raw, v_raw, dk_hat, dv_hat, gate_u};
+  const int64_t isz[5] = {raw_bytes, raw_bytes, hbytes, hbytes, ubytes};
+  for (int i = 0; i < 4; ++i) {
+    if (!outs[i]) continue;
+    for (int k = i + 1; k < 4; ++k)
+      if (outs[k] && overlaps(outs[i], osz[i], outs[k], osz[k])) return SPEECHKV_ERR_ALIAS;
+    for (int k = 0; k < 5; ++k)
+      if (ins[k] && overlaps(outs[i], osz[i], ins[k], isz[k])) return SPEECHKV_ERR_ALIAS;
+  }
+  skv::PoolBwdArgs a;
+  a.k_raw = k_raw;
+  a.v_raw = v_raw;
+  a.stride_b = stride_b;
+  a.stride_s = stride_s;
+  a.stride_h = stride_h;
+  a.raw_len = raw_len;
+  a.prefix_len = spans->prefix_len;
+  a.speech_len = spans->speech_len;
+  a.suffix_len = spans->suffix_len;
+  a.w_eff = layer >= l0 ? w : 1;
+  a.kv_heads = num_kv_heads;
+  a.gate = gate_u;
+  a.dk_hat = dk_hat;
+  a.dv_hat = dv_hat;
+  a.hat_cap = hat_capacity;
+  a.dk_raw = dk_raw;
+  a.dv_raw = dv_raw;
+  a.du = du;
+  a.du_part = du ? static_cast<float*>(workspace) : nullptr;
+  a.max_out = spans->max_total_len;
+  a.slots_per_block = spb;
+  a.blocks_per_seq = spans->max_total_len > 0 ? (spans->max_total_len + spb - 1) / spb : 1;
+  return status_of(skv::launch_pool_bwd(a, dtype, head_dim, batch, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

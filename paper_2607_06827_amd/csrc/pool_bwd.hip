@@ -1,0 +1,227 @@
+// Backward of the window pooling (arXiv 2607.06827, Sec. III-B, Eq. 4; Sec.
+// III-C: the gate is trained jointly with the model).
+//
+// For window i with frames j, logits s_j = u_g . k_j, alpha = softmax(s) and
+// the gradients dK^_i, dV^_i of its pooled row:
+//   dalpha_j = dK^_i . k_j + dV^_i . v_j
+//   ds_j     = alpha_j (dalpha_j - sum_j' alpha_j' dalpha_j')
+//   dk_j     = alpha_j dK^_i + ds_j u_g,    dv_j = alpha_j dV^_i
+//   du_g    += ds_j k_j                    (over every sequence and window)
+// A text row (or a one-frame window) was copied, so its gradient is that of
+// the row it became.
+//
+// Layout: each thread owns 8 consecutive elements of one KV head; D/8 threads
+// cover a head, kv_heads * D/8 a slot of the compressed sequence, and a block
+// walks kIters groups of 256 / (kv_heads * D/8) slots of one sequence.  Every
+// raw row is read at most twice (once more for windows longer than four
+// frames) and every gradient row written once: the kernel is bound by HBM
+// bandwidth.  The gate gradient is kept per thread, summed over the block in
+// LDS into one partial per block, and the partials are summed by a second
+// kernel in a fixed order, so the result does not depend on scheduling.
+#include "kernels.hpp"
+#include "kernels_bwd.hpp"
+
+namespace skv {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kIters = 8;  // slot groups per block
+
+template <int D>
+constexpr int lanes_per_head() { return D / 8; }
+
+template <typename T, int D, bool kGate>
+__global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
+  constexpr int kLanes = lanes_per_head<D>();
+  const int heads = a.kv_heads;
+  const int per_slot = heads * kLanes;   // threads per slot (divides 256)
+  const int slot_lanes = 256 / per_slot;
+  const int tid = threadIdx.x;
+  const int sl = tid / per_slot, u = tid % per_slot;
+  const int g = u / kLanes, j = u % kLanes;
+  const int b = blockIdx.y;
+
+  const int P = max(a.prefix_len[b], 0);
+  const int S = max(a.speech_len[b], 0);
+  const int N = max(a.suffix_len[b], 0);
+  const int w = a.w_eff;
+  const int nW = (S + w - 1) / w;
+  const int len = min(min(P + nW + N, a.max_out), a.hat_cap);
+
+  const int64_t base = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h + 8 * j;
+  const T* kr = static_cast<const T*>(a.k_raw) + base;
+  const T* vr = static_cast<const T*>(a.v_raw) + base;
+  T* dkr = static_cast<T*>(a.dk_raw) + base;
+  T* dvr = static_cast<T*>(a.dv_raw) + base;
+  auto at = [&](int s) { return (int64_t)min(s, a.raw_len - 1) * a.stride_s; };
+
+  float uu[8];
+  if constexpr (kGate) {
+    const float4* gp = reinterpret_cast<const float4*>(a.gate + (int64_t)g * D + 8 * j);
+    const float4 u0 = gp[0], u1 = gp[1];
+    uu[0] = u0.x; uu[1] = u0.y; uu[2] = u0.z; uu[3] = u0.w;
+    uu[4] = u1.x; uu[5] = u1.y; uu[6] = u1.z; uu[7] = u1.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) uu[e] = 0.f;
+  }
+  float du[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) du[e] = 0.f;
+
+  for (int k = 0; k < kIters; ++k) {
+    const int c = (blockIdx.x * kIters + k) * slot_lanes + sl;
+    if (sl >= slot_lanes || c >= len) continue;
+    const bool text_before = c < P, text_after = c >= P + nW;
+    const int src = text_before ? c : text_after ? P + S + (c - P - nW) : P + (c - P) * w;
+    const int n = (text_before || text_after) ? 1 : min(w, P + S - src);
+    if (src + n > a.raw_len) continue;  // a broken caller obligation: rows left alone
+
+    // gradient of pooled row c (fp32)
+    float gk[8], gv[8];
+    const float* hk = a.dk_hat + (((int64_t)b * a.hat_cap + c) * heads + g) * D + 8 * j;
+    const float* hv = a.dv_hat + (((int64_t)b * a.hat_cap + c) * heads + g) * D + 8 * j;
+    {
+      const float4 k0 = reinterpret_cast<const float4*>(hk)[0], k1 = reinterpret_cast<const float4*>(hk)[1];
+      const float4 v0 = reinterpret_cast<const float4*>(hv)[0], v1 = reinterpret_cast<const float4*>(hv)[1];
+      gk[0] = k0.x; gk[1] = k0.y; gk[2] = k0.z; gk[3] = k0.w; gk[4] = k1.x; gk[5] = k1.y; gk[6] = k1.z; gk[7] = k1.w;
+      gv[0] = v0.x; gv[1] = v0.y; gv[2] = v0.z; gv[3] = v0.w; gv[4] = v1.x; gv[5] = v1.y; gv[6] = v1.z; gv[7] = v1.w;
+    }
+    if (n == 1) {  // a copied row: weight exactly 1, no logit path
+      Chunk<T> ok, ov;
+      ok.from_float(gk);
+      ov.from_float(gv);
+      ok.store(dkr + at(src));
+      ov.store(dvr + at(src));
+      continue;
+    }
+
+    // frames f0..f0+3 (past the window: its last frame, weight 0), their log2
+    // logits and dalpha
+    Chunk<T> kc[4], vc[4];
+    float ls[4], da[4];
+    auto group = [&](int f0) __attribute__((always_inline)) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int64_t o = at(src + min(f0 + t, n - 1));
+        kc[t].load(kr + o);
+        vc[t].load(vr + o);
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float kf[8], vf[8];
+        kc[t].to_float(kf);
+        vc[t].to_float(vf);
+        float s = 0.f, d = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          s = __builtin_fmaf(uu[e], kf[e], s);
+          d = __builtin_fmaf(gk[e], kf[e], __builtin_fmaf(gv[e], vf[e], d));
+        }
+        ls[t] = f0 + t < n ? group_sum<kLanes>(s) * kLog2e : neg_inf();
+        da[t] = group_sum<kLanes>(d);
+      }
+    };
+    // pass 1: the window's softmax normaliser Z and sum_j alpha_j dalpha_j
+    float m = neg_inf(), z = 0.f, y = 0.f;
+    for (int f0 = 0; f0 < n; f0 += 4) {
+      group(f0);
+      const float mx = fmaxf(m, fmaxf(fmaxf(ls[0], ls[1]), fmaxf(ls[2], ls[3])));
+      const float corr = fast_exp2(m - mx);  // 0 on the first group
+      z *= corr;
+      y *= corr;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float p = fast_exp2(ls[t] - mx);  // 0 past the window
+        z += p;
+        y = __builtin_fmaf(p, da[t], y);
+      }
+      m = mx;
+    }
+    const float inv = 1.f / z, mean = y * inv;
+    // pass 2: the frame gradients (a window of at most four frames is still
+    // in registers from pass 1)
+    for (int f0 = 0; f0 < n; f0 += 4) {
+      if (n > 4) group(f0);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float al = fast_exp2(ls[t] - m) * inv;
+        const float ds = al * (da[t] - mean);
+        float kf[8], gkf[8], gvf[8];
+        kc[t].to_float(kf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          gkf[e] = __builtin_fmaf(ds, uu[e], al * gk[e]);
+          gvf[e] = al * gv[e];
+          du[e] = __builtin_fmaf(ds, kf[e], du[e]);  // ds = 0 past the window
+        }
+        if (f0 + t < n) {
+          Chunk<T> ok, ov;
+          ok.from_float(gkf);
+          ov.from_float(gvf);
+          const int64_t o = at(src + f0 + t);
+          ok.store(dkr + o);
+          ov.store(dvr + o);
+        }
+      }
+    }
+  }
+
+  if (!a.du_part) return;
+  // this block's gate gradient: the slot lanes' sums, in LDS, in a fixed order
+  __shared__ float s_du[256 * 8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s_du[tid * 8 + e] = du[e];
+  __syncthreads();
+  if (tid < per_slot) {
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    for (int q = 0; q < slot_lanes; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += s_du[(q * per_slot + tid) * 8 + e];
+    float* dst = a.du_part + ((int64_t)b * a.blocks_per_seq + blockIdx.x) * heads * D + g * D + 8 * j;
+    reinterpret_cast<float4*>(dst)[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    reinterpret_cast<float4*>(dst)[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  }
+}
+
+// du[i] = sum over the per-block partials, in block order.
+__global__ __launch_bounds__(256) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int p = 0; p < parts; ++p) s += part[(int64_t)p * n + i];
+  du[i] = s;
+}
+
+template <typename T, int D>
+hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
+  const dim3 grid((unsigned)a.blocks_per_seq, batch);
+  hipError_t e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true>, grid, dim3(256), s, a)
+                        : launch_struct(pool_bwd_kernel<T, D, false>, grid, dim3(256), s, a);
+  if (e != hipSuccess || !a.du) return e;
+  const int n = a.kv_heads * D;
+  hipLaunchKernelGGL(du_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a.du_part,
+                     batch * a.blocks_per_seq, n, a.du);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int pool_bwd_slots_per_block(int kv_heads, int head_dim) {
+  if (head_dim != 64 && head_dim != 128) return 0;
+  const int per_slot = kv_heads * (head_dim / 8);
+  if (kv_heads < 1 || per_slot > 256 || 256 % per_slot) return 0;
+  return (256 / per_slot) * kIters;
+}
+
+hipError_t launch_pool_bwd(const PoolBwdArgs& a, int dtype, int head_dim, int batch,
+                           hipStream_t s) {
+  if (dtype == 1)
+    return head_dim == 128 ? launch_t<bf16_bits, 128>(a, batch, s) : launch_t<bf16_bits, 64>(a, batch, s);
+  return head_dim == 128 ? launch_t<float, 128>(a, batch, s) : launch_t<float, 64>(a, batch, s);
+}
+
+}  // namespace skv

@@ -11,7 +11,10 @@
 //   slot P + nW + m            copy raw row P + T + m                (bitwise)
 // The gate logit u_g . k_j is a 16-lane (8-lane for D = 64) DPP reduction.
 // The window softmax is computed online over groups of four frames so that
-// eight loads are in flight per lane; a one-frame window is a copy.
+// eight loads are in flight per lane; a one-frame window is a copy.  The
+// loads are unconditional (frame indices are clamped, frames past the window
+// get weight 0) and the block-table entry is checked only before the stores,
+// so no branch makes a lane wait for one load before issuing the next.
 // The kernel reads each raw row once and writes each cache row once: it is
 // bound by HBM bandwidth.
 #include "kernels.hpp"
@@ -20,7 +23,7 @@ namespace skv {
 
 namespace {
 
-template <typename T, int D>
+template <typename T, int D, bool kGate>
 __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   constexpr int kLanes = D / 8;          // lanes per unit
   constexpr int kUnits = 256 / kLanes;   // units per block
@@ -44,49 +47,42 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   if (c64 >= len || c64 >= a.max_out) return;
   const int c = (int)c64;
 
-  int src, frames;
-  if (c < P) {
-    src = c;
-    frames = 1;
-  } else if (c < P + nW) {
-    src = P + (c - P) * w;
-    frames = min(w, P + S - src);
-  } else {
-    src = P + S + (c - P - nW);
-    frames = 1;
-  }
-  if (src + frames > a.raw_len) return;
-  const int64_t page = page_of(a.table, b, c, a.pv);
-  if (page < 0) return;
-  const int64_t dst = page_row<D>(page, g, c & ((1 << a.pv.page_shift) - 1), a.pv) + 8 * j;
+  const bool text_before = c < P, text_after = c >= P + nW;
+  const int src = text_before ? c : text_after ? P + S + (c - P - nW) : P + (c - P) * w;
+  const int frames = (text_before || text_after) ? 1 : min(w, P + S - src);
+  // page of slot c: the entry is loaded now and checked only before the stores
+  const int idx = c >> a.pv.page_shift;
+  const int32_t entry = a.table[(int64_t)b * a.pv.max_pages + min(idx, a.pv.max_pages - 1)];
 
   const T* kr = static_cast<const T*>(a.k_raw) + b * a.stride_b + g * a.stride_h + 8 * j;
   const T* vr = static_cast<const T*>(a.v_raw) + b * a.stride_b + g * a.stride_h + 8 * j;
-  T* kd = static_cast<T*>(a.k_pages) + dst;
-  T* vd = static_cast<T*>(a.v_pages) + dst;
+  auto at = [&](int s) { return (int64_t)min(s, a.raw_len - 1) * a.stride_s; };
+  auto dst = [&]() {
+    return page_row<D>(entry, g, c & ((1 << a.pv.page_shift) - 1), a.pv) + 8 * j;
+  };
+  // rows past the raw tensor (a broken caller obligation) or without a page are skipped
+  auto writable = [&]() {
+    return src + frames <= a.raw_len && idx < a.pv.max_pages && entry >= 0 &&
+           entry < a.pv.num_pages;
+  };
 
   if (frames == 1) {  // text row or one-frame window: weight exactly 1
     Chunk<T> kc, vc;
-    kc.load(kr + src * a.stride_s);
-    vc.load(vr + src * a.stride_s);
-    kc.store(kd);
-    vc.store(vd);
+    kc.load(kr + at(src));
+    vc.load(vr + at(src));
+    if (writable()) {
+      kc.store(static_cast<T*>(a.k_pages) + dst());
+      vc.store(static_cast<T*>(a.v_pages) + dst());
+    }
     return;
   }
 
-  // gate slice of this lane, pre-multiplied by log2(e) so that exp2 gives the
-  // natural-base softmax of the logits
   float u[8];
-  if (a.gate) {
+  if constexpr (kGate) {
     const float4* gp = reinterpret_cast<const float4*>(a.gate + (int64_t)g * D + 8 * j);
-    float4 u0 = gp[0], u1 = gp[1];
+    const float4 u0 = gp[0], u1 = gp[1];
     u[0] = u0.x; u[1] = u0.y; u[2] = u0.z; u[3] = u0.w;
     u[4] = u1.x; u[5] = u1.y; u[6] = u1.z; u[7] = u1.w;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) u[i] *= kLog2e;
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) u[i] = 0.f;
   }
 
   float m = neg_inf(), l = 0.f, ak[8], av[8];
@@ -94,26 +90,25 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   for (int i = 0; i < 8; ++i) ak[i] = av[i] = 0.f;
 
   for (int f0 = 0; f0 < frames; f0 += 4) {
+    // all eight loads in flight; frames past the window repeat its last one
     Chunk<T> kc[4], vc[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      if (f0 + t < frames) {
-        kc[t].load(kr + (int64_t)(src + f0 + t) * a.stride_s);
-        vc[t].load(vr + (int64_t)(src + f0 + t) * a.stride_s);
-      } else {
-        kc[t].zero();
-        vc[t].zero();
-      }
+      const int64_t o = at(src + min(f0 + t, frames - 1));
+      kc[t].load(kr + o);
+      vc[t].load(vr + o);
     }
     float kf[4][8], s[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       kc[t].to_float(kf[t]);
       float part = 0.f;
+      if constexpr (kGate) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) part += u[i] * kf[t][i];
-      s[t] = group_sum<kLanes>(part);
-      if (f0 + t >= frames) s[t] = neg_inf();
+        for (int i = 0; i < 8; ++i) part = __builtin_fmaf(u[i], kf[t][i], part);
+        part = group_sum<kLanes>(part);
+      }
+      s[t] = f0 + t < frames ? part * kLog2e : neg_inf();  // log2 units
     }
     const float mn = fmaxf(m, fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
     const float corr = fast_exp2(m - mn);  // m = -inf on the first group gives 0
@@ -131,8 +126,8 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
       l += p;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        ak[i] += p * kf[t][i];
-        av[i] += p * vf[i];
+        ak[i] = __builtin_fmaf(p, kf[t][i], ak[i]);
+        av[i] = __builtin_fmaf(p, vf[i], av[i]);
       }
     }
     m = mn;
@@ -146,8 +141,10 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   Chunk<T> ko, vo;
   ko.from_float(ak);
   vo.from_float(av);
-  ko.store(kd);
-  vo.store(vd);
+  if (writable()) {
+    ko.store(static_cast<T*>(a.k_pages) + dst());
+    vo.store(static_cast<T*>(a.v_pages) + dst());
+  }
 }
 
 }  // namespace
@@ -160,11 +157,17 @@ hipError_t launch_pool(const PoolArgs& a, int dtype, int head_dim, int batch, hi
   const dim3 grid((unsigned)(blocks > 0 ? blocks : 1), batch);
   const dim3 block(256);
   if (dtype == 1) {
-    if (head_dim == 128) return launch_struct(pool_kv_kernel<bf16_bits, 128>, grid, block, s, a);
-    return launch_struct(pool_kv_kernel<bf16_bits, 64>, grid, block, s, a);
+    if (head_dim == 128)
+      return a.gate ? launch_struct(pool_kv_kernel<bf16_bits, 128, true>, grid, block, s, a)
+                    : launch_struct(pool_kv_kernel<bf16_bits, 128, false>, grid, block, s, a);
+    return a.gate ? launch_struct(pool_kv_kernel<bf16_bits, 64, true>, grid, block, s, a)
+                  : launch_struct(pool_kv_kernel<bf16_bits, 64, false>, grid, block, s, a);
   }
-  if (head_dim == 128) return launch_struct(pool_kv_kernel<float, 128>, grid, block, s, a);
-  return launch_struct(pool_kv_kernel<float, 64>, grid, block, s, a);
+  if (head_dim == 128)
+    return a.gate ? launch_struct(pool_kv_kernel<float, 128, true>, grid, block, s, a)
+                  : launch_struct(pool_kv_kernel<float, 128, false>, grid, block, s, a);
+  return a.gate ? launch_struct(pool_kv_kernel<float, 64, true>, grid, block, s, a)
+                : launch_struct(pool_kv_kernel<float, 64, false>, grid, block, s, a);
 }
 
 }  // namespace skv

@@ -1,0 +1,549 @@
+// Backward of the attention over the compressed cache (arXiv 2607.06827,
+// Sec. III-B, Eq. 5 under the causal mask over compressed positions; Sec.
+// III-C: training runs the pooling inside the forward pass and optimises it
+// jointly, so the gradient reaches Q, the pooled K^/V^ and, through them, the
+// raw K/V and the gate).
+//
+// With P = softmax(scale Q K^T) under the mask, O = P V and the gradient dO:
+//   dP      = dO V^T,   Delta_p = sum_c P_pc dP_pc  (= dO_p . O_p exactly)
+//   dZ      = P o (dP - Delta)
+//   dQ      = scale dZ K^,   dK^ = scale dZ^T Q,   dV^ = P^T dO
+// Delta is formed from P and dP in fp32, not from the stored output: a row
+// that sees few keys has dZ = P (dP - Delta) nearly cancelling, and the bf16
+// rounding of O would otherwise dominate its dQ.
+// P is recomputed from the forward's log-sum-exp, so nothing of size
+// queries x keys is stored.  Two kernels, each owning its output so that
+// nothing is accumulated across blocks:
+//
+// dQ kernel - the forward's tiling: a block owns one (sequence, KV head) and
+//   32*RB query rows for the G query heads; per 32-key tile
+//     S^T = K Q^T,  dP^T = V dO^T          (keys x queries, one query per lane)
+//     dQ^T += K^T dZ0^T,  Kbar^T += K^T P^T (K^T read transposed from the K tile)
+//   in one pass, with dZ0 = P o (dP - Delta0) for Delta0 = dO . O from the
+//   stored output; the exact Delta accumulates beside it, and at the end
+//   dQ = scale (dZ0 K^ + (Delta0 - Delta) Kbar), Kbar = P K^.  It saves
+//   Delta for:
+// dK/dV kernel - a block owns 32 keys of one (sequence, KV head); its waves
+//   take turns over the (query head, 32-row query tile) pairs that see those
+//   keys, staging each Q / dO tile in their own LDS, and per pair
+//     S = Q K^T,  dP = dO V^T               (queries x keys, one key per lane)
+//     dV^T += dO^T P,  dK^T += Q^T dZ        (dO^T, Q^T read transposed)
+//   The waves' partial sums meet in LDS at the end.
+// All products run on the 32x32 MFMAs (bf16 operands with P and dZ rounded to
+// bf16, or fp32), accumulating in fp32; dK^ and dV^ are written in fp32.
+#include <climits>
+#include <type_traits>
+
+#include "attn_mfma.hpp"
+#include "kernels.hpp"
+#include "kernels_bwd.hpp"
+
+namespace skv {
+
+namespace {
+
+constexpr float kLog2eF = 1.4426950408889634f;
+
+// Full-resolution position from which compressed key c may be attended (the
+// visibility rule of the forward): row p sees key c iff p >= tau(c).
+__device__ __forceinline__ int key_visible_from(int c, int P, int T, int nW, int w, int mode) {
+  if (c < P) return c;
+  if (c < P + nW) {
+    const int i = c - P;
+    if (mode == 1) return P + i * w;
+    return min(P + (i + 1) * w, P + T) - 1;
+  }
+  return P + T + (c - P - nW);
+}
+
+__device__ __forceinline__ float frag_dot(bf16x8_t x, bf16x8_t y) {
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s = __builtin_fmaf((float)x[i], (float)y[i], s);
+  return s;
+}
+__device__ __forceinline__ float frag_dot(float x, float y) { return x * y; }
+
+// ------------------------------------------------------------------ dQ
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_bwd_dq_kernel(PrefillBwdArgs a) {
+  typedef Mfma<T> M;
+  typedef typename M::Frag Frag;
+  constexpr int kThreads = PrefillShape<G>::kThreads;
+  constexpr int kRows = PrefillShape<G>::kRows;
+  constexpr int kKeys = 32;                       // keys per tile
+  constexpr int kPack = M::kPack;
+  constexpr int kStep = 2 * kPack;                // head-dim elements per MFMA
+  constexpr int kQChunks = D / kStep;
+  constexpr int kElems16 = 16 / (int)sizeof(T);   // elements per 16-byte chunk
+  constexpr int kChunksPerRow = D / kElems16;
+  constexpr int kRowK = D + kElems16;             // padded K and V rows (elements)
+  constexpr int kItems = kKeys * kChunksPerRow;   // staging work: (key, 16-byte chunk)
+  constexpr int kItemsPerThread = (kItems + kThreads - 1) / kThreads;
+  constexpr int kTile = kKeys * kRowK;
+
+  __shared__ __attribute__((aligned(16))) T s_buf[2 * 2 * kTile];  // [buffer][K, V]
+
+  // XCD-aware item order (as in the forward): XCD x runs a contiguous range
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int tile = a.num_q_tiles - 1 - item % a.num_q_tiles;
+  const int g = (item / a.num_q_tiles) % heads;
+  const int b = item / a.num_q_tiles / heads;
+
+  const int P = max(a.prefix_len[b], 0);
+  const int T_ = max(a.speech_len[b], 0);
+  const int N = max(a.suffix_len[b], 0);
+  const int w = a.w_eff;
+  const int nW = (T_ + w - 1) / w;
+  const int rows = min(P + T_ + N, a.q_len);
+  const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
+  const int p0 = tile * kRows;
+  if (p0 >= rows) return;
+  const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = g * G + wave % G;
+  const int col = lane & 31, hg = lane >> 5;
+  const int wrow0 = p0 + (wave / G) * 32;
+  const int p = wrow0 + col;
+  const bool qvalid = p < rows;
+  const int nvis = qvalid ? min(visible_keys(p, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int hq = a.num_q_heads;
+  const int slot_mask = (1 << a.pv.page_shift) - 1;
+
+  f32x16_t acc[D / 32], kbar[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[db][i] = kbar[db][i] = 0.f;
+  float dsum = 0.f;  // sum over this lane's keys of P dP (half of Delta)
+
+  const T* kpool = static_cast<const T*>(a.k_pages);
+  const T* vpool = static_cast<const T*>(a.v_pages);
+  const int ntiles = (kmax + kKeys - 1) / kKeys;
+
+  // K/V staging: the forward's branch-free pipeline (table entries three tiles
+  // ahead, rows two tiles ahead in registers, LDS one tile ahead), both tiles
+  // row-major; rows past the visible range are zero.
+  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
+  const int64_t num_pages = a.pv.num_pages;
+  const int shift = a.pv.page_shift;
+  int pg[2][kItemsPerThread];
+  uint4 rk[2][kItemsPerThread], rv[2][kItemsPerThread];
+  uint32_t okm[2];
+  auto item_key = [&](int it) { return (tid + it * kThreads) / kChunksPerRow; };
+  auto item_chunk = [&](int it) { return (tid + it * kThreads) % kChunksPerRow; };
+  auto table_load = [&](int kt, int* pgs) {
+#pragma unroll
+    for (int it = 0; it < kItemsPerThread; ++it)
+      pgs[it] = table_row[min((kt * kKeys + item_key(it)) >> shift, a.pv.max_pages - 1)];
+  };
+  auto fetch = [&](int kt, const int* pgs, uint4* rks, uint4* rvs, uint32_t& oks) {
+    oks = 0;
+#pragma unroll
+    for (int it = 0; it < kItemsPerThread; ++it) {
+      const int key = kt * kKeys + item_key(it);
+      const int page = pgs[it];
+      const bool ok = key < kmax && page >= 0 && page < num_pages;
+      oks |= ok ? 1u << it : 0u;
+      const int64_t off = page_row<D>(ok ? page : 0, g, key & slot_mask, a.pv) + item_chunk(it) * kElems16;
+      rks[it] = *reinterpret_cast<const uint4*>(kpool + off);
+      rvs[it] = *reinterpret_cast<const uint4*>(vpool + off);
+    }
+  };
+  auto stage = [&](int buf, const uint4* rks, const uint4* rvs, uint32_t oks) {
+    T* sk = s_buf + buf * 2 * kTile;
+    T* sv = sk + kTile;
+#pragma unroll
+    for (int it = 0; it < kItemsPerThread; ++it) {
+      if (tid + it * kThreads >= kItems) continue;
+      const int key = item_key(it), ch = item_chunk(it);
+      const uint32_t m = 0u - ((oks >> it) & 1u);
+      const uint4 kv = rks[it], vv = rvs[it];
+      *reinterpret_cast<uint4*>(&sk[key * kRowK + ch * kElems16]) = make_uint4(kv.x & m, kv.y & m, kv.z & m, kv.w & m);
+      *reinterpret_cast<uint4*>(&sv[key * kRowK + ch * kElems16]) = make_uint4(vv.x & m, vv.y & m, vv.z & m, vv.w & m);
+    }
+  };
+
+  table_load(0, pg[0]);
+  table_load(1, pg[1]);
+  fetch(0, pg[0], rk[0], rv[0], okm[0]);
+  table_load(2, pg[0]);
+  fetch(1, pg[1], rk[1], rv[1], okm[1]);
+  __builtin_amdgcn_sched_barrier(0);
+  // this lane's query, output and output-gradient row (B operands; rows past
+  // the end read row 0 of the sequence: finite, never stored)
+  Frag qf[kQChunks], gf[kQChunks];
+  const int64_t row_off = (((int64_t)b * a.q_len + (qvalid ? p : 0)) * hq + h) * D + hg * kPack;
+  const T* qrow = static_cast<const T*>(a.q) + row_off;
+  const T* grow = static_cast<const T*>(a.dout) + row_off;
+  const T* orow = static_cast<const T*>(a.out) + row_off;
+  float delta0 = 0.f;  // dO . O from the stored output: the pivot of dZ0
+#pragma unroll
+  for (int kc = 0; kc < kQChunks; ++kc) {
+    qf[kc] = M::load(qrow + kc * kStep);
+    gf[kc] = M::load(grow + kc * kStep);
+    delta0 += frag_dot(gf[kc], M::load(orow + kc * kStep));
+  }
+  const int64_t stat = ((int64_t)b * hq + h) * a.q_len + (qvalid ? p : 0);
+  const float lse2 = a.lse[stat] * kLog2eF;
+  __builtin_amdgcn_sched_barrier(0);
+  stage(0, rk[0], rv[0], okm[0]);
+  __syncthreads();
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  delta0 = partner_sum(delta0);  // the partner lane holds the other half of the row
+
+  auto tile_step = [&](int kt, auto par) {
+    constexpr int kPar = decltype(par)::value;
+    constexpr int kOther = 1 - kPar;
+    table_load(kt + 3, pg[kOther]);
+    fetch(kt + 2, pg[kPar], rk[kPar], rv[kPar], okm[kPar]);
+    const int kb = kt * kKeys;
+    const T* sk = s_buf + kPar * 2 * kTile;
+    const T* sv = sk + kTile;
+    if (kt < ntiles) {
+      // S^T and dP^T: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
+      f32x16_t st, dpt;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) st[i] = dpt[i] = 0.f;
+      const T* krow = &sk[col * kRowK + hg * kPack];
+      const T* vrow = &sv[col * kRowK + hg * kPack];
+#pragma unroll
+      for (int kc = 0; kc < kQChunks; ++kc) {
+        st = M::mma(M::load(krow + kc * kStep), qf[kc], st);
+        dpt = M::mma(M::load(vrow + kc * kStep), gf[kc], dpt);
+      }
+      float pr[16], dz[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
+        const float e = fast_exp2(__builtin_fmaf(st[i], a.scale_log2, -lse2));
+        pr[i] = key < nvis ? e : 0.f;
+        dz[i] = pr[i] * (dpt[i] - delta0);
+        dsum = __builtin_fmaf(pr[i], dpt[i], dsum);
+      }
+      // dQ^T += K^T dZ0^T and Kbar^T += K^T P^T over the 32 keys of the tile
+#pragma unroll
+      for (int kk = 0; kk < kKeys / kStep; ++kk) {
+        const Frag zf = M::pack_p(dz + kk * kPack);
+        const Frag pf = M::pack_p(pr + kk * kPack);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const Frag kt = M::template load_v<kRowK>(sk, kk, db, lane);
+          acc[db] = M::mma(kt, zf, acc[db]);
+          kbar[db] = M::mma(kt, pf, kbar[db]);
+        }
+      }
+    }
+    stage(kOther, rk[kOther], rv[kOther], okm[kOther]);
+    __syncthreads();
+  };
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    tile_step(kt, std::integral_constant<int, 0>());
+    tile_step(kt + 1, std::integral_constant<int, 1>());
+  }
+
+  const float delta = partner_sum(dsum);  // sum over all the row's keys of P dP
+  if (!qvalid) return;
+  if (hg == 0) a.delta[stat] = delta;
+  T* drow = static_cast<T*>(a.dq) + (((int64_t)b * a.q_len + p) * hq + h) * D;
+  const float sc = a.scale, fix = delta0 - delta;
+  auto dq_at = [&](int db, int i) { return sc * __builtin_fmaf(fix, kbar[db][i], acc[db][i]); };
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int ig = 0; ig < 4; ++ig)
+      M::store4(drow + db * 32 + 8 * ig + 4 * hg, dq_at(db, 4 * ig), dq_at(db, 4 * ig + 1),
+                dq_at(db, 4 * ig + 2), dq_at(db, 4 * ig + 3));
+}
+
+// --------------------------------------------------------------- dK / dV
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) void* global_void_ptr;
+
+// Q / dO tiles of the dK/dV kernel: 32 unpadded rows in LDS, filled by
+// direct loads (global_load_lds: a wave-wide load writes 64 x 16 bytes in
+// lane order), 16-byte chunks XOR-swizzled within a row: chunk c of row r sits
+// at position c ^ swz(r), so the operand reads of 16 rows at one chunk hit
+// distinct banks.
+template <typename T, int D>
+struct QTile {
+  static constexpr int kElems16 = 16 / (int)sizeof(T);
+  static constexpr int kChunks = D / kElems16;              // 16-byte chunks per row
+  static constexpr int kRowsPerLoad = 64 / kChunks;         // rows per wave-wide load
+  static constexpr int kLoads = 32 / kRowsPerLoad;          // wave-wide loads per tile
+  static constexpr int kElems = 32 * D;
+  static __device__ __forceinline__ int swz(int r) { return r & (kChunks >= 16 ? 15 : kChunks - 1); }
+  // element e of row r
+  static __device__ __forceinline__ int at(int r, int e) {
+    return r * D + (((e / kElems16) ^ swz(r)) * kElems16) + (e % kElems16);
+  }
+};
+
+// A operand (kPack elements from element e) of row r of a swizzled tile
+__device__ __forceinline__ bf16x8_t tile_a(const bf16_bits* t, int off) {
+  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(t + off));
+}
+__device__ __forceinline__ float tile_a(const float* t, int off) { return t[off]; }
+
+// Transposed A operand of a swizzled 32-row tile: what Mfma<T>::load_v
+// returns for a padded row-major tile (rows 16kk + 4(g/2) + j/4 (+8) for
+// bf16, row 8(kk/4) + 4hg + kk%4 for fp32; columns of head-dim block db).
+template <int D>
+__device__ __forceinline__ bf16x8_t tile_t(const bf16_bits* t, int kk, int db, int lane) {
+  typedef QTile<bf16_bits, D> Q;
+  const int g = lane >> 4, j = lane & 15;
+  const int r = 16 * kk + 4 * (g >> 1) + (j >> 2);
+  const int e = 32 * db + 16 * (g & 1) + 4 * (j & 3);
+  const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(t + Q::at(r, e)));
+  const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(t + Q::at(r + 8, e)));
+  const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
+                     (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+template <int D>
+__device__ __forceinline__ float tile_t(const float* t, int kk, int db, int lane) {
+  typedef QTile<float, D> Q;
+  return t[Q::at(8 * (kk / 4) + 4 * (lane >> 5) + (kk % 4), 32 * db + (lane & 31))];
+}
+
+template <typename T, int D>
+struct KvBwdShape {
+  // fp32 tiles at d = 128 are twice as large: one wave keeps LDS in bounds
+  static constexpr int kWaves = (sizeof(T) == 4 && D == 128) ? 1 : 4;
+  static constexpr int kThreads = 64 * kWaves;
+};
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv_kernel(PrefillBwdArgs a) {
+  typedef Mfma<T> M;
+  typedef typename M::Frag Frag;
+  typedef QTile<T, D> Q;
+  constexpr int kWaves = KvBwdShape<T, D>::kWaves;
+  constexpr int kThreads = KvBwdShape<T, D>::kThreads;
+  constexpr int kKeys = 32;   // keys per block (one per lane column)
+  constexpr int kQ = 32;      // query rows per step
+  constexpr int kPack = M::kPack;
+  constexpr int kStep = 2 * kPack;
+  constexpr int kQChunks = D / kStep;
+  constexpr int kElems16 = Q::kElems16;
+  constexpr int kRowK = D + kElems16;  // padded K / V rows (elements)
+  static_assert(kWaves * 32 * 32 * 4 <= kWaves * Q::kElems * (int)sizeof(T), "reduction fits a Q buffer");
+
+  // two staging buffers per wave, each its own array so that the compiler
+  // sees that direct loads in flight never touch the buffer being read
+  __shared__ __attribute__((aligned(16))) T s_q0[kWaves * Q::kElems];
+  __shared__ __attribute__((aligned(16))) T s_g0[kWaves * Q::kElems];
+  __shared__ __attribute__((aligned(16))) float s_l0[kWaves * 2 * kQ];  // [wave][LSE, Delta]
+  __shared__ __attribute__((aligned(16))) T s_q1[kWaves * Q::kElems];
+  __shared__ __attribute__((aligned(16))) T s_g1[kWaves * Q::kElems];
+  __shared__ __attribute__((aligned(16))) float s_l1[kWaves * 2 * kQ];
+  __shared__ __attribute__((aligned(16))) T s_k[kKeys * kRowK];
+  __shared__ __attribute__((aligned(16))) T s_v[kKeys * kRowK];
+
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int kt = item % a.num_key_tiles;  // early key tiles (most query rows) first
+  const int g = (item / a.num_key_tiles) % heads;
+  const int b = item / a.num_key_tiles / heads;
+
+  const int P = max(a.prefix_len[b], 0);
+  const int T_ = max(a.speech_len[b], 0);
+  const int N = max(a.suffix_len[b], 0);
+  const int w = a.w_eff;
+  const int nW = (T_ + w - 1) / w;
+  const int rows = min(P + T_ + N, a.q_len);
+  const int clen = min(min(P + nW + N, a.pv.max_pages << a.pv.page_shift), a.hat_cap);
+  const int kb = kt * kKeys;
+  if (kb >= clen) return;  // block-uniform
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, hg = lane >> 5;
+  const int hq = a.num_q_heads;
+  const int key = kb + col;  // this lane's key (C-layout column)
+  const int tau = key < clen ? key_visible_from(key, P, T_, nW, w, a.mask_mode) : INT_MAX;
+
+  // the block's K and V rows, row-major in LDS: B operands of S = Q K^T and
+  // dP = dO V^T (keys past the compressed length or without a page are zero)
+  {
+    constexpr int kChunks = D / kElems16;
+    const int shift = a.pv.page_shift;
+    for (int idx = tid; idx < kKeys * kChunks; idx += kThreads) {
+      const int kr = idx / kChunks, ch = idx % kChunks;
+      const int c = kb + kr;
+      const int32_t page = a.table[(int64_t)b * a.pv.max_pages + min(c >> shift, a.pv.max_pages - 1)];
+      const bool ok = c < clen && page >= 0 && page < a.pv.num_pages;
+      const int64_t off = page_row<D>(ok ? page : 0, g, c & ((1 << shift) - 1), a.pv) + ch * kElems16;
+      const uint4 kx = *reinterpret_cast<const uint4*>(static_cast<const T*>(a.k_pages) + off);
+      const uint4 vx = *reinterpret_cast<const uint4*>(static_cast<const T*>(a.v_pages) + off);
+      const uint32_t m = ok ? ~0u : 0u;
+      *reinterpret_cast<uint4*>(&s_k[kr * kRowK + ch * kElems16]) = make_uint4(kx.x & m, kx.y & m, kx.z & m, kx.w & m);
+      *reinterpret_cast<uint4*>(&s_v[kr * kRowK + ch * kElems16]) = make_uint4(vx.x & m, vx.y & m, vx.z & m, vx.w & m);
+    }
+  }
+  const T* krow = &s_k[col * kRowK + hg * kPack];
+  const T* vrow = &s_v[col * kRowK + hg * kPack];
+
+  // query rows that see some key of the block: from tau(kb) (tau grows with c)
+  const int q_first = key_visible_from(kb, P, T_, nW, w, a.mask_mode);
+  const int t0 = q_first / kQ, t1 = (rows + kQ - 1) / kQ;
+  const int n_items = max(t1 - t0, 0) * G;
+
+  // item it (query head, 32-row tile) into one of this wave's buffers, by
+  // direct loads: Q and dO rows, then LSE (lanes 0-31) and Delta (32-63).
+  // Rows past the end load row 0: finite, never visible.
+  const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
+  auto load_item = [&](int it, T* sq, T* sg, float* sl) __attribute__((always_inline)) {
+    const int h = g * G + it % G;
+    const int q0 = (t0 + it / G) * kQ;
+#pragma unroll
+    for (int l = 0; l < Q::kLoads; ++l) {
+      const int r = l * Q::kRowsPerLoad + lrow;
+      const int pr = q0 + r < rows ? q0 + r : 0;
+      const int64_t off = (((int64_t)b * a.q_len + pr) * hq + h) * D + (lpos ^ Q::swz(r)) * kElems16;
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(static_cast<const T*>(a.q) + off),
+                                       (lds_void_ptr)(sq + wave * Q::kElems + l * Q::kRowsPerLoad * D), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(static_cast<const T*>(a.dout) + off),
+                                       (lds_void_ptr)(sg + wave * Q::kElems + l * Q::kRowsPerLoad * D), 16, 0, 0);
+    }
+    const int pr = q0 + col < rows ? q0 + col : 0;
+    const int64_t stat = ((int64_t)b * hq + h) * a.q_len + pr;
+    __builtin_amdgcn_global_load_lds((global_void_ptr)(hg ? a.delta + stat : a.lse + stat),
+                                     (lds_void_ptr)(sl + wave * 2 * kQ), 4, 0, 0);
+  };
+
+  f32x16_t dk[D / 32], dv[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) dk[db][i] = dv[db][i] = 0.f;
+
+  // one item from buffer kPar while the next one loads into the other
+  auto step = [&](int it, auto par) __attribute__((always_inline)) {
+    constexpr int kPar = decltype(par)::value;
+    const T* sq = (kPar ? s_q1 : s_q0) + wave * Q::kElems;
+    const T* sg = (kPar ? s_g1 : s_g0) + wave * Q::kElems;
+    const float* sl = (kPar ? s_l1 : s_l0) + wave * 2 * kQ;
+    // this buffer's loads were issued one step ago; nothing else is in flight
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    if (it + kWaves < n_items) load_item(it + kWaves, kPar ? s_q0 : s_q1, kPar ? s_g0 : s_g1, kPar ? s_l0 : s_l1);
+    const int q0 = (t0 + it / G) * kQ;
+
+    // S = Q K^T and dP = dO V^T: row = query (8*(i/4) + 4*hg + i%4), column = this lane's key
+    f32x16_t s, dp;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[i] = dp[i] = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < kQChunks; ++kc) {
+      const int e = hg * kPack + kc * kStep;
+      s = M::mma(tile_a(sq, Q::at(col, e)), M::load(krow + kc * kStep), s);
+      dp = M::mma(tile_a(sg, Q::at(col, e)), M::load(vrow + kc * kStep), dp);
+    }
+    float pr[16], dz[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 8 * (i / 4) + 4 * hg + (i % 4);
+      const bool vis = q0 + r >= tau && q0 + r < rows;
+      const float e = fast_exp2(__builtin_fmaf(s[i], a.scale_log2, -sl[r] * kLog2eF));
+      pr[i] = vis ? e : 0.f;
+      dz[i] = vis ? e * (dp[i] - sl[kQ + r]) : 0.f;
+    }
+    // dV^T += dO^T P and dK^T += Q^T dZ over the 32 query rows (the row order
+    // of the C layout carried into the transposed reads)
+#pragma unroll
+    for (int kk = 0; kk < kQ / kStep; ++kk) {
+      const Frag pf = M::pack_p(pr + kk * kPack);
+      const Frag zf = M::pack_p(dz + kk * kPack);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        dv[db] = M::mma(tile_t<D>(sg, kk, db, lane), pf, dv[db]);
+        dk[db] = M::mma(tile_t<D>(sq, kk, db, lane), zf, dk[db]);
+      }
+    }
+  };
+
+  if (wave < n_items) load_item(wave, s_q0, s_g0, s_l0);
+  __syncthreads();  // K and V are staged
+  for (int it = wave; it < n_items; it += 2 * kWaves) {
+    step(it, std::integral_constant<int, 0>());
+    if (it + kWaves < n_items) step(it + kWaves, std::integral_constant<int, 1>());
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+
+  // sum the waves' partial dK^T / dV^T through LDS, one 32-wide head-dim block
+  // at a time ([wave][d][key] fp32, keys XOR-swizzled by d), and store rows of
+  // keys below the compressed length
+  float* sr = reinterpret_cast<float*>(s_q0);
+  auto reduce_store = [&](const auto& part, float* dst, float sc) __attribute__((always_inline)) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      __syncthreads();  // the buffer is free (staging done, or the previous block read)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int d = 8 * (i / 4) + 4 * hg + (i % 4);
+        sr[(wave * 32 + d) * 32 + (col ^ d)] = part[db][i];
+      }
+      __syncthreads();
+      for (int v = tid; v < 32 * 32; v += kThreads) {
+        const int d = v & 31, k = v >> 5;
+        float sum = 0.f;
+#pragma unroll
+        for (int wv = 0; wv < kWaves; ++wv) sum += sr[(wv * 32 + d) * 32 + (k ^ d)];
+        if (kb + k < clen) dst[(((int64_t)b * a.hat_cap + kb + k) * heads + g) * D + 32 * db + d] = sum * sc;
+      }
+    }
+  };
+  reduce_store(dk, a.dk_hat, a.scale);
+  reduce_store(dv, a.dv_hat, 1.f);
+}
+
+template <typename T, int D, int G>
+hipError_t launch_bwd_g(const PrefillBwdArgs& a, int batch, hipStream_t s) {
+  const unsigned qitems = (unsigned)(batch * a.pv.kv_heads * a.num_q_tiles);
+  hipError_t e = launch_struct(prefill_bwd_dq_kernel<T, D, G>, dim3(qitems),
+                               dim3(PrefillShape<G>::kThreads), s, a);
+  if (e != hipSuccess) return e;
+  const unsigned kitems = (unsigned)(batch * a.pv.kv_heads * a.num_key_tiles);
+  return launch_struct(prefill_bwd_dkdv_kernel<T, D, G>, dim3(kitems),
+                       dim3(KvBwdShape<T, D>::kThreads), s, a);
+}
+
+template <typename T, int D>
+hipError_t launch_bwd_d(const PrefillBwdArgs& a, int group, int batch, hipStream_t s) {
+  switch (group) {
+    case 1: return launch_bwd_g<T, D, 1>(a, batch, s);
+    case 2: return launch_bwd_g<T, D, 2>(a, batch, s);
+    case 4: return launch_bwd_g<T, D, 4>(a, batch, s);
+    default: return launch_bwd_g<T, D, 8>(a, batch, s);
+  }
+}
+
+}  // namespace
+
+int prefill_bwd_rows_per_tile(int group) {
+  switch (group) {
+    case 1: return PrefillShape<1>::kRows;
+    case 2: return PrefillShape<2>::kRows;
+    case 4: return PrefillShape<4>::kRows;
+    default: return PrefillShape<8>::kRows;
+  }
+}
+
+hipError_t launch_prefill_bwd(const PrefillBwdArgs& a, int dtype, int head_dim, int group,
+                              int batch, hipStream_t s) {
+  if (dtype == 1) {
+    if (head_dim == 128) return launch_bwd_d<bf16_bits, 128>(a, group, batch, s);
+    return launch_bwd_d<bf16_bits, 64>(a, group, batch, s);
+  }
+  if (head_dim == 128) return launch_bwd_d<float, 128>(a, group, batch, s);
+  return launch_bwd_d<float, 64>(a, group, batch, s);
+}
+
+}  // namespace skv

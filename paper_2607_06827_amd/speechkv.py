@@ -65,6 +65,18 @@ _lib.speechkv_prefill_attn.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_Pa
                                        ctypes.POINTER(_Spans), _i32, _i32, _i32, _i32, _f32, _vp,
                                        _vp, _vp]
 _lib.speechkv_prefill_attn.restype = ctypes.c_int
+_lib.speechkv_prefill_attn_bwd.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_PagedKV),
+                                           ctypes.POINTER(_Spans), _i32, _i32, _i32, _i32, _f32,
+                                           _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _sz, _vp]
+_lib.speechkv_prefill_attn_bwd.restype = ctypes.c_int
+_lib.speechkv_prefill_attn_bwd_workspace_bytes.argtypes = [_i32, _i32, _i32]
+_lib.speechkv_prefill_attn_bwd_workspace_bytes.restype = _sz
+_lib.speechkv_pool_kv_bwd.argtypes = [_vp, _vp, _i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
+                                      ctypes.POINTER(_Spans), _i32, _vp, _i32, _i32, _vp, _vp, _i32,
+                                      _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.speechkv_pool_kv_bwd.restype = ctypes.c_int
+_lib.speechkv_pool_kv_bwd_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32]
+_lib.speechkv_pool_kv_bwd_workspace_bytes.restype = _sz
 _lib.speechkv_compressed_len.argtypes = [_i32] * 6
 _lib.speechkv_compressed_len.restype = _i64
 _lib.speechkv_decode_num_splits.argtypes = [_i32, _i32, _i32]
@@ -220,6 +232,72 @@ def speechkv_prefill_attn(q: torch.Tensor, cache: PagedKV, spans: Spans, w: int,
                                     w, layer, l0, mask_mode, scale, out.data_ptr(), _ptr(lse),
                                     _stream(stream))
     _check(st, "speechkv_prefill_attn")
+
+
+def speechkv_prefill_attn_bwd_workspace_bytes(batch: int, num_q_heads: int, q_len: int) -> int:
+    return int(_lib.speechkv_prefill_attn_bwd_workspace_bytes(batch, num_q_heads, q_len))
+
+
+def speechkv_prefill_attn_bwd(q: torch.Tensor, cache: PagedKV, spans: Spans, w: int, layer: int,
+                              l0: int, out: torch.Tensor, lse: torch.Tensor, dout: torch.Tensor,
+                              dq: torch.Tensor, dk_hat: torch.Tensor, dv_hat: torch.Tensor,
+                              workspace: torch.Tensor, mask_mode: int = MASK_WINDOW_END,
+                              scale: Optional[float] = None, stream=None) -> None:
+    """q, out, dout, dq: [B, q_len, Hq, D]; lse: [B, Hq, q_len] fp32;
+    dk_hat, dv_hat: [B, hat_capacity, Hkv, D] fp32; workspace: device bytes."""
+    for x in (q, out, dout, dq, lse, dk_hat, dv_hat, workspace):
+        if not x.is_contiguous():
+            raise ValueError("backward tensors must be contiguous")
+    if dk_hat.dtype != torch.float32 or dv_hat.dtype != torch.float32 or lse.dtype != torch.float32:
+        raise ValueError("lse, dk_hat and dv_hat are fp32")
+    if dk_hat.shape != dv_hat.shape or dk_hat.dim() != 4:
+        raise ValueError("dk_hat and dv_hat must share one [B, capacity, Hkv, D] shape")
+    B, q_len, Hq, D = q.shape
+    if scale is None:
+        scale = D ** -0.5
+    c = cache._c()
+    s = spans._c()
+    st = _lib.speechkv_prefill_attn_bwd(q.data_ptr(), B, Hq, q_len, ctypes.byref(c), ctypes.byref(s),
+                                        w, layer, l0, mask_mode, scale, out.data_ptr(),
+                                        lse.data_ptr(), dout.data_ptr(), dq.data_ptr(),
+                                        dk_hat.data_ptr(), dv_hat.data_ptr(), dk_hat.shape[1],
+                                        workspace.data_ptr(),
+                                        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "speechkv_prefill_attn_bwd")
+
+
+def speechkv_pool_kv_bwd_workspace_bytes(batch: int, max_total_len: int, num_kv_heads: int,
+                                         head_dim: int) -> int:
+    return int(_lib.speechkv_pool_kv_bwd_workspace_bytes(batch, max_total_len, num_kv_heads,
+                                                         head_dim))
+
+
+def speechkv_pool_kv_bwd(k_raw: torch.Tensor, v_raw: torch.Tensor, spans: Spans, w: int,
+                         gate_u: Optional[torch.Tensor], layer: int, l0: int,
+                         dk_hat: torch.Tensor, dv_hat: torch.Tensor, dk_raw: torch.Tensor,
+                         dv_raw: torch.Tensor, du: Optional[torch.Tensor] = None,
+                         workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """k_raw, v_raw, dk_raw, dv_raw: [B, S_raw, Hkv, D] with one stride and a
+    contiguous last axis; dk_hat, dv_hat: [B, capacity, Hkv, D] fp32; du:
+    [Hkv, D] fp32 or None."""
+    for x in (v_raw, dk_raw, dv_raw):
+        if x.shape != k_raw.shape or x.stride() != k_raw.stride() or x.dtype != k_raw.dtype:
+            raise ValueError("k_raw, v_raw, dk_raw and dv_raw must share shape, stride and dtype")
+    if k_raw.dim() != 4 or k_raw.stride(3) != 1:
+        raise ValueError("raw K/V must be [B, S, Hkv, D] with a contiguous last axis")
+    for x in (dk_hat, dv_hat) + ((du,) if du is not None else ()):
+        if x.dtype != torch.float32 or not x.is_contiguous():
+            raise ValueError("dk_hat, dv_hat and du are contiguous fp32")
+    B, S, H, D = k_raw.shape
+    sb, ss, sh, _ = k_raw.stride()
+    s = spans._c()
+    ws = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.speechkv_pool_kv_bwd(k_raw.data_ptr(), v_raw.data_ptr(), sb, ss, sh, B, S, H, D,
+                                   _dtype_code(k_raw.dtype), ctypes.byref(s), w, _ptr(gate_u),
+                                   layer, l0, dk_hat.data_ptr(), dv_hat.data_ptr(), dk_hat.shape[1],
+                                   dk_raw.data_ptr(), dv_raw.data_ptr(), _ptr(du), _ptr(workspace),
+                                   ws, _stream(stream))
+    _check(st, "speechkv_pool_kv_bwd")
 
 
 def speechkv_compressed_len(prefix_len: int, speech_len: int, suffix_len: int, w: int,

@@ -26,7 +26,9 @@ def declared_functions():
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
-                          "speechkv_pool_hidden",
+                          "speechkv_pool_hidden", "speechkv_prefill_attn_bwd",
+                          "speechkv_prefill_attn_bwd_workspace_bytes", "speechkv_pool_kv_bwd",
+                          "speechkv_pool_kv_bwd_workspace_bytes",
                           "speechkv_compressed_len", "speechkv_decode_num_splits",
                           "speechkv_decode_workspace_bytes", "speechkv_status_string",
                           "speechkv_version"}
@@ -218,3 +220,77 @@ def test_binding_constants_match_header():
     for name in ("OK", "ERR_INVALID_ARG", "ERR_UNSUPPORTED", "ERR_WORKSPACE", "ERR_ALIAS", "ERR_HIP",
                  "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START", "MAX_WINDOW"):
         assert int(defs[name]) == getattr(skv, name), name
+
+
+# ---------------------------------------------------------------- backward
+
+def prefill_bwd(c=None, s=None, **kw):
+    a = dict(q=FAKE + (15 << 24), batch=2, hq=4, q_len=60, w=4, layer=1, l0=0, mode=0, scale=0.125,
+             out=FAKE + (16 << 24), lse=FAKE + (17 << 24), dout=FAKE + (18 << 24),
+             dq=FAKE + (19 << 24), dk=FAKE + (20 << 24), dv=FAKE + (21 << 24), cap=60,
+             ws=FAKE + (22 << 24), ws_bytes=1 << 20)
+    a.update(kw)
+    c = c or cache()
+    s = s or spans()
+    return lib.speechkv_prefill_attn_bwd(a["q"], a["batch"], a["hq"], a["q_len"], ctypes.byref(c),
+                                         ctypes.byref(s), a["w"], a["layer"], a["l0"], a["mode"],
+                                         a["scale"], a["out"], a["lse"], a["dout"], a["dq"], a["dk"],
+                                         a["dv"], a["cap"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(lse=None), E_ARG), (dict(dout=None), E_ARG),
+    (dict(dq=None), E_ARG), (dict(dk=None), E_ARG), (dict(dv=None), E_ARG), (dict(cap=0), E_ARG),
+    (dict(w=0), E_ARG), (dict(w=skv.MAX_WINDOW + 1), E_ARG), (dict(q_len=59), E_ARG),
+    (dict(mode=2), E_ARG), (dict(scale=0.0), E_ARG), (dict(hq=5), E_ARG), (dict(hq=6), E_UNS),
+    (dict(batch=0), E_ARG), (dict(dq=FAKE + (19 << 24) + 4), E_ARG), (dict(lse=FAKE + (17 << 24) + 2), E_ARG),
+    (dict(ws=None), E_WS), (dict(ws_bytes=2 * 4 * 60 * 4 - 4), E_WS),
+    (dict(dq=FAKE + (15 << 24)), E_ALIAS), (dict(dv=FAKE + (20 << 24) + 256), E_ALIAS),
+    (dict(dk=FAKE + 4096), E_ALIAS), (dict(ws=FAKE + (18 << 24)), E_ALIAS),
+])
+def test_prefill_bwd_rejects(kw, code):
+    assert prefill_bwd(**kw) == code
+
+
+def test_prefill_bwd_rejects_bad_cache_and_spans():
+    assert prefill_bwd(c=cache(head_dim=96)) == E_UNS
+    assert prefill_bwd(c=cache(k_pages=None)) == E_ARG
+    assert prefill_bwd(s=spans(prefix_len=None)) == E_ARG
+
+
+def test_bwd_workspace_sizes():
+    assert skv.speechkv_prefill_attn_bwd_workspace_bytes(8, 16, 1596) == 8 * 16 * 1596 * 4
+    assert skv.speechkv_prefill_attn_bwd_workspace_bytes(0, 16, 1596) == 0
+    # per-block partial gate gradients: 16 slots per block at 8 heads x 128
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(64, 782, 8, 128) == 64 * 49 * 8 * 128 * 4
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 0, 8, 128) == 2 * 1 * 8 * 128 * 4
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 3, 128) == 0   # 3 x 16 does not divide 256
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 8, 96) == 0
+
+
+def pool_bwd(s=None, **kw):
+    a = dict(k=RAW, v=RAW + (1 << 22), sb=60 * 2 * 64, ss=2 * 64, sh=64, batch=2, raw_len=60, heads=2,
+             hd=64, dtype=skv.DTYPE_BF16, w=4, gate=None, layer=1, l0=0, dk=FAKE + (23 << 24),
+             dv=FAKE + (24 << 24), cap=60, dkr=FAKE + (25 << 24), dvr=FAKE + (26 << 24), du=None,
+             ws=None, ws_bytes=0)
+    a.update(kw)
+    s = s or spans()
+    return lib.speechkv_pool_kv_bwd(a["k"], a["v"], a["sb"], a["ss"], a["sh"], a["batch"], a["raw_len"],
+                                    a["heads"], a["hd"], a["dtype"], ctypes.byref(s), a["w"], a["gate"],
+                                    a["layer"], a["l0"], a["dk"], a["dv"], a["cap"], a["dkr"], a["dvr"],
+                                    a["du"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), E_ARG), (dict(dk=None), E_ARG), (dict(dkr=None), E_ARG), (dict(dvr=None), E_ARG),
+    (dict(dtype=7), E_UNS), (dict(hd=96), E_UNS), (dict(heads=3), E_UNS), (dict(heads=64), E_UNS),
+    (dict(heads=0), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=50), E_ARG), (dict(w=0), E_ARG),
+    (dict(w=skv.MAX_WINDOW + 1), E_ARG), (dict(cap=0), E_ARG), (dict(layer=-1), E_ARG),
+    (dict(sb=-8), E_ARG), (dict(ss=3), E_ARG), (dict(dkr=FAKE + (25 << 24) + 4), E_ARG),
+    (dict(gate=FAKE + 4), E_ARG), (dict(du=FAKE + (27 << 24)), E_WS),
+    (dict(du=FAKE + (27 << 24), ws=FAKE + (28 << 24), ws_bytes=64), E_WS),
+    (dict(dkr=RAW), E_ALIAS), (dict(dvr=FAKE + (25 << 24) + 1024), E_ALIAS),
+    (dict(dkr=FAKE + (23 << 24) + 2048), E_ALIAS),
+])
+def test_pool_bwd_rejects(kw, code):
+    assert pool_bwd(**kw) == code
