@@ -405,7 +405,7 @@ int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads,
 size_t speechkv_pool_kv_bwd_workspace_bytes(int32_t batch, int32_t max_total_len,
                                             int32_t num_kv_heads, int32_t head_dim) {
   if (batch < 1 || max_total_len < 0 || num_kv_heads < 1) return 0;
-  const int spb = skv::pool_bwd_slots_per_block(num_kv_heads, head_dim);
+  const int spb = skv::pool_bwd_slots_per_block(batch, max_total_len, num_kv_heads, head_dim);
   if (spb == 0) return 0;
   const int64_t blocks = max_total_len > 0 ? (max_total_len + spb - 1) / spb : 1;
   return (size_t)batch * blocks * num_kv_heads * head_dim * sizeof(float);
@@ -422,8 +422,9 @@ int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw, int64_t stride_b,
   if (st) return st;
   if (dtype != SPEECHKV_DTYPE_F32 && dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
   if (head_dim != 64 && head_dim != 128) return SPEECHKV_ERR_UNSUPPORTED;
-  if (num_kv_heads < 1) return SPEECHKV_ERR_INVALID_ARG;
-  const int spb = skv::pool_bwd_slots_per_block(num_kv_heads, head_dim);
+  if (num_kv_heads < 1 || batch < 1) return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > raw_len) return SPEECHKV_ERR_INVALID_ARG;
+  const int spb = skv::pool_bwd_slots_per_block(batch, spans->max_total_len, num_kv_heads, head_dim);
   if (spb == 0) return SPEECHKV_ERR_UNSUPPORTED;
   if (batch < 1 || batch > kMaxGrid || raw_len < 1 || raw_len > kMaxRows || w < 1 ||
       w > SPEECHKV_MAX_WINDOW || layer < 0 || l0 < 0 || hat_capacity < 1)

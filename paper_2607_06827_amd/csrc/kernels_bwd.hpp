@@ -65,9 +65,10 @@ struct PoolBwdArgs {
 int prefill_bwd_rows_per_tile(int group);
 hipError_t launch_prefill_bwd(const PrefillBwdArgs& a, int dtype, int head_dim, int group,
                               int batch, hipStream_t s);
-// Slots of one sequence a pooling-backward block covers, and so the size of
-// the partial gate-gradient buffer; 0 when (kv_heads, head_dim) is not supported.
-int pool_bwd_slots_per_block(int kv_heads, int head_dim);
+// Slots of one sequence a pooling-backward block covers (a multiple of the
+// slots one pass of 256 threads covers), and so the size of the partial
+// gate-gradient buffer; 0 when (kv_heads, head_dim) is not supported.
+int pool_bwd_slots_per_block(int batch, int max_out, int kv_heads, int head_dim);
 hipError_t launch_pool_bwd(const PoolBwdArgs& a, int dtype, int head_dim, int batch,
                            hipStream_t s);
 

@@ -12,7 +12,8 @@
 //
 // Layout: each thread owns 8 consecutive elements of one KV head; D/8 threads
 // cover a head, kv_heads * D/8 a slot of the compressed sequence, and a block
-// walks kIters groups of 256 / (kv_heads * D/8) slots of one sequence.  Every
+// walks `iters` groups of 256 / (kv_heads * D/8) slots of one sequence, iters
+// chosen so that the whole launch has about a thousand blocks.  Every
 // raw row is read at most twice (once more for windows longer than four
 // frames) and every gradient row written once: the kernel is bound by HBM
 // bandwidth.  The gate gradient is kept per thread, summed over the block in
@@ -26,7 +27,7 @@ namespace skv {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kIters = 8;  // slot groups per block
+constexpr int kTargetBlocks = 1024;  // about four blocks per CU, and as many gate partials
 
 template <int D>
 constexpr int lanes_per_head() { return D / 8; }
@@ -70,8 +71,9 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) du[e] = 0.f;
 
-  for (int k = 0; k < kIters; ++k) {
-    const int c = (blockIdx.x * kIters + k) * slot_lanes + sl;
+  const int iters = a.slots_per_block / slot_lanes;
+  for (int k = 0; k < iters; ++k) {
+    const int c = (blockIdx.x * iters + k) * slot_lanes + sl;
     if (sl >= slot_lanes || c >= len) continue;
     const bool text_before = c < P, text_after = c >= P + nW;
     const int src = text_before ? c : text_after ? P + S + (c - P - nW) : P + (c - P) * w;
@@ -187,13 +189,29 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
   }
 }
 
-// du[i] = sum over the per-block partials, in block order.
+// du[i] = sum over the per-block partials: 64 threads per output each add
+// every 64th partial (four independent sums), then the 64 sums are added in
+// LDS in a fixed order.
+constexpr int kReduceOut = 4;  // outputs per 256-thread block
 __global__ __launch_bounds__(256) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  float s = 0.f;
-  for (int p = 0; p < parts; ++p) s += part[(int64_t)p * n + i];
-  du[i] = s;
+  __shared__ float s_sum[256];
+  const int o = threadIdx.x % kReduceOut, r = threadIdx.x / kReduceOut;  // r < 64
+  const int i = blockIdx.x * kReduceOut + o;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (i < n) {
+    int p = r;
+    for (; p + 3 * 64 < parts; p += 4 * 64)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] += part[(int64_t)(p + q * 64) * n + i];
+    for (int q = 0; p < parts; p += 64, ++q) acc[q & 3] += part[(int64_t)p * n + i];
+  }
+  s_sum[threadIdx.x] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  __syncthreads();
+  if (r == 0 && i < n) {
+    float sum = 0.f;
+    for (int k = 0; k < 64; ++k) sum += s_sum[k * kReduceOut + o];
+    du[i] = sum;
+  }
 }
 
 template <typename T, int D>
@@ -203,18 +221,21 @@ hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
                         : launch_struct(pool_bwd_kernel<T, D, false>, grid, dim3(256), s, a);
   if (e != hipSuccess || !a.du) return e;
   const int n = a.kv_heads * D;
-  hipLaunchKernelGGL(du_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a.du_part,
-                     batch * a.blocks_per_seq, n, a.du);
+  hipLaunchKernelGGL(du_reduce_kernel, dim3((n + kReduceOut - 1) / kReduceOut), dim3(256), 0, s,
+                     a.du_part, batch * a.blocks_per_seq, n, a.du);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int pool_bwd_slots_per_block(int kv_heads, int head_dim) {
+int pool_bwd_slots_per_block(int batch, int max_out, int kv_heads, int head_dim) {
   if (head_dim != 64 && head_dim != 128) return 0;
   const int per_slot = kv_heads * (head_dim / 8);
-  if (kv_heads < 1 || per_slot > 256 || 256 % per_slot) return 0;
-  return (256 / per_slot) * kIters;
+  if (batch < 1 || kv_heads < 1 || per_slot > 256 || 256 % per_slot) return 0;
+  const int lanes = 256 / per_slot;
+  const int groups = max_out > 0 ? (max_out + lanes - 1) / lanes : 1;  // slot groups per sequence
+  const int blocks = batch >= kTargetBlocks ? 1 : kTargetBlocks / batch;  // per sequence
+  return ((groups + blocks - 1) / blocks) * lanes;
 }
 
 hipError_t launch_pool_bwd(const PoolBwdArgs& a, int dtype, int head_dim, int batch,

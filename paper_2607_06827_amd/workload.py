@@ -17,7 +17,9 @@ import torch
 from . import inputs
 from .speechkv import (PagedKV, Spans, speechkv_compressed_len, speechkv_decode_attn,
                        speechkv_decode_num_splits, speechkv_decode_workspace_bytes,
-                       speechkv_pool_hidden, speechkv_pool_kv, speechkv_prefill_attn)
+                       speechkv_pool_hidden, speechkv_pool_kv, speechkv_pool_kv_bwd,
+                       speechkv_pool_kv_bwd_workspace_bytes, speechkv_prefill_attn,
+                       speechkv_prefill_attn_bwd, speechkv_prefill_attn_bwd_workspace_bytes)
 
 
 def visible_pairs(P: int, T: int, N: int, w: int) -> int:
@@ -246,3 +248,83 @@ class HiddenPoolJob:
         e = self.h.element_size()
         return self.wl.batch * self.hidden * e * (self.wl.prefill_len + self.out_rows) \
             + self.hidden * 4
+
+
+class TrainJob:
+    """One training-mode layer of a workload (Sec. III-C: the pooling runs in
+    the forward pass and is optimised jointly): the forward (pool, then
+    attention with its log-sum-exp) and the backward from a seeded output
+    gradient (attention backward, then pooling backward down to the raw K/V
+    and the gate).  Layer index `layer` of the workload, its first layer by
+    default."""
+
+    def __init__(self, wl: inputs.Workload, layer: Optional[int] = None, device="cuda"):
+        layer = wl.l0 if layer is None else layer
+        self.fwd = Job(wl, device=device, layers=[layer])
+        self.wl = wl
+        self.layer = layer
+        f = self.fwd
+        B, S, Hq, Hkv, D = wl.batch, wl.prefill_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+        dev = f.device
+        self.out = torch.empty(B, S, Hq, D, dtype=wl.torch_dtype, device=dev)
+        self.lse = torch.empty(B, Hq, S, dtype=torch.float32, device=dev)
+        self.dout = inputs.normal((B, S, Hq, D), wl.seed * 100 + 81, device=dev, dtype=wl.torch_dtype)
+        self.clen = f.prefill_clen[0]
+        self.dq = torch.empty_like(self.out)
+        self.dk_hat = torch.empty(B, self.clen, Hkv, D, dtype=torch.float32, device=dev)
+        self.dv_hat = torch.empty_like(self.dk_hat)
+        self.dk_raw = torch.empty_like(f.k_raw[0])
+        self.dv_raw = torch.empty_like(f.v_raw[0])
+        self.du = torch.empty(Hkv, D, dtype=torch.float32, device=dev)
+        n = max(speechkv_prefill_attn_bwd_workspace_bytes(B, Hq, S),
+                speechkv_pool_kv_bwd_workspace_bytes(B, S, Hkv, D))
+        self.workspace = torch.empty(n, dtype=torch.uint8, device=dev)
+
+    def run_forward(self, stream=None):
+        f, wl = self.fwd, self.wl
+        speechkv_pool_kv(f.k_raw[0], f.v_raw[0], f.spans, wl.w, f.gate[0], self.layer, f.l0,
+                         f.caches[0], stream=stream)
+        speechkv_prefill_attn(f.q_prefill[0], f.caches[0], f.spans, wl.w, self.layer, f.l0,
+                              self.out, scale=f.scale, lse=self.lse, stream=stream)
+
+    def run_attn_bwd(self, stream=None):
+        f, wl = self.fwd, self.wl
+        speechkv_prefill_attn_bwd(f.q_prefill[0], f.caches[0], f.spans, wl.w, self.layer, f.l0,
+                                  self.out, self.lse, self.dout, self.dq, self.dk_hat, self.dv_hat,
+                                  self.workspace, scale=f.scale, stream=stream)
+
+    def run_pool_bwd(self, stream=None):
+        f, wl = self.fwd, self.wl
+        speechkv_pool_kv_bwd(f.k_raw[0], f.v_raw[0], f.spans, wl.w, f.gate[0], self.layer, f.l0,
+                             self.dk_hat, self.dv_hat, self.dk_raw, self.dv_raw, self.du,
+                             self.workspace, stream=stream)
+
+    def run_backward(self, stream=None):
+        self.run_attn_bwd(stream)
+        self.run_pool_bwd(stream)
+
+    def attn_bwd_flops(self) -> int:
+        """Algorithmic FLOPs of the attention backward: the four gradient
+        products dP = dO V^T, dV^ = P^T dO, dK^ = dZ^T Q, dQ = dZ K^ over
+        every (row, visible key) pair of every query head, 2 FLOPs per
+        multiply-add (recomputing S is not counted)."""
+        return 8 * self.wl.batch * self.wl.num_q_heads * self.wl.head_dim * \
+            self.fwd.prefill_visible_pairs(0)
+
+    def attn_bwd_bytes(self) -> int:
+        """Algorithmic HBM bytes of the attention backward: Q, O, dO read and
+        dQ written once, K^ and V^ read once, dK^ and dV^ (fp32) written once,
+        LSE read once."""
+        wl = self.wl
+        e = 2 if wl.dtype == "bf16" else 4
+        q = wl.batch * wl.prefill_len * wl.num_q_heads * wl.head_dim
+        kv = wl.batch * self.clen * wl.num_kv_heads * wl.head_dim
+        return 4 * q * e + 2 * kv * e + 2 * kv * 4 + wl.batch * wl.num_q_heads * wl.prefill_len * 4
+
+    def pool_bwd_bytes(self) -> int:
+        """Algorithmic HBM bytes of the pooling backward: raw K and V read once,
+        their gradients written once, dK^ and dV^ (fp32) read once."""
+        wl = self.wl
+        e = 2 if wl.dtype == "bf16" else 4
+        row = wl.num_kv_heads * wl.head_dim
+        return wl.batch * (4 * wl.prefill_len * row * e + 2 * self.clen * row * 4)

@@ -261,8 +261,12 @@ def test_prefill_bwd_rejects_bad_cache_and_spans():
 def test_bwd_workspace_sizes():
     assert skv.speechkv_prefill_attn_bwd_workspace_bytes(8, 16, 1596) == 8 * 16 * 1596 * 4
     assert skv.speechkv_prefill_attn_bwd_workspace_bytes(0, 16, 1596) == 0
-    # per-block partial gate gradients: 16 slots per block at 8 heads x 128
-    assert skv.speechkv_pool_kv_bwd_workspace_bytes(64, 782, 8, 128) == 64 * 49 * 8 * 128 * 4
+    # per-block partial gate gradients, about 1024 blocks in all: at 8 heads x
+    # 128 a 256-thread pass covers 2 slots; 64 sequences of 782 slots take 16
+    # blocks of 25 passes (50 slots) each
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(64, 782, 8, 128) == 64 * 16 * 8 * 128 * 4
+    # 8 sequences of 1596: 128 blocks of 7 passes (14 slots) -> 114 blocks cover them
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(8, 1596, 8, 128) == 8 * 114 * 8 * 128 * 4
     assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 0, 8, 128) == 2 * 1 * 8 * 128 * 4
     assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 3, 128) == 0   # 3 x 16 does not divide 256
     assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 8, 96) == 0
