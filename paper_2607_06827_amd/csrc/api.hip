@@ -369,7 +369,8 @@ int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads,
   const int rows_per_tile = skv::prefill_bwd_rows_per_tile(group);
   const int64_t q_tiles = (spans->max_total_len + rows_per_tile - 1) / rows_per_tile;
   const int64_t keys = spans->max_total_len < hat_capacity ? spans->max_total_len : hat_capacity;
-  const int64_t key_tiles = (keys + 31) / 32;
+  const int keys_per_block = skv::prefill_bwd_keys_per_block(cache->dtype, cache->head_dim);
+  const int64_t key_tiles = (keys + keys_per_block - 1) / keys_per_block;
   if ((int64_t)batch * cache->num_kv_heads * q_tiles > INT32_MAX ||
       (int64_t)batch * cache->num_kv_heads * key_tiles > INT32_MAX)
     return SPEECHKV_ERR_INVALID_ARG;

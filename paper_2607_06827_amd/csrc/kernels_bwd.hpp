@@ -28,7 +28,7 @@ struct PrefillBwdArgs {
   int q_len;
   int num_q_heads;
   int num_q_tiles;    // query tiles per (sequence, KV head), dQ kernel
-  int num_key_tiles;  // 32-key tiles per (sequence, KV head), dK/dV kernel
+  int num_key_tiles;  // key blocks per (sequence, KV head), dK/dV kernel
   float scale;
   float scale_log2;
   float* delta;       // [B][Hq][q_len]: rowsum(dO * O), written by the dQ kernel
@@ -63,6 +63,7 @@ struct PoolBwdArgs {
 };
 
 int prefill_bwd_rows_per_tile(int group);
+int prefill_bwd_keys_per_block(int dtype, int head_dim);  // keys of one dK/dV block
 hipError_t launch_prefill_bwd(const PrefillBwdArgs& a, int dtype, int head_dim, int group,
                               int batch, hipStream_t s);
 // Slots of one sequence a pooling-backward block covers (a multiple of the

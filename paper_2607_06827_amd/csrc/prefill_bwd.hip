@@ -23,12 +23,14 @@
 //   stored output; the exact Delta accumulates beside it, and at the end
 //   dQ = scale (dZ0 K^ + (Delta0 - Delta) Kbar), Kbar = P K^.  It saves
 //   Delta for:
-// dK/dV kernel - a block owns 32 keys of one (sequence, KV head); its waves
-//   take turns over the (query head, 32-row query tile) pairs that see those
-//   keys, staging each Q / dO tile in their own LDS, and per pair
+// dK/dV kernel - a block owns 32 keys per wave (128 keys) of one (sequence,
+//   KV head) and walks the (query head, 32-row query tile) pairs that see
+//   them; each pair's Q / dO tile is staged once in LDS for all the waves
+//   (direct loads, three steps ahead), and each wave computes on its own keys,
+//   K and V held in registers
 //     S = Q K^T,  dP = dO V^T               (queries x keys, one key per lane)
 //     dV^T += dO^T P,  dK^T += Q^T dZ        (dO^T, Q^T read transposed)
-//   The waves' partial sums meet in LDS at the end.
+//   starting S and dP from -LSE/scale and -Delta of their rows.
 // All products run on the 32x32 MFMAs (bf16 operands with P and dZ rounded to
 // bf16, or fp32), accumulating in fp32; dK^ and dV^ are written in fp32.
 #include <climits>
@@ -43,6 +45,12 @@ namespace skv {
 namespace {
 
 constexpr float kLog2eF = 1.4426950408889634f;
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// the wave are outstanding (vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt
+// at their maxima, so they are not waited for)
+constexpr int wait_vmcnt(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
+static_assert(wait_vmcnt(0) == kWaitVmcnt0, "vmcnt(0) encoding");
 
 // Full-resolution position from which compressed key c may be attended (the
 // visibility rule of the forward): row p sees key c iff p >= tau(c).
@@ -314,9 +322,10 @@ __device__ __forceinline__ float tile_t(const float* t, int kk, int db, int lane
 
 template <typename T, int D>
 struct KvBwdShape {
-  // fp32 tiles at d = 128 are twice as large: one wave keeps LDS in bounds
-  static constexpr int kWaves = (sizeof(T) == 4 && D == 128) ? 1 : 4;
+  // fp32 at d = 128 has twice the bytes per tile: two waves keep LDS in bounds
+  static constexpr int kWaves = (sizeof(T) == 4 && D == 128) ? 2 : 4;
   static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kKeys = 32 * kWaves;  // keys per block, 32 per wave
 };
 
 template <typename T, int D, int G>
@@ -325,32 +334,40 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
   typedef typename M::Frag Frag;
   typedef QTile<T, D> Q;
   constexpr int kWaves = KvBwdShape<T, D>::kWaves;
-  constexpr int kThreads = KvBwdShape<T, D>::kThreads;
-  constexpr int kKeys = 32;   // keys per block (one per lane column)
+  constexpr int kBlockKeys = KvBwdShape<T, D>::kKeys;
   constexpr int kQ = 32;      // query rows per step
   constexpr int kPack = M::kPack;
   constexpr int kStep = 2 * kPack;
   constexpr int kQChunks = D / kStep;
   constexpr int kElems16 = Q::kElems16;
-  constexpr int kRowK = D + kElems16;  // padded K / V rows (elements)
-  static_assert(kWaves * 32 * 32 * 4 <= kWaves * Q::kElems * (int)sizeof(T), "reduction fits a Q buffer");
 
-  // two staging buffers per wave, each its own array so that the compiler
-  // sees that direct loads in flight never touch the buffer being read
-  __shared__ __attribute__((aligned(16))) T s_q0[kWaves * Q::kElems];
-  __shared__ __attribute__((aligned(16))) T s_g0[kWaves * Q::kElems];
-  __shared__ __attribute__((aligned(16))) float s_l0[kWaves * 2 * kQ];  // [wave][LSE, Delta]
-  __shared__ __attribute__((aligned(16))) T s_q1[kWaves * Q::kElems];
-  __shared__ __attribute__((aligned(16))) T s_g1[kWaves * Q::kElems];
-  __shared__ __attribute__((aligned(16))) float s_l1[kWaves * 2 * kQ];
-  __shared__ __attribute__((aligned(16))) T s_k[kKeys * kRowK];
-  __shared__ __attribute__((aligned(16))) T s_v[kKeys * kRowK];
+  // the shared Q / dO tile (with LSE and Delta) of kBufs steps, each buffer
+  // its own array so that the compiler sees that direct loads in flight never
+  // touch the buffer being read
+  struct Buf {
+    T q[Q::kElems];
+    T g[Q::kElems];
+    float l[2 * kQ];  // LSE, Delta
+  };
+  constexpr int kBufs = 4 * (int)sizeof(Buf) <= 160 * 1024 ? 4 : 2;
+  typedef std::conditional_t<(kBufs > 2), Buf, char> Buf23;  // (unused with two buffers)
+  __shared__ __attribute__((aligned(16))) Buf s_b0;
+  __shared__ __attribute__((aligned(16))) Buf s_b1;
+  __shared__ __attribute__((aligned(16))) Buf23 s_b2;
+  __shared__ __attribute__((aligned(16))) Buf23 s_b3;
+  auto buf = [&](auto n) -> auto& {
+    constexpr int kN = decltype(n)::value % kBufs;
+    if constexpr (kN == 0) return s_b0;
+    else if constexpr (kN == 1) return s_b1;
+    else if constexpr (kN == 2) return s_b2;
+    else return s_b3;
+  };
 
   const int nblk = gridDim.x, bid = blockIdx.x;
   const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
   const int item = xcd * per + min(xcd, rem) + (bid >> 3);
   const int heads = a.pv.kv_heads;
-  const int kt = item % a.num_key_tiles;  // early key tiles (most query rows) first
+  const int kt = item % a.num_key_tiles;  // early keys (most query rows) first
   const int g = (item / a.num_key_tiles) % heads;
   const int b = item / a.num_key_tiles / heads;
 
@@ -361,62 +378,67 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
   const int nW = (T_ + w - 1) / w;
   const int rows = min(P + T_ + N, a.q_len);
   const int clen = min(min(P + nW + N, a.pv.max_pages << a.pv.page_shift), a.hat_cap);
-  const int kb = kt * kKeys;
-  if (kb >= clen) return;  // block-uniform
+  const int kb0 = kt * kBlockKeys;
+  if (kb0 >= clen) return;  // block-uniform
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, hg = lane >> 5;
   const int hq = a.num_q_heads;
-  const int key = kb + col;  // this lane's key (C-layout column)
+  const int kb = kb0 + 32 * wave;  // this wave's keys
+  const int key = kb + col;       // this lane's key (C-layout column)
   const int tau = key < clen ? key_visible_from(key, P, T_, nW, w, a.mask_mode) : INT_MAX;
+  // first row that sees a key of this wave (none: INT_MAX)
+  const int wave_from = kb < clen ? key_visible_from(kb, P, T_, nW, w, a.mask_mode) : INT_MAX;
 
-  // the block's K and V rows, row-major in LDS: B operands of S = Q K^T and
-  // dP = dO V^T (keys past the compressed length or without a page are zero)
+  // this lane's K and V rows, the B operands of S = Q K^T and dP = dO V^T,
+  // in registers for every step (a key past the compressed length or without
+  // a page reads page 0 and is zeroed)
+  Frag kf[kQChunks], vf[kQChunks];
   {
-    constexpr int kChunks = D / kElems16;
     const int shift = a.pv.page_shift;
-    for (int idx = tid; idx < kKeys * kChunks; idx += kThreads) {
-      const int kr = idx / kChunks, ch = idx % kChunks;
-      const int c = kb + kr;
-      const int32_t page = a.table[(int64_t)b * a.pv.max_pages + min(c >> shift, a.pv.max_pages - 1)];
-      const bool ok = c < clen && page >= 0 && page < a.pv.num_pages;
-      const int64_t off = page_row<D>(ok ? page : 0, g, c & ((1 << shift) - 1), a.pv) + ch * kElems16;
-      const uint4 kx = *reinterpret_cast<const uint4*>(static_cast<const T*>(a.k_pages) + off);
-      const uint4 vx = *reinterpret_cast<const uint4*>(static_cast<const T*>(a.v_pages) + off);
-      const uint32_t m = ok ? ~0u : 0u;
-      *reinterpret_cast<uint4*>(&s_k[kr * kRowK + ch * kElems16]) = make_uint4(kx.x & m, kx.y & m, kx.z & m, kx.w & m);
-      *reinterpret_cast<uint4*>(&s_v[kr * kRowK + ch * kElems16]) = make_uint4(vx.x & m, vx.y & m, vx.z & m, vx.w & m);
+    const int32_t page = a.table[(int64_t)b * a.pv.max_pages + min(key >> shift, a.pv.max_pages - 1)];
+    const bool ok = key < clen && page >= 0 && page < a.pv.num_pages;
+    const int64_t off = page_row<D>(ok ? page : 0, g, key & ((1 << shift) - 1), a.pv) + hg * kPack;
+#pragma unroll
+    for (int kc = 0; kc < kQChunks; ++kc) {
+      const Frag k = M::load(static_cast<const T*>(a.k_pages) + off + kc * kStep);
+      const Frag v = M::load(static_cast<const T*>(a.v_pages) + off + kc * kStep);
+      kf[kc] = ok ? k : M::zero();
+      vf[kc] = ok ? v : M::zero();
     }
   }
-  const T* krow = &s_k[col * kRowK + hg * kPack];
-  const T* vrow = &s_v[col * kRowK + hg * kPack];
 
-  // query rows that see some key of the block: from tau(kb) (tau grows with c)
-  const int q_first = key_visible_from(kb, P, T_, nW, w, a.mask_mode);
+  // query rows that see some key of the block: from tau(kb0) (tau grows with
+  // c); one step per (query head, 32-row tile) pair
+  const int q_first = key_visible_from(kb0, P, T_, nW, w, a.mask_mode);
   const int t0 = q_first / kQ, t1 = (rows + kQ - 1) / kQ;
-  const int n_items = max(t1 - t0, 0) * G;
+  const int n_steps = max(t1 - t0, 0) * G;
 
-  // item it (query head, 32-row tile) into one of this wave's buffers, by
-  // direct loads: Q and dO rows, then LSE (lanes 0-31) and Delta (32-63).
+  // step it into a buffer by direct loads, the block's wave-wide loads dealt
+  // round the waves: Q and dO rows, then LSE (lanes 0-31) and Delta (32-63).
   // Rows past the end load row 0: finite, never visible.
   const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
-  auto load_item = [&](int it, T* sq, T* sg, float* sl) __attribute__((always_inline)) {
+  auto load_step = [&](int it, Buf& bf) __attribute__((always_inline)) {
     const int h = g * G + it % G;
     const int q0 = (t0 + it / G) * kQ;
 #pragma unroll
-    for (int l = 0; l < Q::kLoads; ++l) {
+    for (int l0 = 0; l0 < Q::kLoads; l0 += kWaves) {
+      const int l = l0 + wave;
+      if (Q::kLoads % kWaves != 0 && l >= Q::kLoads) break;
       const int r = l * Q::kRowsPerLoad + lrow;
       const int pr = q0 + r < rows ? q0 + r : 0;
       const int64_t off = (((int64_t)b * a.q_len + pr) * hq + h) * D + (lpos ^ Q::swz(r)) * kElems16;
       __builtin_amdgcn_global_load_lds((global_void_ptr)(static_cast<const T*>(a.q) + off),
-                                       (lds_void_ptr)(sq + wave * Q::kElems + l * Q::kRowsPerLoad * D), 16, 0, 0);
+                                       (lds_void_ptr)(bf.q + l * Q::kRowsPerLoad * D), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((global_void_ptr)(static_cast<const T*>(a.dout) + off),
-                                       (lds_void_ptr)(sg + wave * Q::kElems + l * Q::kRowsPerLoad * D), 16, 0, 0);
+                                       (lds_void_ptr)(bf.g + l * Q::kRowsPerLoad * D), 16, 0, 0);
     }
-    const int pr = q0 + col < rows ? q0 + col : 0;
-    const int64_t stat = ((int64_t)b * hq + h) * a.q_len + pr;
-    __builtin_amdgcn_global_load_lds((global_void_ptr)(hg ? a.delta + stat : a.lse + stat),
-                                     (lds_void_ptr)(sl + wave * 2 * kQ), 4, 0, 0);
+    if (wave == kWaves - 1) {
+      const int pr = q0 + col < rows ? q0 + col : 0;
+      const int64_t stat = ((int64_t)b * hq + h) * a.q_len + pr;
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(hg ? a.delta + stat : a.lse + stat),
+                                       (lds_void_ptr)bf.l, 4, 0, 0);
+    }
   };
 
   f32x16_t dk[D / 32], dv[D / 32];
@@ -425,35 +447,58 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
 #pragma unroll
     for (int i = 0; i < 16; ++i) dk[db][i] = dv[db][i] = 0.f;
 
-  // one item from buffer kPar while the next one loads into the other
-  auto step = [&](int it, auto par) __attribute__((always_inline)) {
+  // loads per wave and step: its share of the Q and dO loads (the last wave
+  // also loads LSE / Delta)
+  constexpr int kMine = 2 * ((Q::kLoads + kWaves - 1) / kWaves);
+  // step n from buffer kPar while the next kBufs - 1 steps load into the others
+  auto step = [&](int n, auto par) __attribute__((always_inline)) {
     constexpr int kPar = decltype(par)::value;
-    const T* sq = (kPar ? s_q1 : s_q0) + wave * Q::kElems;
-    const T* sg = (kPar ? s_g1 : s_g0) + wave * Q::kElems;
-    const float* sl = (kPar ? s_l1 : s_l0) + wave * 2 * kQ;
-    // this buffer's loads were issued one step ago; nothing else is in flight
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    if (it + kWaves < n_items) load_item(it + kWaves, kPar ? s_q0 : s_q1, kPar ? s_g0 : s_g1, kPar ? s_l0 : s_l1);
-    const int q0 = (t0 + it / G) * kQ;
+    const Buf& bf = buf(par);
+    const T* sq = bf.q;
+    const T* sg = bf.g;
+    const float* sl = bf.l;
+    // this buffer's loads (issued kBufs - 1 steps ago by every wave) have
+    // landed: only the loads of the later steps may remain in flight, kMine
+    // per step (the LSE / Delta load is not counted, so that wave waits a
+    // little longer than it must); then every wave is done with the buffer
+    // the next load refills
+    const int later = min(n_steps - 1 - n, kBufs - 2);
+    if (later >= 2) __builtin_amdgcn_s_waitcnt(wait_vmcnt(2 * kMine));
+    else if (later == 1) __builtin_amdgcn_s_waitcnt(wait_vmcnt(kMine));
+    else __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    if (n + kBufs - 1 < n_steps) load_step(n + kBufs - 1, buf(std::integral_constant<int, kPar + kBufs - 1>()));
+    const int q0 = (t0 + n / G) * kQ;
+    if (q0 + kQ <= wave_from) return;  // no row of the tile sees a key of this wave
 
-    // S = Q K^T and dP = dO V^T: row = query (8*(i/4) + 4*hg + i%4), column = this lane's key
+    // S - LSE/scale and dP - Delta: row = query (8*(i/4) + 4*hg + i%4), column
+    // = this lane's key.  The accumulators start from -LSE/scale and -Delta
+    // of their rows (four consecutive rows at a time), so that P = exp(scale
+    // S - LSE) and dZ = P (dP - Delta) need nothing more per row.
     f32x16_t s, dp;
+    const float neg_inv_scale = -1.f / a.scale;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[i] = dp[i] = 0.f;
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const float4 lv = *reinterpret_cast<const float4*>(sl + 8 * q4 + 4 * hg);
+      const float4 dv4 = *reinterpret_cast<const float4*>(sl + kQ + 8 * q4 + 4 * hg);
+      s[4 * q4] = lv.x * neg_inv_scale; s[4 * q4 + 1] = lv.y * neg_inv_scale;
+      s[4 * q4 + 2] = lv.z * neg_inv_scale; s[4 * q4 + 3] = lv.w * neg_inv_scale;
+      dp[4 * q4] = -dv4.x; dp[4 * q4 + 1] = -dv4.y; dp[4 * q4 + 2] = -dv4.z; dp[4 * q4 + 3] = -dv4.w;
+    }
 #pragma unroll
     for (int kc = 0; kc < kQChunks; ++kc) {
       const int e = hg * kPack + kc * kStep;
-      s = M::mma(tile_a(sq, Q::at(col, e)), M::load(krow + kc * kStep), s);
-      dp = M::mma(tile_a(sg, Q::at(col, e)), M::load(vrow + kc * kStep), dp);
+      s = M::mma(tile_a(sq, Q::at(col, e)), kf[kc], s);
+      dp = M::mma(tile_a(sg, Q::at(col, e)), vf[kc], dp);
     }
     float pr[16], dz[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int r = 8 * (i / 4) + 4 * hg + (i % 4);
       const bool vis = q0 + r >= tau && q0 + r < rows;
-      const float e = fast_exp2(__builtin_fmaf(s[i], a.scale_log2, -sl[r] * kLog2eF));
+      const float e = fast_exp2(s[i] * a.scale_log2);
       pr[i] = vis ? e : 0.f;
-      dz[i] = vis ? e * (dp[i] - sl[kQ + r]) : 0.f;
+      dz[i] = vis ? e * dp[i] : 0.f;
     }
     // dV^T += dO^T P and dK^T += Q^T dZ over the 32 query rows (the row order
     // of the C layout carried into the transposed reads)
@@ -469,39 +514,35 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
     }
   };
 
-  if (wave < n_items) load_item(wave, s_q0, s_g0, s_l0);
-  __syncthreads();  // K and V are staged
-  for (int it = wave; it < n_items; it += 2 * kWaves) {
-    step(it, std::integral_constant<int, 0>());
-    if (it + kWaves < n_items) step(it + kWaves, std::integral_constant<int, 1>());
+  // the first kBufs - 1 steps, then steps in groups of kBufs (compile-time buffers)
+  if (n_steps > 0) load_step(0, buf(std::integral_constant<int, 0>()));
+  if constexpr (kBufs == 4) {
+    if (n_steps > 1) load_step(1, buf(std::integral_constant<int, 1>()));
+    if (n_steps > 2) load_step(2, buf(std::integral_constant<int, 2>()));
   }
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-
-  // sum the waves' partial dK^T / dV^T through LDS, one 32-wide head-dim block
-  // at a time ([wave][d][key] fp32, keys XOR-swizzled by d), and store rows of
-  // keys below the compressed length
-  float* sr = reinterpret_cast<float*>(s_q0);
-  auto reduce_store = [&](const auto& part, float* dst, float sc) __attribute__((always_inline)) {
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      __syncthreads();  // the buffer is free (staging done, or the previous block read)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int d = 8 * (i / 4) + 4 * hg + (i % 4);
-        sr[(wave * 32 + d) * 32 + (col ^ d)] = part[db][i];
-      }
-      __syncthreads();
-      for (int v = tid; v < 32 * 32; v += kThreads) {
-        const int d = v & 31, k = v >> 5;
-        float sum = 0.f;
-#pragma unroll
-        for (int wv = 0; wv < kWaves; ++wv) sum += sr[(wv * 32 + d) * 32 + (k ^ d)];
-        if (kb + k < clen) dst[(((int64_t)b * a.hat_cap + kb + k) * heads + g) * D + 32 * db + d] = sum * sc;
-      }
+  for (int n = 0; n < n_steps; n += kBufs) {
+    step(n, std::integral_constant<int, 0>());
+    if (n + 1 < n_steps) step(n + 1, std::integral_constant<int, 1>());
+    if constexpr (kBufs == 4) {
+      if (n + 2 < n_steps) step(n + 2, std::integral_constant<int, 2>());
+      if (n + 3 < n_steps) step(n + 3, std::integral_constant<int, 3>());
     }
-  };
-  reduce_store(dk, a.dk_hat, a.scale);
-  reduce_store(dv, a.dv_hat, 1.f);
+  }
+
+  // this lane's key: d = 32 db + 8 (i/4) + 4 hg + i%4, four consecutive at a time
+  if (key >= clen) return;
+  float* dkrow = a.dk_hat + (((int64_t)b * a.hat_cap + key) * heads + g) * D + 4 * hg;
+  float* dvrow = a.dv_hat + (((int64_t)b * a.hat_cap + key) * heads + g) * D + 4 * hg;
+  const float sc = a.scale;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int ig = 0; ig < 4; ++ig) {
+      *reinterpret_cast<float4*>(dkrow + 32 * db + 8 * ig) =
+          make_float4(dk[db][4 * ig] * sc, dk[db][4 * ig + 1] * sc, dk[db][4 * ig + 2] * sc, dk[db][4 * ig + 3] * sc);
+      *reinterpret_cast<float4*>(dvrow + 32 * db + 8 * ig) =
+          make_float4(dv[db][4 * ig], dv[db][4 * ig + 1], dv[db][4 * ig + 2], dv[db][4 * ig + 3]);
+    }
 }
 
 template <typename T, int D, int G>
@@ -534,6 +575,11 @@ int prefill_bwd_rows_per_tile(int group) {
     case 4: return PrefillShape<4>::kRows;
     default: return PrefillShape<8>::kRows;
   }
+}
+
+int prefill_bwd_keys_per_block(int dtype, int head_dim) {
+  if (dtype == 1) return head_dim == 128 ? KvBwdShape<bf16_bits, 128>::kKeys : KvBwdShape<bf16_bits, 64>::kKeys;
+  return head_dim == 128 ? KvBwdShape<float, 128>::kKeys : KvBwdShape<float, 64>::kKeys;
 }
 
 hipError_t launch_prefill_bwd(const PrefillBwdArgs& a, int dtype, int head_dim, int group,
