@@ -19,10 +19,13 @@ cache rows written once) and the prefill attention's achieved bf16 TFLOP/s
 against the 2.5 PFLOP/s dense MFMA peak (FLOPs of the visible (row, key) pairs
 only), each from a graph of that kernel alone; HS Compression's pooling of
 the whole hidden state (hidden 2048) on the same batch and spans, in GB/s;
-and the fp64 CPU oracle timed on a bounded sample of the same job.
+the training backward of one layer (attention and pooling gradients) at the
+1596-query prefill workload; and the fp64 CPU oracle timed on a bounded
+sample of the same job.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-full]
     python bench.py --traffic [--workload NAME]   # eager launches for counter runs
+    python bench.py --traffic --train             # one training layer, eagerly
 """
 from __future__ import annotations
 
@@ -177,6 +180,39 @@ def measure_hs_pool(wl, steps, copies=4):
     return res
 
 
+def measure_train_bwd(steps, copies=3):
+    """The training backward of one layer (Sec. III-C) at the 1596-query x
+    471-key prefill workload: attention backward (dQ, dK^, dV^) and pooling
+    backward (raw dK, dV and the gate's du).  `copies` independent jobs run in
+    turn so that no launch finds its inputs left in the last-level cache."""
+    from paper_2607_06827_amd import inputs
+    from paper_2607_06827_amd.workload import TrainJob
+
+    wl = inputs.PREFILL_1500
+    jobs = [TrainJob(wl.with_(seed=wl.seed + i)) for i in range(copies)]
+    for j in jobs:
+        j.run_forward()
+    g_attn = capture(lambda: [j.run_attn_bwd() for j in jobs])
+    g_pool = capture(lambda: [j.run_pool_bwd() for j in jobs])
+    ms_attn = time_graph(g_attn, max(10, steps)) / copies
+    ms_pool = time_graph(g_pool, max(10, steps)) / copies
+    j = jobs[0]
+    flops, abytes, pbytes = j.attn_bwd_flops(), j.attn_bwd_bytes(), j.pool_bwd_bytes()
+    tflops = flops / (ms_attn * 1e-3) / 1e12
+    gbps = pbytes / (ms_pool * 1e-3) / 1e9
+    t_floor = max(flops / (BF16_MFMA_PEAK_TFLOPS * 1e12), abytes / (HBM_PEAK_GBPS * 1e9))
+    log(f"train backward ({wl.name}): attention {ms_attn * 1e3:.1f} us ({tflops:.0f} TFLOP/s), "
+        f"pooling {ms_pool * 1e3:.1f} us ({gbps:.0f} GB/s)")
+    res = {"workload": wl.name,
+           "attn_bwd": {"avg_launch_us": ms_attn * 1e3, "flops_per_launch": flops,
+                        "achieved_tflops": tflops, "frac_of_bf16_mfma_peak": tflops / BF16_MFMA_PEAK_TFLOPS,
+                        "bytes_per_launch": abytes, "roofline_frac": t_floor / (ms_attn * 1e-3)},
+           "pool_bwd": {"avg_launch_us": ms_pool * 1e3, "bytes_per_launch": pbytes,
+                        "achieved_gbps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBPS}}
+    del g_attn, g_pool, jobs
+    return res
+
+
 def cpu_baseline(job, budget_s=15.0):
     """The fp64 oracle on whole sequences of the same job (all layers: pool,
     prefill attention, every decode step), one sequence at a time until about
@@ -229,6 +265,9 @@ def main():
     ap.add_argument("--traffic", action="store_true",
                     help="counter-collection run: the job's launches and one HS pooling launch "
                          "issued eagerly once, then a plain 1 GiB device copy that calibrates the byte counters")
+    ap.add_argument("--train", action="store_true",
+                    help="with --traffic: one training layer of the 1596-query prefill workload "
+                         "instead (forward, then attention and pooling backward)")
     ap.add_argument("--workload", default=None,
                     help="with --traffic: run this workload (by name) instead of the benchmark's")
     args = ap.parse_args()
@@ -243,6 +282,9 @@ def main():
     from paper_2607_06827_amd.workload import Job
 
     wl = inputs.STACK_60S
+    if args.train and not args.traffic:
+        print("--train applies to --traffic runs only", file=sys.stderr)
+        sys.exit(2)
     if args.workload:
         if not args.traffic:
             print("--workload applies to --traffic runs only", file=sys.stderr)
@@ -253,6 +295,19 @@ def main():
             sys.exit(2)
         wl = named[args.workload]
     torch.cuda.set_device(0)
+    if args.train:
+        from paper_2607_06827_amd.workload import TrainJob
+        tj = TrainJob(inputs.PREFILL_1500)
+        tj.run_forward()
+        tj.run_backward()  # attention backward (dQ, then dK/dV), pooling backward (+ du sum)
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"traffic_run": True, "train": True, "workload": tj.wl.name,
+                          "copy_bytes": 1 << 30, "attn_bwd_flops": tj.attn_bwd_flops(),
+                          "attn_bwd_bytes": tj.attn_bwd_bytes(), "pool_bwd_bytes": tj.pool_bwd_bytes()}))
+        return
     log(f"building {wl.name} on {torch.cuda.get_device_name(0)}")
     t0 = time.perf_counter()
     job = Job(wl, num_splits=args.num_splits)
@@ -285,6 +340,8 @@ def main():
         torch.cuda.empty_cache()
 
     hs_pool = measure_hs_pool(wl, args.steps)
+    torch.cuda.empty_cache()
+    train_bwd = measure_train_bwd(args.steps)
     torch.cuda.empty_cache()
 
     dec_bytes, launches = decode_launch_stats(job)
@@ -320,6 +377,7 @@ def main():
         "pool": pooled["pool"],
         "prefill_attn": pooled["prefill_attn"],
         "hs_pool": hs_pool,
+        "train_bwd": train_bwd,
     }
     if full:
         result["full_kv"] = {"tokens_per_s": full["tokens_per_s"], "ms_per_step": full["ms_per_step"],
