@@ -160,6 +160,32 @@ def measure(job, steps, warmup, label):
     return res
 
 
+def measure_adaptive(base, steps, warmup, num_splits):
+    """The same step with a window that grows with depth (adaptive compression
+    ratios across layers, future work in Sec. VI): each compressed layer pools
+    and attends with its own window, so its cache has its own length."""
+    from paper_2607_06827_amd import inputs
+    from paper_2607_06827_amd.workload import Job
+
+    wl = inputs.ADAPTIVE_W_60S
+    job = Job(wl, share_inputs=base, num_splits=num_splits)
+    g_step = capture(job.run)
+    g_dec = capture(lambda: [job.run_decode_step(s) for s in range(wl.decode_steps)])
+    for _ in range(warmup):
+        g_step.replay()
+    ms_step = time_graph(g_step, steps)
+    ms_dec = time_graph(g_dec, max(2, steps))
+    dec_bytes, _ = decode_launch_stats(job)
+    res = {"workload": wl.name, "w_layers": list(wl.w_layers[wl.l0:]), "ms_per_step": ms_step,
+           "tokens_per_s": wl.batch * wl.decode_steps / (ms_step * 1e-3), "decode_ms": ms_dec,
+           "decode_gbps": dec_bytes / (ms_dec * 1e-3) / 1e9,
+           "cache_rows": [job.prefill_clen[i] for i in range(wl.l0, wl.num_layers)]}
+    log(f"adaptive windows: step {ms_step:.3f} ms, decode {ms_dec:.3f} ms "
+        f"({res['decode_gbps']:.0f} GB/s)")
+    del g_step, g_dec, job
+    return res
+
+
 def measure_hs_pool(wl, steps, copies=4):
     """HS Compression's hidden-state pooling on the same batch and spans.
 
@@ -232,8 +258,8 @@ def cpu_baseline(job, budget_s=15.0):
             qd = f64(job.q_dec[i][:, b])
             kn, vn = f64(job.k_new[i][:, b]), f64(job.v_new[i][:, b])
             t0 = time.perf_counter()
-            kh, vh, clen = oracle.pool(k, v, P, T, N, wl.w, l, job.l0, u)
-            oracle.attention(q, kh, vh, P, T, N, wl.w, l, job.l0, 0, job.scale)
+            kh, vh, clen = oracle.pool(k, v, P, T, N, wl.window(l), l, job.l0, u)
+            oracle.attention(q, kh, vh, P, T, N, wl.window(l), l, job.l0, 0, job.scale)
             L = int(clen[0])
             K = np.concatenate([kh[:, :L], kn[None]], axis=1)
             V = np.concatenate([vh[:, :L], vn[None]], axis=1)
@@ -339,6 +365,9 @@ def main():
         del fjob
         torch.cuda.empty_cache()
 
+    adaptive = measure_adaptive(job, args.steps, args.warmup, args.num_splits)
+    adaptive["speedup_over_uniform_w"] = adaptive["tokens_per_s"] / pooled["tokens_per_s"]
+    torch.cuda.empty_cache()
     hs_pool = measure_hs_pool(wl, args.steps)
     torch.cuda.empty_cache()
     train_bwd = measure_train_bwd(args.steps)
@@ -376,6 +405,7 @@ def main():
         "prefill_ms": pooled["prefill_ms"],
         "pool": pooled["pool"],
         "prefill_attn": pooled["prefill_attn"],
+        "adaptive_w": adaptive,
         "hs_pool": hs_pool,
         "train_bwd": train_bwd,
     }

@@ -34,7 +34,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
-from typing import Optional, Sequence
+from typing import Optional, Sequence, Tuple
 
 import numpy as np
 import torch
@@ -64,6 +64,20 @@ class Workload:
     dtype: str           # "bf16" or "f32"
     seed: int
     page_size: int = 16
+    # per-layer window sizes (one per layer, used from l0 on): the adaptive
+    # compression ratio across layers that the paper leaves to future work
+    # (Sec. VI); None gives every compressed layer the window w
+    w_layers: Optional[Tuple[int, ...]] = None
+
+    def __post_init__(self):
+        if self.w_layers is not None:
+            if len(self.w_layers) != self.num_layers or min(self.w_layers) < 1:
+                raise ValueError("w_layers needs one window size >= 1 per layer")
+
+    def window(self, layer: int) -> int:
+        """Window size R of a layer (layers below l0 keep every frame
+        whatever this returns)."""
+        return self.w_layers[layer] if self.w_layers is not None else self.w
 
     @property
     def prefill_len(self) -> int:
@@ -103,6 +117,13 @@ PREFILL_1500 = _wl("qwen3-1.7b-prefill-b8-1596q-471k", batch=8, num_q_heads=16,
                    suffix_len=64, decode_steps=0, w=4, l0=0, num_layers=1,
                    rho=0.9, dtype="bf16", seed=4)
 WORKLOADS = [TINY_F32, LAYER_30S, STACK_60S, LONG_10MIN, PREFILL_1500]
+
+# The 60 s stack with a window that grows with depth (2 for layers 14-17, 4 for
+# 18-23, 8 for 24-27): an instance of per-layer adaptive compression ratios.
+# The paper names them as future work and fixes no schedule; this one is
+# illustrative.
+ADAPTIVE_W_60S = STACK_60S.with_(name="qwen3-1.7b-28L-60s-b64-l0_14-w2_4_8",
+                                 w_layers=(1,) * 14 + (2,) * 4 + (4,) * 6 + (8,) * 4)
 
 
 def stream_seed(seed: int, layer: int, stream: int, step: int = 0) -> int:

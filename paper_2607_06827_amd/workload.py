@@ -93,7 +93,7 @@ class Job:
 
         # caches sized for prefill plus every decoded token
         self.prefill_clen = [speechkv_compressed_len(wl.prefix_len, wl.speech_len, wl.suffix_len,
-                                                     wl.w, l, self.l0) for l in self.layers]
+                                                     wl.window(l), l, self.l0) for l in self.layers]
         self.caches: List[PagedKV] = []
         self.cache_len_out = []
         for i, l in enumerate(self.layers):
@@ -127,24 +127,24 @@ class Job:
         for i, l in enumerate(self.layers):
             if layers is not None and l not in layers:
                 continue
-            speechkv_pool_kv(self.k_raw[i], self.v_raw[i], self.spans, wl.w, self.gate[i], l,
-                             self.l0, self.caches[i], self.cache_len_out[i], stream=stream)
+            speechkv_pool_kv(self.k_raw[i], self.v_raw[i], self.spans, wl.window(l), self.gate[i],
+                             l, self.l0, self.caches[i], self.cache_len_out[i], stream=stream)
             if self.with_prefill:
-                speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.w, l,
+                speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.window(l), l,
                                       self.l0, self.prefill_out, scale=self.scale, stream=stream)
 
     def run_pool(self, stream=None):
         """Pooling of every layer (writes the caches)."""
         wl = self.wl
         for i, l in enumerate(self.layers):
-            speechkv_pool_kv(self.k_raw[i], self.v_raw[i], self.spans, wl.w, self.gate[i], l,
-                             self.l0, self.caches[i], self.cache_len_out[i], stream=stream)
+            speechkv_pool_kv(self.k_raw[i], self.v_raw[i], self.spans, wl.window(l), self.gate[i],
+                             l, self.l0, self.caches[i], self.cache_len_out[i], stream=stream)
 
     def run_prefill_attn(self, stream=None):
         """Prefill attention of every layer over caches already pooled."""
         wl = self.wl
         for i, l in enumerate(self.layers):
-            speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.w, l,
+            speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.window(l), l,
                                   self.l0, self.prefill_out, scale=self.scale, stream=stream)
 
     def decode_out_at(self, i: int, step: int) -> torch.Tensor:
@@ -195,7 +195,7 @@ class Job:
     def prefill_visible_pairs(self, i: int) -> int:
         """(row, visible key) pairs of one sequence's prefill at layer index i."""
         wl = self.wl
-        w = wl.w if self.layers[i] >= self.l0 else 1
+        w = wl.window(self.layers[i]) if self.layers[i] >= self.l0 else 1
         return visible_pairs(wl.prefix_len, wl.speech_len, wl.suffix_len, w)
 
     def prefill_bytes_layer(self, i: int) -> int:
@@ -230,7 +230,7 @@ class HiddenPoolJob:
         self.gate = inputs.normal((self.hidden,), wl.seed * 100 + 72, device=device,
                                   scale=self.hidden ** -0.5)
         self.out_rows = speechkv_compressed_len(wl.prefix_len, wl.speech_len, wl.suffix_len,
-                                                wl.w, 1, 0)
+                                                wl.window(wl.l0), 1, 0)
         self.out = torch.empty(B, self.out_rows, self.hidden, dtype=wl.torch_dtype,
                                device=device)
         self.out_len = torch.empty(B, dtype=torch.int32, device=device)
@@ -239,8 +239,8 @@ class HiddenPoolJob:
                            wl.speech_len, S)
 
     def run(self, stream=None):
-        speechkv_pool_hidden(self.h, self.spans, self.wl.w, self.gate, self.out, self.out_len,
-                             stream)
+        speechkv_pool_hidden(self.h, self.spans, self.wl.window(self.wl.l0), self.gate, self.out,
+                             self.out_len, stream)
 
     def bytes(self) -> int:
         """Algorithmic HBM bytes of one launch: every input row read once,
@@ -263,6 +263,7 @@ class TrainJob:
         self.fwd = Job(wl, device=device, layers=[layer])
         self.wl = wl
         self.layer = layer
+        self.w = wl.window(layer)
         f = self.fwd
         B, S, Hq, Hkv, D = wl.batch, wl.prefill_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
         dev = f.device
@@ -282,20 +283,20 @@ class TrainJob:
 
     def run_forward(self, stream=None):
         f, wl = self.fwd, self.wl
-        speechkv_pool_kv(f.k_raw[0], f.v_raw[0], f.spans, wl.w, f.gate[0], self.layer, f.l0,
+        speechkv_pool_kv(f.k_raw[0], f.v_raw[0], f.spans, self.w, f.gate[0], self.layer, f.l0,
                          f.caches[0], stream=stream)
-        speechkv_prefill_attn(f.q_prefill[0], f.caches[0], f.spans, wl.w, self.layer, f.l0,
+        speechkv_prefill_attn(f.q_prefill[0], f.caches[0], f.spans, self.w, self.layer, f.l0,
                               self.out, scale=f.scale, lse=self.lse, stream=stream)
 
     def run_attn_bwd(self, stream=None):
         f, wl = self.fwd, self.wl
-        speechkv_prefill_attn_bwd(f.q_prefill[0], f.caches[0], f.spans, wl.w, self.layer, f.l0,
+        speechkv_prefill_attn_bwd(f.q_prefill[0], f.caches[0], f.spans, self.w, self.layer, f.l0,
                                   self.out, self.lse, self.dout, self.dq, self.dk_hat, self.dv_hat,
                                   self.workspace, scale=f.scale, stream=stream)
 
     def run_pool_bwd(self, stream=None):
         f, wl = self.fwd, self.wl
-        speechkv_pool_kv_bwd(f.k_raw[0], f.v_raw[0], f.spans, wl.w, f.gate[0], self.layer, f.l0,
+        speechkv_pool_kv_bwd(f.k_raw[0], f.v_raw[0], f.spans, self.w, f.gate[0], self.layer, f.l0,
                              self.dk_hat, self.dv_hat, self.dk_raw, self.dv_raw, self.du,
                              self.workspace, stream=stream)
 

@@ -121,7 +121,8 @@ def oracle_pool_for(job, i: int, b: int):
     k = f64(job.k_raw[i][b:b + 1])
     v = f64(job.v_raw[i][b:b + 1])
     u = f64(job.gate[i])
-    return oracle.pool(k, v, [wl.prefix_len], [wl.speech_len], [wl.suffix_len], wl.w, l, job.l0, u)
+    return oracle.pool(k, v, [wl.prefix_len], [wl.speech_len], [wl.suffix_len], wl.window(l), l,
+                       job.l0, u)
 
 
 def oracle_decode_for(job, i: int, b: int, step: int, pooled=None):
@@ -147,6 +148,6 @@ def oracle_prefill_for(job, i: int, bs, mode: int = 0):
     u = f64(job.gate[i])
     n = len(bs)
     P, T, N = [wl.prefix_len] * n, [wl.speech_len] * n, [wl.suffix_len] * n
-    kh, vh, _ = oracle.pool(k, v, P, T, N, wl.w, l, job.l0, u)
+    kh, vh, _ = oracle.pool(k, v, P, T, N, wl.window(l), l, job.l0, u)
     q = f64(job.q_prefill[i][bs])
-    return oracle.attention(q, kh, vh, P, T, N, wl.w, l, job.l0, mode, job.scale)
+    return oracle.attention(q, kh, vh, P, T, N, wl.window(l), l, job.l0, mode, job.scale)

@@ -2,6 +2,7 @@
 import math
 
 import numpy as np
+import pytest
 import torch
 
 from paper_2607_06827_amd import inputs
@@ -71,3 +72,13 @@ def test_workload_shapes():
     assert [w.prefill_len for w in inputs.WORKLOADS] == [68, 407, 782, 7532, 1596]
     assert inputs.PREFILL_1500.prefix_len + inputs.PREFILL_1500.speech_len + inputs.PREFILL_1500.suffix_len == 1596
     assert np.all([w.num_q_heads % w.num_kv_heads == 0 for w in inputs.WORKLOADS])
+
+
+def test_per_layer_windows():
+    wl = inputs.ADAPTIVE_W_60S
+    assert [wl.window(l) for l in (13, 14, 17, 18, 23, 24, 27)] == [1, 2, 2, 4, 4, 8, 8]
+    assert inputs.STACK_60S.window(20) == inputs.STACK_60S.w
+    with pytest.raises(ValueError):
+        inputs.STACK_60S.with_(w_layers=(4,) * 27)
+    with pytest.raises(ValueError):
+        inputs.STACK_60S.with_(w_layers=(0,) + (4,) * 27)
