@@ -186,6 +186,33 @@ def measure_adaptive(base, steps, warmup, num_splits):
     return res
 
 
+def measure_fused(base, steps, copies=3):
+    """Pooling and prefill attention as one launch (pooling on the fly inside
+    the attention, Sec. III-C) against the two launches: at the 1596-query
+    workload (one layer, `copies` jobs in turn so that no launch finds its
+    inputs in the last-level cache) and over the prefill of the whole stack."""
+    from paper_2607_06827_amd import inputs
+    from paper_2607_06827_amd.workload import Job
+
+    wl = inputs.PREFILL_1500
+    jobs = [Job(wl.with_(seed=wl.seed + i)) for i in range(copies)]
+    g_split = capture(lambda: [j.run_prefill() for j in jobs])
+    g_fused = capture(lambda: [j.run_prefill_fused() for j in jobs])
+    us_split = time_graph(g_split, max(10, steps)) / copies * 1e3
+    us_fused = time_graph(g_fused, max(10, steps)) / copies * 1e3
+    del g_split, g_fused, jobs
+    g_split = capture(base.run_prefill)
+    g_fused = capture(base.run_prefill_fused)
+    ms_split = time_graph(g_split, max(2, steps))
+    ms_fused = time_graph(g_fused, max(2, steps))
+    del g_split, g_fused
+    log(f"fused pool+prefill ({wl.name}): {us_fused:.1f} us against {us_split:.1f} us as two "
+        f"launches; stack prefill {ms_fused:.3f} ms against {ms_split:.3f} ms")
+    return {"workload": wl.name, "fused_us": us_fused, "split_us": us_split,
+            "fused_over_split": us_fused / us_split, "stack_workload": base.wl.name,
+            "stack_prefill_fused_ms": ms_fused, "stack_prefill_split_ms": ms_split}
+
+
 def measure_hs_pool(wl, steps, copies=4):
     """HS Compression's hidden-state pooling on the same batch and spans.
 
@@ -365,6 +392,8 @@ def main():
         del fjob
         torch.cuda.empty_cache()
 
+    fused = measure_fused(job, args.steps)
+    torch.cuda.empty_cache()
     adaptive = measure_adaptive(job, args.steps, args.warmup, args.num_splits)
     adaptive["speedup_over_uniform_w"] = adaptive["tokens_per_s"] / pooled["tokens_per_s"]
     torch.cuda.empty_cache()
@@ -405,6 +434,7 @@ def main():
         "prefill_ms": pooled["prefill_ms"],
         "pool": pooled["pool"],
         "prefill_attn": pooled["prefill_attn"],
+        "fused_prefill": fused,
         "adaptive_w": adaptive,
         "hs_pool": hs_pool,
         "train_bwd": train_bwd,

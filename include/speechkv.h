@@ -18,6 +18,8 @@
  *   speechkv_prefill_attn  full-resolution queries over the cache (Eq. 5 + mask)
  *   speechkv_pool_hidden   the same pooling applied to whole hidden states
  *                          (HS Compression, Sec. IV-A method (4))
+ *   speechkv_pool_prefill_attn  pooling and prefill attention in one launch,
+ *                          the pooling done on the fly (Sec. III-C)
  * and two more carry its training (Sec. III-C: the pooling runs inside the
  * forward pass and is optimised jointly with the model):
  *   speechkv_prefill_attn_bwd  gradients of speechkv_prefill_attn: dQ, dK^, dV^
@@ -64,7 +66,7 @@ extern "C" {
 #define SPEECHKV_ERR_INVALID_ARG (-1) /* null pointer, bad size or count      */
 #define SPEECHKV_ERR_UNSUPPORTED (-2) /* dtype, head_dim, G or page_size      */
 #define SPEECHKV_ERR_WORKSPACE (-3)   /* workspace missing or too small       */
-#define SPEECHKV_ERR_ALIAS (-4)       /* raw K/V overlap the destination pool */
+#define SPEECHKV_ERR_ALIAS (-4)       /* a buffer written overlaps one read or another written */
 #define SPEECHKV_ERR_HIP (-5)         /* the HIP runtime refused a launch     */
 
 /* Element types. */
@@ -290,6 +292,39 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
                           const speechkv_spans* spans, int32_t w, int32_t layer,
                           int32_t l0, int32_t mask_mode, float scale, void* out,
                           float* lse, void* stream);
+
+/*
+ * speechkv_pool_prefill_attn - speechkv_pool_kv followed by
+ * speechkv_prefill_attn in one launch: the attention reads the raw keys and
+ * values and pools each key tile on the fly (Sec. III-C: in training the
+ * pooling of Eq. 4 runs inside the forward pass), and the pooled rows are
+ * stored into the paged cache as well, so that decoding (or the backward)
+ * can follow.
+ *
+ * The cache, cache_len_out, out and lse receive exactly what the two calls
+ * would write, bit for bit: the pooled rows come from the same arithmetic,
+ * and the attention over them is the same.  Every pooled row is stored once,
+ * also rows that no query sees.
+ *
+ * q, out, q_len, num_q_heads, mask_mode, scale, lse  as for
+ *                speechkv_prefill_attn.
+ * k_raw, v_raw, stride_b, stride_s, stride_h, raw_len, w, gate_u, layer, l0,
+ * cache_len_out  as for speechkv_pool_kv; max_total_len must not exceed
+ *                raw_len or q_len.
+ * cache          host pointer to the cache description; written as by
+ *                speechkv_pool_kv.  dtype must be SPEECHKV_DTYPE_BF16.
+ * Nothing written (the pages, out, lse) may overlap anything read (q, the raw
+ * K/V, the gate) or another written buffer (ALIAS).
+ * Errors: INVALID_ARG, UNSUPPORTED (also for fp32), ALIAS, HIP.
+ */
+int speechkv_pool_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
+                               int32_t q_len, const void* k_raw, const void* v_raw,
+                               int64_t stride_b, int64_t stride_s, int64_t stride_h,
+                               int32_t raw_len, const speechkv_spans* spans, int32_t w,
+                               const float* gate_u, int32_t layer, int32_t l0,
+                               const speechkv_paged_kv* cache, int32_t* cache_len_out,
+                               int32_t mask_mode, float scale, void* out, float* lse,
+                               void* stream);
 
 /*
  * speechkv_prefill_attn_bwd - gradients of speechkv_prefill_attn with respect

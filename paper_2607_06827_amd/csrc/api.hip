@@ -8,6 +8,7 @@
 
 #include "kernels.hpp"
 #include "kernels_bwd.hpp"
+#include "kernels_fused.hpp"
 
 namespace {
 
@@ -118,7 +119,7 @@ const char* speechkv_status_string(int status) {
     case SPEECHKV_ERR_INVALID_ARG: return "invalid argument";
     case SPEECHKV_ERR_UNSUPPORTED: return "unsupported dtype, head_dim, group size or page size";
     case SPEECHKV_ERR_WORKSPACE: return "workspace missing or too small";
-    case SPEECHKV_ERR_ALIAS: return "raw K/V overlap the destination page pool";
+    case SPEECHKV_ERR_ALIAS: return "a buffer written overlaps one read or another written";
     case SPEECHKV_ERR_HIP: return "HIP runtime error";
     default: return "unknown status";
   }
@@ -316,6 +317,91 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int
   a.scale_log2 = scale * 1.4426950408889634f;
   return status_of(skv::launch_prefill(a, cache->dtype, cache->head_dim, group, batch,
                                        static_cast<hipStream_t>(stream)));
+}
+
+int speechkv_pool_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                               const void* k_raw, const void* v_raw, int64_t stride_b,
+                               int64_t stride_s, int64_t stride_h, int32_t raw_len,
+                               const speechkv_spans* spans, int32_t w, const float* gate_u,
+                               int32_t layer, int32_t l0, const speechkv_paged_kv* cache,
+                               int32_t* cache_len_out, int32_t mask_mode, float scale, void* out,
+                               float* lse, void* stream) {
+  if (!q || !out || !k_raw || !v_raw) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_cache(cache);
+  if (st) return st;
+  if ((st = check_spans(spans))) return st;
+  if (cache->dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
+  if (batch < 1 || batch > kMaxGrid || q_len < 1 || q_len > kMaxRows || raw_len < 1 ||
+      raw_len > kMaxRows || w < 1 || w > SPEECHKV_MAX_WINDOW || layer < 0 || l0 < 0)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (mask_mode != SPEECHKV_MASK_WINDOW_END && mask_mode != SPEECHKV_MASK_WINDOW_START)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if (spans->max_total_len > q_len || spans->max_total_len > raw_len) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || scale > 3.0e38f) return SPEECHKV_ERR_INVALID_ARG;  // finite, > 0
+  if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
+  const int group = group_of(num_q_heads, cache->num_kv_heads);
+  if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
+  if (stride_b < 0 || stride_s < 0 || stride_h < 0) return SPEECHKV_ERR_INVALID_ARG;
+  const int esz = elt_size(cache->dtype);
+  const int D = cache->head_dim;
+  const int64_t per16 = 16 / esz;
+  if (stride_b % per16 || stride_s % per16 || stride_h % per16) return SPEECHKV_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(out) || !aligned16(k_raw) || !aligned16(v_raw) ||
+      (gate_u && !aligned16(gate_u)) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
+    return SPEECHKV_ERR_INVALID_ARG;
+  // nothing written (pages, out, lse) may overlap anything read (q, raw K/V,
+  // gate) or another written region
+  const int64_t raw_bytes = ((int64_t)(batch - 1) * stride_b + (int64_t)(raw_len - 1) * stride_s +
+                             (int64_t)(cache->num_kv_heads - 1) * stride_h + D) * esz;
+  const int64_t qo_bytes = (int64_t)batch * q_len * num_q_heads * D * esz;
+  const int64_t lse_bytes = (int64_t)batch * num_q_heads * q_len * 4;
+  const int64_t pool_bytes = page_pool_bytes(cache);
+  const int64_t gate_bytes = (int64_t)cache->num_kv_heads * D * 4;
+  const void* rd[] = {q, k_raw, v_raw, gate_u};
+  const int64_t rd_n[] = {qo_bytes, raw_bytes, raw_bytes, gate_bytes};
+  const void* wr[] = {cache->k_pages, cache->v_pages, out, lse};
+  const int64_t wr_n[] = {pool_bytes, pool_bytes, qo_bytes, lse_bytes};
+  for (int i = 0; i < 4; ++i) {
+    if (!wr[i]) continue;
+    for (int j = 0; j < 4; ++j)
+      if (rd[j] && overlaps(wr[i], wr_n[i], rd[j], rd_n[j])) return SPEECHKV_ERR_ALIAS;
+    for (int j = i + 1; j < 4; ++j)
+      if (wr[j] && overlaps(wr[i], wr_n[i], wr[j], wr_n[j])) return SPEECHKV_ERR_ALIAS;
+  }
+  const int rows_per_tile = skv::prefill_fused_rows_per_tile(group);
+  // at least one tile per (sequence, head): tile 0 writes cache_len_out
+  int64_t tiles = (spans->max_total_len + rows_per_tile - 1) / rows_per_tile;
+  if (tiles < 1) tiles = 1;
+  if ((int64_t)batch * cache->num_kv_heads * tiles > INT32_MAX) return SPEECHKV_ERR_INVALID_ARG;
+  skv::PrefillFusedArgs f;
+  skv::PrefillArgs& a = f.at;
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.k_pages = cache->k_pages;
+  a.v_pages = cache->v_pages;
+  a.table = cache->block_table;
+  a.pv = view_of(cache);
+  a.prefix_len = spans->prefix_len;
+  a.speech_len = spans->speech_len;
+  a.suffix_len = spans->suffix_len;
+  a.w_eff = layer >= l0 ? w : 1;
+  a.mask_mode = mask_mode;
+  a.q_len = q_len;
+  a.num_tiles = (int)tiles;
+  a.num_q_heads = num_q_heads;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  f.k_pages = cache->k_pages;
+  f.v_pages = cache->v_pages;
+  f.k_raw = k_raw;
+  f.v_raw = v_raw;
+  f.stride_b = stride_b;
+  f.stride_s = stride_s;
+  f.stride_h = stride_h;
+  f.raw_len = raw_len;
+  f.gate = gate_u;
+  f.cache_len_out = cache_len_out;
+  return status_of(skv::launch_prefill_fused(f, D, group, batch, static_cast<hipStream_t>(stream)));
 }
 
 size_t speechkv_prefill_attn_bwd_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t q_len) {

@@ -18,6 +18,7 @@
 // The kernel reads each raw row once and writes each cache row once: it is
 // bound by HBM bandwidth.
 #include "kernels.hpp"
+#include "pool_window.hpp"
 
 namespace skv {
 
@@ -27,7 +28,6 @@ template <typename T, int D, bool kGate>
 __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   constexpr int kLanes = D / 8;          // lanes per unit
   constexpr int kUnits = 256 / kLanes;   // units per block
-  constexpr float kLog2e = 1.4426950408889634f;
 
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
@@ -47,9 +47,8 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   if (c64 >= len || c64 >= a.max_out) return;
   const int c = (int)c64;
 
-  const bool text_before = c < P, text_after = c >= P + nW;
-  const int src = text_before ? c : text_after ? P + S + (c - P - nW) : P + (c - P) * w;
-  const int frames = (text_before || text_after) ? 1 : min(w, P + S - src);
+  const SlotSource sl(c, P, S, nW, w);
+  const int src = sl.first, frames = sl.frames;
   // page of slot c: the entry is loaded now and checked only before the stores
   const int idx = c >> a.pv.page_shift;
   const int32_t entry = a.table[(int64_t)b * a.pv.max_pages + min(idx, a.pv.max_pages - 1)];
@@ -85,10 +84,8 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
     u[4] = u1.x; u[5] = u1.y; u[6] = u1.z; u[7] = u1.w;
   }
 
-  float m = neg_inf(), l = 0.f, ak[8], av[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) ak[i] = av[i] = 0.f;
-
+  WindowPool<T, kLanes> wp;
+  wp.init();
   for (int f0 = 0; f0 < frames; f0 += 4) {
     // all eight loads in flight; frames past the window repeat its last one
     Chunk<T> kc[4], vc[4];
@@ -98,49 +95,10 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
       kc[t].load(kr + o);
       vc[t].load(vr + o);
     }
-    float kf[4][8], s[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      kc[t].to_float(kf[t]);
-      float part = 0.f;
-      if constexpr (kGate) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) part = __builtin_fmaf(u[i], kf[t][i], part);
-        part = group_sum<kLanes>(part);
-      }
-      s[t] = f0 + t < frames ? part * kLog2e : neg_inf();  // log2 units
-    }
-    const float mn = fmaxf(m, fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
-    const float corr = fast_exp2(m - mn);  // m = -inf on the first group gives 0
-    l *= corr;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      ak[i] *= corr;
-      av[i] *= corr;
-    }
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const float p = fast_exp2(s[t] - mn);
-      float vf[8];
-      vc[t].to_float(vf);
-      l += p;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        ak[i] = __builtin_fmaf(p, kf[t][i], ak[i]);
-        av[i] = __builtin_fmaf(p, vf[i], av[i]);
-      }
-    }
-    m = mn;
-  }
-  const float inv = 1.f / l;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    ak[i] *= inv;
-    av[i] *= inv;
+    wp.template add4<kGate>(kc, vc, u, f0, frames);
   }
   Chunk<T> ko, vo;
-  ko.from_float(ak);
-  vo.from_float(av);
+  wp.finish(ko, vo);
   if (writable()) {
     ko.store(static_cast<T*>(a.k_pages) + dst());
     vo.store(static_cast<T*>(a.v_pages) + dst());

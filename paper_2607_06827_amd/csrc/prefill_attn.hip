@@ -40,6 +40,8 @@
 
 #include "attn_mfma.hpp"
 #include "kernels.hpp"
+#include "kernels_fused.hpp"
+#include "pool_window.hpp"
 
 namespace skv {
 
@@ -336,19 +338,58 @@ struct LdsSwz {
 };
 
 // Waves per SIMD the compiler must fit: three where the registers allow it
-// without spilling (it measured faster than two at the same tile sizes).
-template <int D, int G>
-constexpr int lds_kernel_waves() { return D == 128 && G == 4 ? 2 : 3; }
+// without spilling (it measured faster than two at the same tile sizes); two
+// when the kernel also pools its tiles (the first frames of the next tile's
+// windows are held in registers across a step).
+template <int D, int G, bool kFused>
+constexpr int lds_kernel_waves() { return kFused || (D == 128 && G == 4) ? 2 : 3; }
 
-template <int D, int G>
-__global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>())) void prefill_kernel_lds(PrefillArgs a) {
+// Block shape of the pooling variant: eight waves whatever the group size, so
+// a block owns 256/G query rows.  Every block pools each key tile it reads,
+// so taller blocks pool each tile fewer times over the whole grid, and eight
+// waves share the work of a tile (one pass of D/8-lane units at D = 128).
+template <int G>
+struct FusedShape {
+  static constexpr int kRowBlocks = 8 / G;
+  static constexpr int kWaves = 8;
+  static constexpr int kThreads = 512;
+  static constexpr int kRows = 32 * kRowBlocks;
+};
+template <int G, bool kFused>
+using LdsShape = typename std::conditional<kFused, FusedShape<G>, PrefillShape<G>>::type;
+template <int G, bool kFused>
+constexpr int lds_threads() { return LdsShape<G, kFused>::kThreads; }
+
+template <bool kFused>
+struct LdsArgs {
+  typedef PrefillArgs type;
+};
+template <>
+struct LdsArgs<true> {
+  typedef PrefillFusedArgs type;
+};
+__device__ __host__ __forceinline__ const PrefillArgs& attn_args(const PrefillArgs& a) { return a; }
+__device__ __host__ __forceinline__ const PrefillArgs& attn_args(const PrefillFusedArgs& a) { return a.at; }
+
+// kFused = false: K/V tiles come from the paged cache by direct loads.
+// kFused = true: the kernel reads the raw K/V instead and pools each key tile
+// on the fly (Sec. III-C) with the pooling kernel's steps (pool_window.hpp),
+// D/8 lanes per (slot, head) unit: the first four frames of every window of
+// tile t+1 are loaded before the MFMAs of tile t and pooled after them,
+// straight into the other LDS buffer in the layout the direct loads give.
+// The block holding a sequence's last query rows (which see every key) also
+// stores each pooled row into the paged cache, and pools the rows no query
+// sees, so the cache ends up as the pooling kernel would have written it.
+template <int D, int G, bool kFused>
+__global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G, kFused>())) void prefill_kernel_lds(typename LdsArgs<kFused>::type args) {
+  const PrefillArgs& a = attn_args(args);
   typedef bf16_bits T;
   typedef Mfma<T> M;
   typedef M::Frag Frag;
   typedef LdsSwz<D> Swz;
-  constexpr int kThreads = PrefillShape<G>::kThreads;
-  constexpr int kWaves = PrefillShape<G>::kWaves;
-  constexpr int kRows = PrefillShape<G>::kRows;
+  constexpr int kThreads = LdsShape<G, kFused>::kThreads;
+  constexpr int kWaves = LdsShape<G, kFused>::kWaves;
+  constexpr int kRows = LdsShape<G, kFused>::kRows;
   constexpr int kKeys = 32;                        // keys per tile
   constexpr int kPack = M::kPack;
   constexpr int kStep = 2 * kPack;                 // head-dim elements per QK MFMA
@@ -384,6 +425,9 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
   const int rows = min(P + T_ + N, a.q_len);
   const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
+  if constexpr (kFused) {
+    if (tile == 0 && g == 0 && threadIdx.x == 0 && args.cache_len_out) args.cache_len_out[b] = P + nW + N;
+  }
   if (p0 >= rows) return;
   const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
   const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
@@ -409,6 +453,125 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
   const bool loads = kLoads >= kWaves || wave < kLoads;
   auto load_row0 = [&](int i) { return (kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * kRowsPerLoad; };
   const int lrow = lane / kChunks, lpos = lane % kChunks;  // row within the load, LDS chunk position
+
+  // on-the-fly pooling (kFused): D/8 lanes per (slot, head) unit, one unit
+  // per key of the tile; the first kPoolWaves waves pool, lane pj-th chunk
+  // of unit pslot.  The first four frames of each unit's window are staged
+  // by direct loads into this wave's own LDS area (lane i's 16 bytes of
+  // frame t at K: 2t KB + 16 i, V: 2t+1 KB + 16 i), so they cost no
+  // registers across the MFMAs and each lane reads back only what it loaded.
+  constexpr int kLanes = D / 8;
+  constexpr int kPoolWaves = kKeys / (64 / kLanes);
+  static_assert(!kFused || kPoolWaves <= kWaves, "one pass of the pooling waves covers a tile");
+  const int pj = lane % kLanes;
+  const int pslot = wave * (64 / kLanes) + lane / kLanes;
+  const bool pool_wave = wave < kPoolWaves;  // uniform over the wave
+  const bool writer = p0 + kRows >= rows;   // holds the last rows: sees every key
+  int fsrc = 0, ffr = 1, fent = 0;          // the unit's first raw row, frames, page
+  float u[8];
+  const T* kr = nullptr;
+  const T* vr = nullptr;
+  T* stage = nullptr;  // this wave's staging area
+  int64_t raw_stride = 0;
+  int raw_last = 0;
+  if constexpr (kFused) {
+    __shared__ __attribute__((aligned(16))) T s_stage[kPoolWaves * 8 * 512];
+    stage = s_stage + (pool_wave ? wave : 0) * 8 * 512;
+    kr = static_cast<const T*>(args.k_raw) + b * args.stride_b + g * args.stride_h + 8 * pj;
+    vr = static_cast<const T*>(args.v_raw) + b * args.stride_b + g * args.stride_h + 8 * pj;
+    raw_stride = args.stride_s;
+    raw_last = args.raw_len - 1;
+    if (args.gate) {  // without a gate every logit is 0 (uniform averaging)
+      const float4* gp = reinterpret_cast<const float4*>(args.gate + (int64_t)g * D + 8 * pj);
+      const float4 u0 = gp[0], u1 = gp[1];
+      u[0] = u0.x; u[1] = u0.y; u[2] = u0.z; u[3] = u0.w;
+      u[4] = u1.x; u[5] = u1.y; u[6] = u1.z; u[7] = u1.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) u[i] = 0.f;
+    }
+  }
+  auto raw_at = [&](int s) __attribute__((always_inline)) { return (int64_t)min(s, raw_last) * raw_stride; };
+  // stage the first four frames of unit (slot min(c0 + pslot, cmax), this
+  // head); frames past a window repeat its last one; w = 1 needs one frame
+  auto pool_fetch = [&](int c0, int cmax) __attribute__((always_inline)) {
+    if (!pool_wave) return;
+    const int c = min(c0 + pslot, cmax);
+    const SlotSource sl(c, P, T_, nW, w);
+    fsrc = sl.first;
+    ffr = sl.frames;
+    fent = writer ? table_row[min(c >> shift, a.pv.max_pages - 1)] : 0;
+    const int nt = w == 1 ? 1 : 4;  // uniform
+    for (int t = 0; t < nt; ++t) {
+      const int64_t o = raw_at(sl.first + min(t, sl.frames - 1));
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(kr + o), (lds_void_ptr)(stage + 2 * t * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((global_void_ptr)(vr + o), (lds_void_ptr)(stage + (2 * t + 1) * 512), 16, 0, 0);
+    }
+  };
+  // the unit's pooled rows from the staged frames (and the later frames of
+  // windows longer than four); a text row or one-frame window is its raw row
+  auto pool_rows = [&](Chunk<T>& ko, Chunk<T>& vo) __attribute__((always_inline)) {
+    // the wave's own direct loads must have landed before it reads them back:
+    // the compiler does not order LDS-DMA writes against later LDS reads, so
+    // wait explicitly, fenced on both sides for the optimiser and scheduler
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    Chunk<T> kc[4], vc[4];
+    const int nt = w == 1 ? 1 : 4;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      if (t < nt) {
+        kc[t].raw = *reinterpret_cast<const uint4*>(stage + 2 * t * 512 + 8 * lane);
+        vc[t].raw = *reinterpret_cast<const uint4*>(stage + (2 * t + 1) * 512 + 8 * lane);
+      }
+    }
+    ko = kc[0];
+    vo = vc[0];
+    if (w > 1) {
+      WindowPool<T, kLanes> wp;
+      wp.init();
+      wp.template add4<true>(kc, vc, u, 0, ffr);
+      for (int f0 = 4; f0 < ffr; f0 += 4) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int64_t o = raw_at(fsrc + min(f0 + t, ffr - 1));
+          kc[t].load(kr + o);
+          vc[t].load(vr + o);
+        }
+        wp.template add4<true>(kc, vc, u, f0, ffr);
+      }
+      Chunk<T> pk, pv;
+      wp.finish(pk, pv);
+      if (ffr > 1) {
+        ko = pk;
+        vo = pv;
+      }
+    }
+  };
+  // cache row c of this head, when it exists, has a valid page and its
+  // source rows lie inside the raw tensor (as the pooling kernel checks)
+  auto cache_store = [&](int c, const Chunk<T>& ko, const Chunk<T>& vo) __attribute__((always_inline)) {
+    if constexpr (kFused) {
+      if (c < clen && fent >= 0 && fent < num_pages && fsrc + ffr <= raw_last + 1) {
+        const int64_t off = page_row<D>(fent, g, c & slot_mask, a.pv) + 8 * pj;
+        ko.store(static_cast<T*>(args.k_pages) + off);
+        vo.store(static_cast<T*>(args.v_pages) + off);
+      }
+    }
+  };
+  // pool key tile kt into LDS; the writer also stores its visible rows
+  auto pool_tile = [&](int kt, T* sk, T* sv) __attribute__((always_inline)) {
+    if (!pool_wave) return;
+    Chunk<T> ko, vo;
+    pool_rows(ko, vo);
+    const int r = pslot;
+    ko.store(sk + r * D + ((pj ^ Swz::k(r)) << 3));
+    vo.store(sv + r * D + ((pj ^ Swz::v(r)) << 3));
+    if (writer && kt * kKeys + r < kmax) cache_store(kt * kKeys + r, ko, vo);
+  };
 
   f32x16_t o[D / 32];
 #pragma unroll
@@ -443,9 +606,13 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
 
   // prologue: tables of tiles 0 and 1, tile 0 into LDS, then this lane's query
   // row (issued after the tile: the memory counter is in order)
-  table_load(0, pg[0]);
-  table_load(1, pg[1]);
-  tile_load(0, pg[0], s_k0, s_v0);
+  if constexpr (kFused) {
+    if (ntiles > 0) pool_fetch(0, kclamp);
+  } else {
+    table_load(0, pg[0]);
+    table_load(1, pg[1]);
+    tile_load(0, pg[0], s_k0, s_v0);
+  }
   __builtin_amdgcn_sched_barrier(0);
   Frag qf[kQChunks];
   {
@@ -453,7 +620,11 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
 #pragma unroll
     for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = M::load(qrow + kc * kStep + hg * kPack);
   }
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  if constexpr (kFused) {
+    if (ntiles > 0) pool_tile(0, s_k0, s_v0);
+  } else {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  }
   __syncthreads();
 
   // one step; kPar = kt & 1 selects buffers and table registers at compile time
@@ -463,8 +634,13 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
     T* const sv = kPar ? s_v1 : s_v0;
     T* const sk_next = kPar ? s_k0 : s_k1;
     T* const sv_next = kPar ? s_v0 : s_v1;
-    table_load(kt + 2, pg[kPar]);                     // parity of kt+2 = kt
-    tile_load(kt + 1, pg[1 - kPar], sk_next, sv_next);  // into the buffer tile kt-1 used
+    const bool pool_next = kt + 1 < ntiles;  // uniform
+    if constexpr (kFused) {
+      if (pool_next) pool_fetch((kt + 1) * kKeys, kclamp);  // pooled after this tile's MFMAs
+    } else {
+      table_load(kt + 2, pg[kPar]);                     // parity of kt+2 = kt
+      tile_load(kt + 1, pg[1 - kPar], sk_next, sv_next);  // into the buffer tile kt-1 used
+    }
     if (kt < ntiles) {  // (the loop runs an even number of steps)
       const int kb = kt * kKeys;
       // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
@@ -535,9 +711,13 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
         }
       }
     }
-    // the next tile's rows (and the table entries after them) have landed in
-    // every wave's part of the buffer once each wave's counter is at zero
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    if constexpr (kFused) {
+      if (pool_next) pool_tile(kt + 1, sk_next, sv_next);
+    } else {
+      // the next tile's rows (and the table entries after them) have landed in
+      // every wave's part of the buffer once each wave's counter is at zero
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    }
     __syncthreads();
   };
   // two steps per iteration so that buffers and registers are compile-time;
@@ -545,6 +725,19 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, (lds_kernel_waves<D, G>(
   for (int kt = 0; kt < ntiles; kt += 2) {
     tile_step(kt, std::integral_constant<int, 0>());
     tile_step(kt + 1, std::integral_constant<int, 1>());
+  }
+  if constexpr (kFused) {
+    // cache rows no query of this sequence sees: pooled and stored by the writer
+    if (writer) {
+      for (int c0 = kmax; c0 < clen; c0 += kKeys) {
+        pool_fetch(c0, clen - 1);
+        if (pool_wave) {
+          Chunk<T> ko, vo;
+          pool_rows(ko, vo);
+          cache_store(c0 + pslot, ko, vo);
+        }
+      }
+    }
   }
 
   const float l_tot = partner_sum(l_run);
@@ -599,14 +792,15 @@ hipError_t launch_prefill_d(const PrefillArgs& a, int group, int batch, hipStrea
   }
 }
 
-template <int D>
-hipError_t launch_prefill_lds(const PrefillArgs& a, int group, int batch, hipStream_t s) {
+template <int D, bool kFused>
+hipError_t launch_prefill_lds(const typename LdsArgs<kFused>::type& args, int group, int batch, hipStream_t s) {
+  const PrefillArgs& a = attn_args(args);
   const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
   switch (group) {
-    case 1: return launch_struct(prefill_kernel_lds<D, 1>, dim3(items), dim3(PrefillShape<1>::kThreads), s, a);
-    case 2: return launch_struct(prefill_kernel_lds<D, 2>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
-    case 4: return launch_struct(prefill_kernel_lds<D, 4>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
-    default: return launch_struct(prefill_kernel_lds<D, 8>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
+    case 1: return launch_struct(prefill_kernel_lds<D, 1, kFused>, dim3(items), dim3(LdsShape<1, kFused>::kThreads), s, args);
+    case 2: return launch_struct(prefill_kernel_lds<D, 2, kFused>, dim3(items), dim3(LdsShape<2, kFused>::kThreads), s, args);
+    case 4: return launch_struct(prefill_kernel_lds<D, 4, kFused>, dim3(items), dim3(LdsShape<4, kFused>::kThreads), s, args);
+    default: return launch_struct(prefill_kernel_lds<D, 8, kFused>, dim3(items), dim3(LdsShape<8, kFused>::kThreads), s, args);
   }
 }
 
@@ -624,11 +818,26 @@ int prefill_rows_per_tile(int group) {
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int group, int batch,
                           hipStream_t s) {
   if (dtype == 1) {
-    if (head_dim == 128) return launch_prefill_lds<128>(a, group, batch, s);
-    return launch_prefill_lds<64>(a, group, batch, s);
+    if (head_dim == 128) return launch_prefill_lds<128, false>(a, group, batch, s);
+    return launch_prefill_lds<64, false>(a, group, batch, s);
   }
   if (head_dim == 128) return launch_prefill_d<float, 128>(a, group, batch, s);
   return launch_prefill_d<float, 64>(a, group, batch, s);
+}
+
+int prefill_fused_rows_per_tile(int group) {
+  switch (group) {
+    case 1: return FusedShape<1>::kRows;
+    case 2: return FusedShape<2>::kRows;
+    case 4: return FusedShape<4>::kRows;
+    default: return FusedShape<8>::kRows;
+  }
+}
+
+hipError_t launch_prefill_fused(const PrefillFusedArgs& a, int head_dim, int group, int batch,
+                                hipStream_t s) {
+  if (head_dim == 128) return launch_prefill_lds<128, true>(a, group, batch, s);
+  return launch_prefill_lds<64, true>(a, group, batch, s);
 }
 
 }  // namespace skv

@@ -65,6 +65,11 @@ _lib.speechkv_prefill_attn.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_Pa
                                        ctypes.POINTER(_Spans), _i32, _i32, _i32, _i32, _f32, _vp,
                                        _vp, _vp]
 _lib.speechkv_prefill_attn.restype = ctypes.c_int
+_lib.speechkv_pool_prefill_attn.argtypes = [_vp, _i32, _i32, _i32, _vp, _vp, _i64, _i64, _i64, _i32,
+                                            ctypes.POINTER(_Spans), _i32, _vp, _i32, _i32,
+                                            ctypes.POINTER(_PagedKV), _vp, _i32, ctypes.c_float,
+                                            _vp, _vp, _vp]
+_lib.speechkv_pool_prefill_attn.restype = ctypes.c_int
 _lib.speechkv_prefill_attn_bwd.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_PagedKV),
                                            ctypes.POINTER(_Spans), _i32, _i32, _i32, _i32, _f32,
                                            _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _sz, _vp]
@@ -232,6 +237,36 @@ def speechkv_prefill_attn(q: torch.Tensor, cache: PagedKV, spans: Spans, w: int,
                                     w, layer, l0, mask_mode, scale, out.data_ptr(), _ptr(lse),
                                     _stream(stream))
     _check(st, "speechkv_prefill_attn")
+
+
+def speechkv_pool_prefill_attn(q: torch.Tensor, k_raw: torch.Tensor, v_raw: torch.Tensor,
+                               spans: Spans, w: int, gate_u: Optional[torch.Tensor], layer: int,
+                               l0: int, cache: PagedKV, out: torch.Tensor,
+                               cache_len_out: Optional[torch.Tensor] = None,
+                               mask_mode: int = MASK_WINDOW_END, scale: Optional[float] = None,
+                               lse: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Pooling and prefill attention in one launch.  q, out: [B, q_len, Hq, D]
+    contiguous; k_raw, v_raw: [B, S_raw, Hkv, D] views with a contiguous last
+    axis; lse: [B, Hq, q_len] fp32 or None."""
+    for x in (q, out) + ((lse,) if lse is not None else ()):
+        if not x.is_contiguous():
+            raise ValueError("prefill tensors must be contiguous")
+    if k_raw.shape != v_raw.shape or k_raw.stride() != v_raw.stride():
+        raise ValueError("k_raw and v_raw must have one shape and one stride")
+    if k_raw.dim() != 4 or k_raw.stride(3) != 1:
+        raise ValueError("raw K/V must be [B, S, Hkv, D] with a contiguous last axis")
+    B, q_len, Hq, D = q.shape
+    if scale is None:
+        scale = D ** -0.5
+    sb, ss, sh, _ = k_raw.stride()
+    c = cache._c()
+    s = spans._c()
+    st = _lib.speechkv_pool_prefill_attn(q.data_ptr(), B, Hq, q_len, k_raw.data_ptr(),
+                                         v_raw.data_ptr(), sb, ss, sh, k_raw.shape[1],
+                                         ctypes.byref(s), w, _ptr(gate_u), layer, l0,
+                                         ctypes.byref(c), _ptr(cache_len_out), mask_mode, scale,
+                                         out.data_ptr(), _ptr(lse), _stream(stream))
+    _check(st, "speechkv_pool_prefill_attn")
 
 
 def speechkv_prefill_attn_bwd_workspace_bytes(batch: int, num_q_heads: int, q_len: int) -> int:

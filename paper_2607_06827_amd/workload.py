@@ -18,8 +18,9 @@ from . import inputs
 from .speechkv import (PagedKV, Spans, speechkv_compressed_len, speechkv_decode_attn,
                        speechkv_decode_num_splits, speechkv_decode_workspace_bytes,
                        speechkv_pool_hidden, speechkv_pool_kv, speechkv_pool_kv_bwd,
-                       speechkv_pool_kv_bwd_workspace_bytes, speechkv_prefill_attn,
-                       speechkv_prefill_attn_bwd, speechkv_prefill_attn_bwd_workspace_bytes)
+                       speechkv_pool_kv_bwd_workspace_bytes, speechkv_pool_prefill_attn,
+                       speechkv_prefill_attn, speechkv_prefill_attn_bwd,
+                       speechkv_prefill_attn_bwd_workspace_bytes)
 
 
 def visible_pairs(P: int, T: int, N: int, w: int) -> int:
@@ -132,6 +133,19 @@ class Job:
             if self.with_prefill:
                 speechkv_prefill_attn(self.q_prefill[i], self.caches[i], self.spans, wl.window(l), l,
                                       self.l0, self.prefill_out, scale=self.scale, stream=stream)
+
+    def run_prefill_fused(self, stream=None, layers: Optional[Sequence[int]] = None):
+        """The prefill of every layer as one launch each: the pooling runs on
+        the fly inside the attention (speechkv_pool_prefill_attn), writing the
+        same caches, lengths and outputs as run_prefill."""
+        wl = self.wl
+        for i, l in enumerate(self.layers):
+            if layers is not None and l not in layers:
+                continue
+            speechkv_pool_prefill_attn(self.q_prefill[i], self.k_raw[i], self.v_raw[i], self.spans,
+                                       wl.window(l), self.gate[i], l, self.l0, self.caches[i],
+                                       self.prefill_out, cache_len_out=self.cache_len_out[i],
+                                       scale=self.scale, stream=stream)
 
     def run_pool(self, stream=None):
         """Pooling of every layer (writes the caches)."""

@@ -26,7 +26,8 @@ def declared_functions():
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
-                          "speechkv_pool_hidden", "speechkv_prefill_attn_bwd",
+                          "speechkv_pool_hidden", "speechkv_pool_prefill_attn",
+                          "speechkv_prefill_attn_bwd",
                           "speechkv_prefill_attn_bwd_workspace_bytes", "speechkv_pool_kv_bwd",
                           "speechkv_pool_kv_bwd_workspace_bytes",
                           "speechkv_compressed_len", "speechkv_decode_num_splits",
@@ -122,6 +123,23 @@ def prefill(c=None, s=None, **kw):
 
 E_ARG, E_UNS, E_WS, E_ALIAS = skv.ERR_INVALID_ARG, skv.ERR_UNSUPPORTED, skv.ERR_WORKSPACE, skv.ERR_ALIAS
 
+FQ, FOUT = FAKE + (23 << 24), FAKE + (24 << 24)
+
+
+def fused(c=None, s=None, **kw):
+    """speechkv_pool_prefill_attn with the pooling arguments of pool() and
+    the attention arguments of prefill()."""
+    a = dict(q=FQ, batch=2, hq=4, q_len=60, k=RAW, v=RAW + (1 << 22), sb=60 * 2 * 64, ss=2 * 64,
+             sh=64, raw_len=60, w=4, gate=None, layer=1, l0=0, clen=None, mode=0, scale=0.125,
+             out=FOUT, lse=None)
+    a.update(kw)
+    c = c or cache()
+    s = s or spans()
+    return lib.speechkv_pool_prefill_attn(a["q"], a["batch"], a["hq"], a["q_len"], a["k"], a["v"],
+                                          a["sb"], a["ss"], a["sh"], a["raw_len"], ctypes.byref(s),
+                                          a["w"], a["gate"], a["layer"], a["l0"], ctypes.byref(c),
+                                          a["clen"], a["mode"], a["scale"], a["out"], a["lse"], None)
+
 
 @pytest.mark.parametrize("kw,code", [
     (dict(k=None), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=0), E_ARG), (dict(w=0), E_ARG),
@@ -170,6 +188,7 @@ def test_cache_description_rejected_by_every_call(ckw, code):
     assert pool(c=cache(**ckw)) == code
     assert decode(c=cache(**ckw)) == code
     assert prefill(c=cache(**ckw)) == code
+    assert fused(c=cache(**ckw)) == code
 
 
 @pytest.mark.parametrize("skw", [dict(prefix_len=None), dict(max_total_len=-1),
@@ -177,6 +196,7 @@ def test_cache_description_rejected_by_every_call(ckw, code):
 def test_bad_spans(skw):
     assert pool(s=spans(**skw)) == E_ARG
     assert prefill(s=spans(**skw)) == E_ARG
+    assert fused(s=spans(**skw)) == E_ARG
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -201,6 +221,25 @@ def test_prefill_rejects(kw, code):
     assert prefill(**kw) == code
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(k=None), E_ARG), (dict(v=None), E_ARG),
+    (dict(batch=0), E_ARG), (dict(q_len=59), E_ARG), (dict(raw_len=59), E_ARG), (dict(w=0), E_ARG),
+    (dict(layer=-1), E_ARG), (dict(l0=-1), E_ARG), (dict(mode=2), E_ARG), (dict(scale=0.0), E_ARG),
+    (dict(scale=float("nan")), E_ARG), (dict(scale=float("inf")), E_ARG), (dict(hq=5), E_ARG),
+    (dict(hq=6), E_UNS), (dict(sb=-8), E_ARG), (dict(ss=3), E_ARG), (dict(k=RAW + 4), E_ARG),
+    (dict(gate=FAKE + 4), E_ARG), (dict(lse=FAKE + 2), E_ARG), (dict(q=FQ + 8), E_ARG),
+    (dict(k=FAKE), E_ALIAS), (dict(v=FAKE + (1 << 24) + 256), E_ALIAS), (dict(out=FQ + 4096), E_ALIAS),
+    (dict(out=RAW), E_ALIAS), (dict(lse=FOUT + 64), E_ALIAS), (dict(lse=FAKE + 1024), E_ALIAS),
+    (dict(gate=FAKE + 512), E_ALIAS), (dict(q=FAKE + (1 << 24)), E_ALIAS),
+])
+def test_fused_rejects(kw, code):
+    assert fused(**kw) == code
+
+
+def test_fused_is_bf16_only():
+    assert fused(c=cache(dtype=skv.DTYPE_F32)) == E_UNS
+
+
 def test_window_and_row_count_bounds():
     """w beyond SPEECHKV_MAX_WINDOW and row counts whose window count could
     overflow 32-bit arithmetic are rejected by every pooling and attention call."""
@@ -208,10 +247,12 @@ def test_window_and_row_count_bounds():
     assert pool(w=big_w) == E_ARG
     assert pool_hidden(w=big_w) == E_ARG
     assert prefill(w=big_w) == E_ARG
+    assert fused(w=big_w) == E_ARG
     too_many = 2**31 - 1 - skv.MAX_WINDOW + 1
     assert pool(raw_len=too_many) == E_ARG
     assert pool_hidden(raw_len=too_many) == E_ARG
     assert prefill(q_len=too_many) == E_ARG
+    assert fused(q_len=too_many, raw_len=too_many) == E_ARG
 
 
 def test_binding_constants_match_header():
