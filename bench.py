@@ -213,6 +213,23 @@ def measure_fused(base, steps, copies=3):
             "stack_prefill_fused_ms": ms_fused, "stack_prefill_split_ms": ms_split}
 
 
+def measure_segments(steps, copies=3):
+    """Pooling + prefill attention of a multi-turn batch (three speech turns
+    per sequence, segment tables) against a batch of the same rows and
+    compressed length laid out as one run per sequence."""
+    from paper_2607_06827_amd.workload import MULTI_TURN, SegmentJob
+
+    res = {"segments": [list(x) for x in MULTI_TURN], "batch": 16}
+    for name, one in (("segments_us", False), ("one_run_us", True)):
+        jobs = [SegmentJob(MULTI_TURN, seed=6 + i, one_run=one) for i in range(copies)]
+        g = capture(lambda: [j.run() for j in jobs])
+        res[name] = time_graph(g, max(10, steps)) / copies * 1e3
+        del g, jobs
+    log(f"multi-turn pool+prefill (b=16, 1261 rows, 418 keys): {res['segments_us']:.1f} us with "
+        f"segment tables, {res['one_run_us']:.1f} us as one run")
+    return res
+
+
 def measure_hs_pool(wl, steps, copies=4):
     """HS Compression's hidden-state pooling on the same batch and spans.
 
@@ -394,6 +411,8 @@ def main():
 
     fused = measure_fused(job, args.steps)
     torch.cuda.empty_cache()
+    segments = measure_segments(args.steps)
+    torch.cuda.empty_cache()
     adaptive = measure_adaptive(job, args.steps, args.warmup, args.num_splits)
     adaptive["speedup_over_uniform_w"] = adaptive["tokens_per_s"] / pooled["tokens_per_s"]
     torch.cuda.empty_cache()
@@ -435,6 +454,7 @@ def main():
         "pool": pooled["pool"],
         "prefill_attn": pooled["prefill_attn"],
         "fused_prefill": fused,
+        "multi_turn": segments,
         "adaptive_w": adaptive,
         "hs_pool": hs_pool,
         "train_bwd": train_bwd,

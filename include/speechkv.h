@@ -78,6 +78,10 @@ extern "C" {
  * with these bounds no window count ceil(T / w) overflows 32-bit arithmetic. */
 #define SPEECHKV_MAX_WINDOW 65536
 
+/* Largest number of segments one sequence may have (speechkv_segments):
+ * every kernel that reads a segment table scans a sequence's segments. */
+#define SPEECHKV_MAX_SEGMENTS 1024
+
 /* Mask modes for speech queries against pooled windows (Sec. III-B: each
  * query attends only to positions that precede it; the figure that draws the
  * mask is not part of the text, so two readings are offered).
@@ -133,6 +137,35 @@ typedef struct speechkv_spans {
 } speechkv_spans;
 
 /*
+ * Sequences with several speech runs (a multi-turn input: the LLM input
+ * interleaves speech and text, Sec. III-A).  Sequence b is the concatenation
+ * of its segments i in [seg_start[b], seg_start[b+1]), segment i being
+ *     [ text_len[i] text rows | speech_len[i] speech frames ].
+ * Each speech run is pooled on its own (Eq. 4): windows of w frames start at
+ * the run's first frame, and the run's last window keeps the frames it has.
+ * One run [P | T | N] is the table {(P, T), (N, 0)}.
+ *
+ * seg_start      device int32 [batch + 1], non-decreasing, seg_start[0] >= 0,
+ *                seg_start[batch] <= num_segments.
+ * text_len, speech_len  device int32 [num_segments], each >= 0.
+ * num_segments   host: entries in text_len and speech_len (>= 0).
+ * max_segments   host: an upper bound on seg_start[b+1] - seg_start[b],
+ *                0 .. SPEECHKV_MAX_SEGMENTS.
+ * max_total_len  host: an upper bound on every sequence's row count.
+ * Caller obligation: the bounds hold.  The kernels read at most
+ * max_segments segments per sequence and at most max_total_len rows, clamp
+ * every table value into range, and never read past num_segments.
+ */
+typedef struct speechkv_segments {
+  const int32_t* seg_start;
+  const int32_t* text_len;
+  const int32_t* speech_len;
+  int32_t num_segments;
+  int32_t max_segments;
+  int32_t max_total_len;
+} speechkv_segments;
+
+/*
  * speechkv_pool_kv - learned window pooling of the speech keys and values,
  * written straight into the paged cache (Sec. III-B, Eq. 4; Sec. III-C).
  *
@@ -175,6 +208,23 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
                      const float* gate_u, int32_t layer, int32_t l0,
                      const speechkv_paged_kv* cache, int32_t* cache_len_out,
                      void* stream);
+
+/*
+ * speechkv_pool_kv_segments - speechkv_pool_kv for sequences with several
+ * speech runs: compressed slots follow the segments in order, each text row
+ * copied bitwise and each window of each run pooled with Eq. 4 as above.
+ * cache_len_out receives the compressed length, the sum over the sequence's
+ * segments of text_len + ceil(speech_len / w_eff).
+ * Arguments as for speechkv_pool_kv, with segs (host pointer) in place of
+ * spans; segs->max_total_len must not exceed raw_len.
+ * Errors: INVALID_ARG, UNSUPPORTED, ALIAS, HIP.
+ */
+int speechkv_pool_kv_segments(const void* k_raw, const void* v_raw, int64_t stride_b,
+                              int64_t stride_s, int64_t stride_h, int32_t batch,
+                              int32_t raw_len, const speechkv_segments* segs, int32_t w,
+                              const float* gate_u, int32_t layer, int32_t l0,
+                              const speechkv_paged_kv* cache, int32_t* cache_len_out,
+                              void* stream);
 
 /*
  * speechkv_pool_hidden - learned window pooling of whole hidden states: the HS
@@ -292,6 +342,23 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
                           const speechkv_spans* spans, int32_t w, int32_t layer,
                           int32_t l0, int32_t mask_mode, float scale, void* out,
                           float* lse, void* stream);
+
+/*
+ * speechkv_prefill_attn_segments - speechkv_prefill_attn for sequences with
+ * several speech runs (the cache written by speechkv_pool_kv_segments).  A
+ * text key is visible from its own row, a pooled window of any run from its
+ * last frame (WINDOW_END) or its first frame (WINDOW_START); the position a
+ * key becomes visible at still grows with the key, so each row sees a prefix
+ * of the cache.
+ * Arguments as for speechkv_prefill_attn, with segs (host pointer) in place
+ * of spans; segs->max_total_len must not exceed q_len.
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ */
+int speechkv_prefill_attn_segments(const void* q, int32_t batch, int32_t num_q_heads,
+                                   int32_t q_len, const speechkv_paged_kv* cache,
+                                   const speechkv_segments* segs, int32_t w, int32_t layer,
+                                   int32_t l0, int32_t mask_mode, float scale, void* out,
+                                   float* lse, void* stream);
 
 /*
  * speechkv_pool_prefill_attn - speechkv_pool_kv followed by
@@ -426,6 +493,13 @@ size_t speechkv_pool_kv_bwd_workspace_bytes(int32_t batch, int32_t max_total_len
 int64_t speechkv_compressed_len(int32_t prefix_len, int32_t speech_len,
                                 int32_t suffix_len, int32_t w, int32_t layer,
                                 int32_t l0);
+
+/* Compressed length of one sequence given as segments (host arrays of
+ * num_segments entries), or -1 for a negative length or count, w < 1, a
+ * negative layer or l0. */
+int64_t speechkv_compressed_len_segments(const int32_t* text_len, const int32_t* speech_len,
+                                         int32_t num_segments, int32_t w, int32_t layer,
+                                         int32_t l0);
 
 /* Split count chosen by speechkv_decode_attn when num_splits = 0, from the
  * number of (sequence, KV head) pairs and the longest cache.  Host only;

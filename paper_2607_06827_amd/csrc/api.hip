@@ -47,6 +47,37 @@ int check_spans(const speechkv_spans* s) {
   return SPEECHKV_OK;
 }
 
+int check_segments(const speechkv_segments* g) {
+  if (!g || !g->seg_start || !g->text_len || !g->speech_len) return SPEECHKV_ERR_INVALID_ARG;
+  if (g->num_segments < 0 || g->max_segments < 0 || g->max_segments > SPEECHKV_MAX_SEGMENTS ||
+      g->max_total_len < 0)
+    return SPEECHKV_ERR_INVALID_ARG;
+  return SPEECHKV_OK;
+}
+
+skv::SegmentTable table_of(const speechkv_segments* g) {
+  skv::SegmentTable t;
+  t.seg_start = g->seg_start;
+  t.text_len = g->text_len;
+  t.speech_len = g->speech_len;
+  t.num_segments = g->num_segments;
+  t.max_segs = g->max_segments;
+  t.max_rows = g->max_total_len;
+  return t;
+}
+
+// The one-run span arguments of a segment-table call: the kernels read the
+// table instead, and these pointers stay unread.
+speechkv_spans spans_of(const speechkv_segments* g) {
+  speechkv_spans s;
+  s.prefix_len = g->seg_start;
+  s.speech_len = g->seg_start;
+  s.suffix_len = g->seg_start;
+  s.max_speech_len = 0;
+  s.max_total_len = g->max_total_len;
+  return s;
+}
+
 skv::PagedView view_of(const speechkv_paged_kv* c) {
   skv::PagedView v;
   v.num_pages = c->num_pages;
@@ -82,6 +113,21 @@ int64_t speechkv_compressed_len(int32_t prefix_len, int32_t speech_len, int32_t 
   if (prefix_len < 0 || speech_len < 0 || suffix_len < 0 || w < 1 || layer < 0 || l0 < 0) return -1;
   const int64_t weff = layer >= l0 ? w : 1;
   return (int64_t)prefix_len + (speech_len + weff - 1) / weff + suffix_len;
+}
+
+int64_t speechkv_compressed_len_segments(const int32_t* text_len, const int32_t* speech_len,
+                                         int32_t num_segments, int32_t w, int32_t layer,
+                                         int32_t l0) {
+  if (num_segments < 0 || (num_segments > 0 && (!text_len || !speech_len)) || w < 1 || layer < 0 ||
+      l0 < 0)
+    return -1;
+  const int64_t weff = layer >= l0 ? w : 1;
+  int64_t n = 0;
+  for (int32_t i = 0; i < num_segments; ++i) {
+    if (text_len[i] < 0 || speech_len[i] < 0) return -1;
+    n += (int64_t)text_len[i] + (speech_len[i] + weff - 1) / weff;
+  }
+  return n;
 }
 
 int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t max_cache_len) {
@@ -127,10 +173,12 @@ const char* speechkv_status_string(int status) {
 
 const char* speechkv_version(void) { return "0.1.0"; }
 
-int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
-                     int64_t stride_h, int32_t batch, int32_t raw_len, const speechkv_spans* spans,
-                     int32_t w, const float* gate_u, int32_t layer, int32_t l0,
-                     const speechkv_paged_kv* cache, int32_t* cache_len_out, void* stream) {
+// speechkv_pool_kv and speechkv_pool_kv_segments (segs set: several runs)
+static int pool_kv_impl(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
+                        int64_t stride_h, int32_t batch, int32_t raw_len, const speechkv_spans* spans,
+                        const skv::SegmentTable* segs, int32_t w, const float* gate_u, int32_t layer,
+                        int32_t l0, const speechkv_paged_kv* cache, int32_t* cache_len_out,
+                        void* stream) {
   if (!k_raw || !v_raw) return SPEECHKV_ERR_INVALID_ARG;
   int st = check_cache(cache);
   if (st) return st;
@@ -174,7 +222,29 @@ int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b, int
   a.pv = view_of(cache);
   a.cache_len_out = cache_len_out;
   a.max_out = spans->max_total_len;
+  if (segs) a.segs = *segs;
   return status_of(skv::launch_pool(a, cache->dtype, D, batch, static_cast<hipStream_t>(stream)));
+}
+
+int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
+                     int64_t stride_h, int32_t batch, int32_t raw_len, const speechkv_spans* spans,
+                     int32_t w, const float* gate_u, int32_t layer, int32_t l0,
+                     const speechkv_paged_kv* cache, int32_t* cache_len_out, void* stream) {
+  return pool_kv_impl(k_raw, v_raw, stride_b, stride_s, stride_h, batch, raw_len, spans, nullptr, w,
+                      gate_u, layer, l0, cache, cache_len_out, stream);
+}
+
+int speechkv_pool_kv_segments(const void* k_raw, const void* v_raw, int64_t stride_b,
+                              int64_t stride_s, int64_t stride_h, int32_t batch, int32_t raw_len,
+                              const speechkv_segments* segs, int32_t w, const float* gate_u,
+                              int32_t layer, int32_t l0, const speechkv_paged_kv* cache,
+                              int32_t* cache_len_out, void* stream) {
+  const int st = check_segments(segs);
+  if (st) return st;
+  const speechkv_spans sp = spans_of(segs);
+  const skv::SegmentTable t = table_of(segs);
+  return pool_kv_impl(k_raw, v_raw, stride_b, stride_s, stride_h, batch, raw_len, &sp, &t, w,
+                      gate_u, layer, l0, cache, cache_len_out, stream);
 }
 
 int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s, int32_t batch,
@@ -274,10 +344,11 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
   return status_of(e);
 }
 
-int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
-                          const speechkv_paged_kv* cache, const speechkv_spans* spans, int32_t w,
-                          int32_t layer, int32_t l0, int32_t mask_mode, float scale, void* out,
-                          float* lse, void* stream) {
+// speechkv_prefill_attn and speechkv_prefill_attn_segments (segs set)
+static int prefill_attn_impl(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                             const speechkv_paged_kv* cache, const speechkv_spans* spans,
+                             const skv::SegmentTable* segs, int32_t w, int32_t layer, int32_t l0,
+                             int32_t mask_mode, float scale, void* out, float* lse, void* stream) {
   if (!q || !out) return SPEECHKV_ERR_INVALID_ARG;
   int st = check_cache(cache);
   if (st) return st;
@@ -315,8 +386,30 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int
   a.num_tiles = (int)tiles;
   a.num_q_heads = num_q_heads;
   a.scale_log2 = scale * 1.4426950408889634f;
+  if (segs) a.segs = *segs;
   return status_of(skv::launch_prefill(a, cache->dtype, cache->head_dim, group, batch,
                                        static_cast<hipStream_t>(stream)));
+}
+
+int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                          const speechkv_paged_kv* cache, const speechkv_spans* spans, int32_t w,
+                          int32_t layer, int32_t l0, int32_t mask_mode, float scale, void* out,
+                          float* lse, void* stream) {
+  return prefill_attn_impl(q, batch, num_q_heads, q_len, cache, spans, nullptr, w, layer, l0,
+                           mask_mode, scale, out, lse, stream);
+}
+
+int speechkv_prefill_attn_segments(const void* q, int32_t batch, int32_t num_q_heads,
+                                   int32_t q_len, const speechkv_paged_kv* cache,
+                                   const speechkv_segments* segs, int32_t w, int32_t layer,
+                                   int32_t l0, int32_t mask_mode, float scale, void* out,
+                                   float* lse, void* stream) {
+  const int st = check_segments(segs);
+  if (st) return st;
+  const speechkv_spans sp = spans_of(segs);
+  const skv::SegmentTable t = table_of(segs);
+  return prefill_attn_impl(q, batch, num_q_heads, q_len, cache, &sp, &t, w, layer, l0, mask_mode,
+                           scale, out, lse, stream);
 }
 
 int speechkv_pool_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,

@@ -6,6 +6,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "spans.hpp"
 
 namespace skv {
 
@@ -91,17 +92,6 @@ struct Mfma<float> {
     *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
   }
 };
-
-// Number of compressed keys visible from full-resolution row p.
-__device__ __forceinline__ int visible_keys(int p, int P, int T, int nW, int w, int mode) {
-  if (p < P) return p + 1;
-  const int t = p - P;
-  if (t < T) {
-    if (mode == 1) return P + t / w + 1;        // window visible from its first frame
-    return (t == T - 1) ? P + nW : P + (t + 1) / w;  // ... from its last frame
-  }
-  return P + nW + (t - T) + 1;
-}
 
 template <int G>
 struct PrefillShape {

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "common.hpp"
+#include "spans.hpp"
 
 namespace skv {
 
@@ -25,6 +26,7 @@ struct PoolArgs {
   PagedView pv;
   int32_t* cache_len_out;  // may be null
   int max_out;             // bound on the compressed length (grid size)
+  SegmentTable segs;       // several speech runs per sequence when segs.seg_start is set
 };
 
 // Window pooling of whole hidden states (HS Compression, Sec. IV-A method
@@ -81,6 +83,7 @@ struct PrefillArgs {
   int num_tiles;  // query tiles per (sequence, KV head)
   int num_q_heads;
   float scale_log2;
+  SegmentTable segs;  // several speech runs per sequence when segs.seg_start is set
 };
 
 // dtype: 0 = fp32, 1 = bf16.  Each launcher returns the launch status.

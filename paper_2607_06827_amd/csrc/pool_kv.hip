@@ -24,7 +24,7 @@ namespace skv {
 
 namespace {
 
-template <typename T, int D, bool kGate>
+template <typename T, int D, bool kGate, bool kRuns>
 __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   constexpr int kLanes = D / 8;          // lanes per unit
   constexpr int kUnits = 256 / kLanes;   // units per block
@@ -37,17 +37,13 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   const int g = (int)(unit % heads);
   const int64_t c64 = unit / heads;
 
-  const int P = max(a.prefix_len[b], 0);
-  const int S = max(a.speech_len[b], 0);  // speech frames
-  const int N = max(a.suffix_len[b], 0);
-  const int w = a.w_eff;
-  const int nW = (S + w - 1) / w;
-  const int len = P + nW + N;
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int len = sp.clen();
   if (blockIdx.x == 0 && tid == 0 && a.cache_len_out) a.cache_len_out[b] = len;
   if (c64 >= len || c64 >= a.max_out) return;
   const int c = (int)c64;
 
-  const SlotSource sl(c, P, S, nW, w);
+  const SlotSource sl = sp.slot(c);
   const int src = sl.first, frames = sl.frames;
   // page of slot c: the entry is loaded now and checked only before the stores
   const int idx = c >> a.pv.page_shift;
@@ -105,6 +101,17 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   }
 }
 
+template <typename T, int D, bool kRuns>
+hipError_t launch_pool_t(const PoolArgs& a, dim3 grid, hipStream_t s) {
+  return a.gate ? launch_struct(pool_kv_kernel<T, D, true, kRuns>, grid, dim3(256), s, a)
+                : launch_struct(pool_kv_kernel<T, D, false, kRuns>, grid, dim3(256), s, a);
+}
+
+template <typename T, int D>
+hipError_t launch_pool_d(const PoolArgs& a, dim3 grid, hipStream_t s) {
+  return a.segs.seg_start ? launch_pool_t<T, D, true>(a, grid, s) : launch_pool_t<T, D, false>(a, grid, s);
+}
+
 }  // namespace
 
 hipError_t launch_pool(const PoolArgs& a, int dtype, int head_dim, int batch, hipStream_t s) {
@@ -113,19 +120,9 @@ hipError_t launch_pool(const PoolArgs& a, int dtype, int head_dim, int batch, hi
   // at least one block per sequence, which also writes cache_len_out
   const int64_t blocks = (units + units_per_block - 1) / units_per_block;
   const dim3 grid((unsigned)(blocks > 0 ? blocks : 1), batch);
-  const dim3 block(256);
-  if (dtype == 1) {
-    if (head_dim == 128)
-      return a.gate ? launch_struct(pool_kv_kernel<bf16_bits, 128, true>, grid, block, s, a)
-                    : launch_struct(pool_kv_kernel<bf16_bits, 128, false>, grid, block, s, a);
-    return a.gate ? launch_struct(pool_kv_kernel<bf16_bits, 64, true>, grid, block, s, a)
-                  : launch_struct(pool_kv_kernel<bf16_bits, 64, false>, grid, block, s, a);
-  }
-  if (head_dim == 128)
-    return a.gate ? launch_struct(pool_kv_kernel<float, 128, true>, grid, block, s, a)
-                  : launch_struct(pool_kv_kernel<float, 128, false>, grid, block, s, a);
-  return a.gate ? launch_struct(pool_kv_kernel<float, 64, true>, grid, block, s, a)
-                : launch_struct(pool_kv_kernel<float, 64, false>, grid, block, s, a);
+  if (dtype == 1)
+    return head_dim == 128 ? launch_pool_d<bf16_bits, 128>(a, grid, s) : launch_pool_d<bf16_bits, 64>(a, grid, s);
+  return head_dim == 128 ? launch_pool_d<float, 128>(a, grid, s) : launch_pool_d<float, 64>(a, grid, s);
 }
 
 }  // namespace skv

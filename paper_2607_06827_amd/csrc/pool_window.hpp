@@ -9,21 +9,9 @@
 #pragma once
 
 #include "common.hpp"
+#include "spans.hpp"
 
 namespace skv {
-
-// Source rows of compressed slot c of a sequence with P prefix rows, T speech
-// frames pooled in windows of w (nW of them) and the suffix after them:
-// `first` is the first raw row, `frames` how many rows it spans (1 for a text
-// row or a one-frame window, whose weight is exactly 1).
-struct SlotSource {
-  int first, frames;
-  __device__ __forceinline__ SlotSource(int c, int P, int T, int nW, int w) {
-    const bool text_before = c < P, text_after = c >= P + nW;
-    first = text_before ? c : text_after ? P + T + (c - P - nW) : P + (c - P) * w;
-    frames = (text_before || text_after) ? 1 : min(w, P + T - first);
-  }
-};
 
 template <typename T, int kLanes>
 struct WindowPool {

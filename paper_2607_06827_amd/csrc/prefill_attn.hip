@@ -52,7 +52,7 @@ namespace {
 // makes the choice of reference exact.
 constexpr float kSlack = 8.f;
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool kRuns>
 __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(PrefillArgs a) {
   typedef Mfma<T> M;
   typedef typename M::Frag Frag;
@@ -86,16 +86,13 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const int g = (item / a.num_tiles) % heads;
   const int b = item / a.num_tiles / heads;
 
-  const int P = max(a.prefix_len[b], 0);
-  const int T_ = max(a.speech_len[b], 0);
-  const int N = max(a.suffix_len[b], 0);
   const int w = a.w_eff;
-  const int nW = (T_ + w - 1) / w;
-  const int rows = min(P + T_ + N, a.q_len);
-  const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
+  const auto sp = span_view<kRuns>(a, b, w);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
   if (p0 >= rows) return;
-  const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = g * G + wave % G;
@@ -103,9 +100,9 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
   const int p = wrow0 + col;
   const bool qvalid = p < rows;
-  const int nvis = qvalid ? min(visible_keys(p, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int nvis = qvalid ? min(sp.visible(p, a.mask_mode), clen) : 0;
   // keys every valid row of the wave sees (n_vis grows with the row)
-  const int nvis_lo = wrow0 < rows ? min(visible_keys(wrow0, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
   const int hq = a.num_q_heads;
   const int slot_mask = (1 << a.pv.page_shift) - 1;
 
@@ -380,7 +377,7 @@ __device__ __host__ __forceinline__ const PrefillArgs& attn_args(const PrefillFu
 // The block holding a sequence's last query rows (which see every key) also
 // stores each pooled row into the paged cache, and pools the rows no query
 // sees, so the cache ends up as the pooling kernel would have written it.
-template <int D, int G, bool kFused>
+template <int D, int G, bool kFused, bool kRuns>
 __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G, kFused>())) void prefill_kernel_lds(typename LdsArgs<kFused>::type args) {
   const PrefillArgs& a = attn_args(args);
   typedef bf16_bits T;
@@ -417,19 +414,16 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   const int g = (item / a.num_tiles) % heads;
   const int b = item / a.num_tiles / heads;
 
-  const int P = max(a.prefix_len[b], 0);
-  const int T_ = max(a.speech_len[b], 0);
-  const int N = max(a.suffix_len[b], 0);
   const int w = a.w_eff;
-  const int nW = (T_ + w - 1) / w;
-  const int rows = min(P + T_ + N, a.q_len);
-  const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
+  const auto sp = span_view<kRuns>(a, b, w);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
   if constexpr (kFused) {
-    if (tile == 0 && g == 0 && threadIdx.x == 0 && args.cache_len_out) args.cache_len_out[b] = P + nW + N;
+    if (tile == 0 && g == 0 && threadIdx.x == 0 && args.cache_len_out) args.cache_len_out[b] = sp.clen();
   }
   if (p0 >= rows) return;
-  const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
   const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -438,9 +432,9 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
   const int p = wrow0 + col;
   const bool qvalid = p < rows;
-  const int nvis = qvalid ? min(visible_keys(p, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int nvis = qvalid ? min(sp.visible(p, a.mask_mode), clen) : 0;
   // keys every valid row of the wave sees (n_vis grows with the row)
-  const int nvis_lo = wrow0 < rows ? min(visible_keys(wrow0, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
   const int hq = a.num_q_heads;
   const int slot_mask = (1 << a.pv.page_shift) - 1;
   const int shift = a.pv.page_shift;
@@ -497,7 +491,7 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   auto pool_fetch = [&](int c0, int cmax) __attribute__((always_inline)) {
     if (!pool_wave) return;
     const int c = min(c0 + pslot, cmax);
-    const SlotSource sl(c, P, T_, nW, w);
+    const SlotSource sl = sp.slot(c);
     fsrc = sl.first;
     ffr = sl.frames;
     fent = writer ? table_row[min(c >> shift, a.pv.max_pages - 1)] : 0;
@@ -781,26 +775,26 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   }
 }
 
-template <typename T, int D>
+template <typename T, int D, bool kRuns>
 hipError_t launch_prefill_d(const PrefillArgs& a, int group, int batch, hipStream_t s) {
   const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
   switch (group) {
-    case 1: return launch_struct(prefill_kernel<T, D, 1>, dim3(items), dim3(PrefillShape<1>::kThreads), s, a);
-    case 2: return launch_struct(prefill_kernel<T, D, 2>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
-    case 4: return launch_struct(prefill_kernel<T, D, 4>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
-    default: return launch_struct(prefill_kernel<T, D, 8>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
+    case 1: return launch_struct(prefill_kernel<T, D, 1, kRuns>, dim3(items), dim3(PrefillShape<1>::kThreads), s, a);
+    case 2: return launch_struct(prefill_kernel<T, D, 2, kRuns>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
+    case 4: return launch_struct(prefill_kernel<T, D, 4, kRuns>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
+    default: return launch_struct(prefill_kernel<T, D, 8, kRuns>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
   }
 }
 
-template <int D, bool kFused>
+template <int D, bool kFused, bool kRuns>
 hipError_t launch_prefill_lds(const typename LdsArgs<kFused>::type& args, int group, int batch, hipStream_t s) {
   const PrefillArgs& a = attn_args(args);
   const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
   switch (group) {
-    case 1: return launch_struct(prefill_kernel_lds<D, 1, kFused>, dim3(items), dim3(LdsShape<1, kFused>::kThreads), s, args);
-    case 2: return launch_struct(prefill_kernel_lds<D, 2, kFused>, dim3(items), dim3(LdsShape<2, kFused>::kThreads), s, args);
-    case 4: return launch_struct(prefill_kernel_lds<D, 4, kFused>, dim3(items), dim3(LdsShape<4, kFused>::kThreads), s, args);
-    default: return launch_struct(prefill_kernel_lds<D, 8, kFused>, dim3(items), dim3(LdsShape<8, kFused>::kThreads), s, args);
+    case 1: return launch_struct(prefill_kernel_lds<D, 1, kFused, kRuns>, dim3(items), dim3(LdsShape<1, kFused>::kThreads), s, args);
+    case 2: return launch_struct(prefill_kernel_lds<D, 2, kFused, kRuns>, dim3(items), dim3(LdsShape<2, kFused>::kThreads), s, args);
+    case 4: return launch_struct(prefill_kernel_lds<D, 4, kFused, kRuns>, dim3(items), dim3(LdsShape<4, kFused>::kThreads), s, args);
+    default: return launch_struct(prefill_kernel_lds<D, 8, kFused, kRuns>, dim3(items), dim3(LdsShape<8, kFused>::kThreads), s, args);
   }
 }
 
@@ -817,12 +811,19 @@ int prefill_rows_per_tile(int group) {
 
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int group, int batch,
                           hipStream_t s) {
+  const bool runs = a.segs.seg_start != nullptr;
   if (dtype == 1) {
-    if (head_dim == 128) return launch_prefill_lds<128, false>(a, group, batch, s);
-    return launch_prefill_lds<64, false>(a, group, batch, s);
+    if (head_dim == 128)
+      return runs ? launch_prefill_lds<128, false, true>(a, group, batch, s)
+                  : launch_prefill_lds<128, false, false>(a, group, batch, s);
+    return runs ? launch_prefill_lds<64, false, true>(a, group, batch, s)
+                : launch_prefill_lds<64, false, false>(a, group, batch, s);
   }
-  if (head_dim == 128) return launch_prefill_d<float, 128>(a, group, batch, s);
-  return launch_prefill_d<float, 64>(a, group, batch, s);
+  if (head_dim == 128)
+    return runs ? launch_prefill_d<float, 128, true>(a, group, batch, s)
+                : launch_prefill_d<float, 128, false>(a, group, batch, s);
+  return runs ? launch_prefill_d<float, 64, true>(a, group, batch, s)
+              : launch_prefill_d<float, 64, false>(a, group, batch, s);
 }
 
 int prefill_fused_rows_per_tile(int group) {
@@ -836,8 +837,8 @@ int prefill_fused_rows_per_tile(int group) {
 
 hipError_t launch_prefill_fused(const PrefillFusedArgs& a, int head_dim, int group, int batch,
                                 hipStream_t s) {
-  if (head_dim == 128) return launch_prefill_lds<128, true>(a, group, batch, s);
-  return launch_prefill_lds<64, true>(a, group, batch, s);
+  if (head_dim == 128) return launch_prefill_lds<128, true, false>(a, group, batch, s);
+  return launch_prefill_lds<64, true, false>(a, group, batch, s);
 }
 
 }  // namespace skv

@@ -33,6 +33,7 @@ DTYPE_BF16 = 1
 MASK_WINDOW_END = 0
 MASK_WINDOW_START = 1
 MAX_WINDOW = 65536  # largest window size the pooling and attention calls take
+MAX_SEGMENTS = 1024  # most segments one sequence of a segment table may have
 
 LIBRARY_PATH = _LIB_PATH
 
@@ -51,10 +52,26 @@ class _Spans(ctypes.Structure):
                 ("max_total_len", ctypes.c_int32)]
 
 
+class _Segments(ctypes.Structure):
+    _fields_ = [("seg_start", ctypes.c_void_p), ("text_len", ctypes.c_void_p),
+                ("speech_len", ctypes.c_void_p), ("num_segments", ctypes.c_int32),
+                ("max_segments", ctypes.c_int32), ("max_total_len", ctypes.c_int32)]
+
+
 _vp, _i32, _i64, _f32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
 _lib.speechkv_pool_kv.argtypes = [_vp, _vp, _i64, _i64, _i64, _i32, _i32, ctypes.POINTER(_Spans),
                                   _i32, _vp, _i32, _i32, ctypes.POINTER(_PagedKV), _vp, _vp]
 _lib.speechkv_pool_kv.restype = ctypes.c_int
+_lib.speechkv_pool_kv_segments.argtypes = [_vp, _vp, _i64, _i64, _i64, _i32, _i32,
+                                           ctypes.POINTER(_Segments), _i32, _vp, _i32, _i32,
+                                           ctypes.POINTER(_PagedKV), _vp, _vp]
+_lib.speechkv_pool_kv_segments.restype = ctypes.c_int
+_lib.speechkv_prefill_attn_segments.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_PagedKV),
+                                                ctypes.POINTER(_Segments), _i32, _i32, _i32, _i32,
+                                                ctypes.c_float, _vp, _vp, _vp]
+_lib.speechkv_prefill_attn_segments.restype = ctypes.c_int
+_lib.speechkv_compressed_len_segments.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32]
+_lib.speechkv_compressed_len_segments.restype = _i64
 _lib.speechkv_pool_hidden.argtypes = [_vp, _i64, _i64, _i32, _i32, _i32, _i32, ctypes.POINTER(_Spans),
                                       _i32, _vp, _vp, _i64, _i64, _i32, _vp, _vp]
 _lib.speechkv_pool_hidden.restype = ctypes.c_int
@@ -141,6 +158,42 @@ class Spans:
                       self.suffix_len.data_ptr(), self.max_speech_len, self.max_total_len)
 
 
+@dataclasses.dataclass
+class Segments:
+    """Sequences with several speech runs: sequence b is its segments
+    [seg_start[b], seg_start[b+1]), segment i being text_len[i] text rows then
+    speech_len[i] speech frames (device int32 tensors), with host-side bounds
+    on the segments of one sequence and on its rows."""
+
+    seg_start: torch.Tensor
+    text_len: torch.Tensor
+    speech_len: torch.Tensor
+    max_segments: int
+    max_total_len: int
+
+    def _c(self) -> _Segments:
+        for x in (self.seg_start, self.text_len, self.speech_len):
+            if x.dtype != torch.int32 or not x.is_contiguous():
+                raise ValueError("segment tables must be contiguous int32 tensors")
+        if self.text_len.shape != self.speech_len.shape:
+            raise ValueError("text_len and speech_len must have one entry per segment")
+        return _Segments(self.seg_start.data_ptr(), self.text_len.data_ptr(),
+                         self.speech_len.data_ptr(), self.text_len.numel(), self.max_segments,
+                         self.max_total_len)
+
+    @staticmethod
+    def from_lists(segs, device="cuda") -> "Segments":
+        """Build the table from [[(text_len, speech_len), ...] per sequence]."""
+        start = [0]
+        for s in segs:
+            start.append(start[-1] + len(s))
+        flat = [x for s in segs for x in s]
+        i32 = lambda v: torch.tensor(v, dtype=torch.int32, device=device)
+        return Segments(i32(start), i32([t for t, _ in flat] or [0]),
+                        i32([s for _, s in flat] or [0]), max([len(s) for s in segs] or [0]),
+                        max([sum(t + s for t, s in x) for x in segs] or [0]))
+
+
 def _dtype_code(dt: torch.dtype) -> int:
     if dt == torch.bfloat16:
         return DTYPE_BF16
@@ -181,6 +234,52 @@ def speechkv_pool_kv(k_raw: torch.Tensor, v_raw: torch.Tensor, spans: Spans, w: 
                                k_raw.shape[1], ctypes.byref(s), w, _ptr(gate_u), layer, l0,
                                ctypes.byref(c), _ptr(cache_len_out), _stream(stream))
     _check(st, "speechkv_pool_kv")
+
+
+def speechkv_pool_kv_segments(k_raw: torch.Tensor, v_raw: torch.Tensor, segs: Segments, w: int,
+                              gate_u: Optional[torch.Tensor], layer: int, l0: int, cache: PagedKV,
+                              cache_len_out: Optional[torch.Tensor] = None, stream=None) -> None:
+    """k_raw, v_raw: [B, S_raw, Hkv, D] views with a contiguous last axis."""
+    if k_raw.shape != v_raw.shape or k_raw.stride() != v_raw.stride():
+        raise ValueError("k_raw and v_raw must have one shape and one stride")
+    if k_raw.dim() != 4 or k_raw.stride(3) != 1:
+        raise ValueError("raw K/V must be [B, S, Hkv, D] with a contiguous last axis")
+    sb, ss, sh, _ = k_raw.stride()
+    c = cache._c()
+    g = segs._c()
+    st = _lib.speechkv_pool_kv_segments(k_raw.data_ptr(), v_raw.data_ptr(), sb, ss, sh,
+                                        k_raw.shape[0], k_raw.shape[1], ctypes.byref(g), w,
+                                        _ptr(gate_u), layer, l0, ctypes.byref(c),
+                                        _ptr(cache_len_out), _stream(stream))
+    _check(st, "speechkv_pool_kv_segments")
+
+
+def speechkv_prefill_attn_segments(q: torch.Tensor, cache: PagedKV, segs: Segments, w: int,
+                                   layer: int, l0: int, out: torch.Tensor,
+                                   mask_mode: int = MASK_WINDOW_END, scale: Optional[float] = None,
+                                   lse: Optional[torch.Tensor] = None, stream=None) -> None:
+    """q, out: [B, q_len, Hq, D] contiguous; lse: [B, Hq, q_len] fp32 or None."""
+    for x in (q, out) + ((lse,) if lse is not None else ()):
+        if not x.is_contiguous():
+            raise ValueError("prefill tensors must be contiguous")
+    B, q_len, Hq, D = q.shape
+    if scale is None:
+        scale = D ** -0.5
+    c = cache._c()
+    g = segs._c()
+    st = _lib.speechkv_prefill_attn_segments(q.data_ptr(), B, Hq, q_len, ctypes.byref(c),
+                                             ctypes.byref(g), w, layer, l0, mask_mode, scale,
+                                             out.data_ptr(), _ptr(lse), _stream(stream))
+    _check(st, "speechkv_prefill_attn_segments")
+
+
+def speechkv_compressed_len_segments(segs, w: int, layer: int, l0: int) -> int:
+    """Compressed length of one sequence given as [(text_len, speech_len), ...]."""
+    n = len(segs)
+    t = (ctypes.c_int32 * max(n, 1))(*[x for x, _ in segs])
+    s = (ctypes.c_int32 * max(n, 1))(*[y for _, y in segs])
+    return int(_lib.speechkv_compressed_len_segments(ctypes.cast(t, _vp), ctypes.cast(s, _vp), n,
+                                                     w, layer, l0))
 
 
 def speechkv_pool_hidden(h: torch.Tensor, spans: Spans, w: int, gate_u: Optional[torch.Tensor],

@@ -15,12 +15,14 @@ from typing import List, Optional, Sequence
 import torch
 
 from . import inputs
-from .speechkv import (PagedKV, Spans, speechkv_compressed_len, speechkv_decode_attn,
+from .speechkv import (PagedKV, Segments, Spans, speechkv_compressed_len,
+                       speechkv_compressed_len_segments, speechkv_decode_attn,
                        speechkv_decode_num_splits, speechkv_decode_workspace_bytes,
                        speechkv_pool_hidden, speechkv_pool_kv, speechkv_pool_kv_bwd,
-                       speechkv_pool_kv_bwd_workspace_bytes, speechkv_pool_prefill_attn,
-                       speechkv_prefill_attn, speechkv_prefill_attn_bwd,
-                       speechkv_prefill_attn_bwd_workspace_bytes)
+                       speechkv_pool_kv_bwd_workspace_bytes, speechkv_pool_kv_segments,
+                       speechkv_pool_prefill_attn, speechkv_prefill_attn,
+                       speechkv_prefill_attn_bwd, speechkv_prefill_attn_bwd_workspace_bytes,
+                       speechkv_prefill_attn_segments)
 
 
 def visible_pairs(P: int, T: int, N: int, w: int) -> int:
@@ -343,3 +345,59 @@ class TrainJob:
         e = 2 if wl.dtype == "bf16" else 4
         row = wl.num_kv_heads * wl.head_dim
         return wl.batch * (4 * wl.prefill_len * row * e + 2 * self.clen * row * 4)
+
+
+# A multi-turn batch: three speech turns (30 s, 20 s and 40 s of 80 ms frames)
+# between text prompts, 1261 rows per sequence, 418 after w = 4 pooling.
+MULTI_TURN = [(32, 375), (24, 250), (16, 500), (64, 0)]
+
+
+class SegmentJob:
+    """One layer of a batch of sequences with several speech runs each
+    (segment tables): pooling into a paged cache, then prefill attention.
+    With one_run=True the same number of text rows and frames per sequence
+    is laid out as a single run (all text before the speech but the last
+    prompt), for comparison."""
+
+    def __init__(self, segs, batch=16, q_heads=16, kv_heads=8, head_dim=128, w=4, seed=6,
+                 page_size=16, one_run=False, device="cuda"):
+        self.segs = [list(segs)] * batch
+        self.w = w
+        self.one_run = one_run
+        rows = sum(t + s for t, s in segs)
+        self.rows = rows
+        self.clen = speechkv_compressed_len_segments(segs, w, 1, 0)
+        dt = torch.bfloat16
+        B, dev = batch, torch.device(device)
+        self.k_raw = inputs.normal((B, rows, kv_heads, head_dim), seed * 100 + 1, device=dev, dtype=dt)
+        self.v_raw = inputs.normal((B, rows, kv_heads, head_dim), seed * 100 + 2, device=dev, dtype=dt)
+        self.gate = inputs.normal((kv_heads, head_dim), seed * 100 + 3, device=dev,
+                                  scale=head_dim ** -0.5)
+        self.q = inputs.normal((B, rows, q_heads, head_dim), seed * 100 + 4, device=dev, dtype=dt)
+        self.out = torch.empty_like(self.q)
+        self.scale = head_dim ** -0.5
+        if one_run:
+            P = sum(t for t, _ in segs[:-1])
+            T = sum(s for _, s in segs)
+            N = segs[-1][0]
+            i32 = lambda v: torch.full((B,), v, dtype=torch.int32, device=dev)
+            self.spans = Spans(i32(P), i32(T), i32(N), T, rows)
+            self.clen = speechkv_compressed_len(P, T, N, w, 1, 0)
+        else:
+            self.table = Segments.from_lists(self.segs, device=dev)
+        pages = -(-self.clen // page_size)
+        table, total = inputs.block_table(B, pages, seed)
+        kp = torch.empty(total, kv_heads, page_size, head_dim, dtype=dt, device=dev)
+        self.cache = PagedKV(kp, torch.empty_like(kp), table.to(dev))
+
+    def run(self, stream=None):
+        if self.one_run:
+            speechkv_pool_kv(self.k_raw, self.v_raw, self.spans, self.w, self.gate, 1, 0,
+                             self.cache, stream=stream)
+            speechkv_prefill_attn(self.q, self.cache, self.spans, self.w, 1, 0, self.out,
+                                  scale=self.scale, stream=stream)
+        else:
+            speechkv_pool_kv_segments(self.k_raw, self.v_raw, self.table, self.w, self.gate, 1, 0,
+                                      self.cache, stream=stream)
+            speechkv_prefill_attn_segments(self.q, self.cache, self.table, self.w, 1, 0, self.out,
+                                           scale=self.scale, stream=stream)

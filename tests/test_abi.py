@@ -27,6 +27,8 @@ def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
                           "speechkv_pool_hidden", "speechkv_pool_prefill_attn",
+                          "speechkv_pool_kv_segments", "speechkv_prefill_attn_segments",
+                          "speechkv_compressed_len_segments",
                           "speechkv_prefill_attn_bwd",
                           "speechkv_prefill_attn_bwd_workspace_bytes", "speechkv_pool_kv_bwd",
                           "speechkv_pool_kv_bwd_workspace_bytes",
@@ -259,7 +261,8 @@ def test_binding_constants_match_header():
     import re
     defs = dict(re.findall(r"#define SPEECHKV_(\w+) \(?(-?\d+)\)?", open(HEADER).read()))
     for name in ("OK", "ERR_INVALID_ARG", "ERR_UNSUPPORTED", "ERR_WORKSPACE", "ERR_ALIAS", "ERR_HIP",
-                 "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START", "MAX_WINDOW"):
+                 "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START", "MAX_WINDOW",
+                 "MAX_SEGMENTS"):
         assert int(defs[name]) == getattr(skv, name), name
 
 
@@ -339,3 +342,83 @@ def pool_bwd(s=None, **kw):
 ])
 def test_pool_bwd_rejects(kw, code):
     assert pool_bwd(**kw) == code
+
+
+# ----------------------------------------------------------- segment tables
+
+def test_compressed_len_segments_agrees_with_oracle():
+    from oracle import segments as seg
+    cases = [[], [(0, 0)], [(32, 375), (24, 250), (16, 500), (64, 0)], [(3, 1), (0, 7), (5, 0)],
+             [(0, 9)] * 5]
+    for segs in cases:
+        for w in (1, 2, 3, 4, 8):
+            for layer, l0 in ((0, 0), (3, 5), (14, 14)):
+                assert skv.speechkv_compressed_len_segments(segs, w, layer, l0) == \
+                    seg.compressed_len(segs, w, layer, l0)
+    assert skv.speechkv_compressed_len_segments([(1, -1)], 4, 0, 0) == -1
+    assert skv.speechkv_compressed_len_segments([(1, 1)], 0, 0, 0) == -1
+
+
+SEG = FAKE + (25 << 24)
+
+
+def segments(**kw):
+    g = dict(seg_start=SEG, text_len=SEG + 256, speech_len=SEG + 512, num_segments=6,
+             max_segments=3, max_total_len=60)
+    g.update(kw)
+    return skv._Segments(**g)
+
+
+def pool_seg(c=None, g=None, **kw):
+    a = dict(k=RAW, v=RAW + (1 << 22), sb=60 * 2 * 64, ss=2 * 64, sh=64, batch=2, raw_len=60, w=4,
+             gate=None, layer=1, l0=0, clen=None)
+    a.update(kw)
+    c = c or cache()
+    g = g or segments()
+    return lib.speechkv_pool_kv_segments(a["k"], a["v"], a["sb"], a["ss"], a["sh"], a["batch"],
+                                         a["raw_len"], ctypes.byref(g), a["w"], a["gate"], a["layer"],
+                                         a["l0"], ctypes.byref(c), a["clen"], None)
+
+
+def prefill_seg(c=None, g=None, **kw):
+    a = dict(q=FAKE + (12 << 24), batch=2, hq=4, q_len=60, w=4, layer=1, l0=0, mode=0,
+             scale=0.125, out=FAKE + (13 << 24), lse=None)
+    a.update(kw)
+    c = c or cache()
+    g = g or segments()
+    return lib.speechkv_prefill_attn_segments(a["q"], a["batch"], a["hq"], a["q_len"],
+                                              ctypes.byref(c), ctypes.byref(g), a["w"], a["layer"],
+                                              a["l0"], a["mode"], a["scale"], a["out"], a["lse"],
+                                              None)
+
+
+@pytest.mark.parametrize("gkw", [dict(seg_start=None), dict(text_len=None), dict(speech_len=None),
+                                 dict(num_segments=-1), dict(max_segments=-1),
+                                 dict(max_segments=skv.MAX_SEGMENTS + 1), dict(max_total_len=-1)])
+def test_segment_tables_rejected(gkw):
+    assert pool_seg(g=segments(**gkw)) == E_ARG
+    assert prefill_seg(g=segments(**gkw)) == E_ARG
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=59), E_ARG), (dict(w=0), E_ARG),
+    (dict(w=skv.MAX_WINDOW + 1), E_ARG), (dict(layer=-1), E_ARG), (dict(ss=3), E_ARG),
+    (dict(gate=FAKE + 4), E_ARG), (dict(k=FAKE), E_ALIAS),
+])
+def test_pool_segments_rejects(kw, code):
+    assert pool_seg(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(q_len=59), E_ARG), (dict(mode=2), E_ARG),
+    (dict(w=0), E_ARG), (dict(hq=6), E_UNS), (dict(hq=5), E_ARG), (dict(lse=FAKE + 2), E_ARG),
+    (dict(scale=0.0), E_ARG), (dict(batch=0), E_ARG),
+])
+def test_prefill_segments_rejects(kw, code):
+    assert prefill_seg(**kw) == code
+
+
+def test_segment_calls_check_the_cache():
+    assert pool_seg(c=cache(head_dim=96)) == E_UNS
+    assert prefill_seg(c=cache(dtype=7)) == E_UNS
+    assert pool_seg(c=cache(k_pages=None)) == E_ARG

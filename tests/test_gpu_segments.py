@@ -1,0 +1,196 @@
+"""GPU parity for sequences with several speech runs (segment tables): the
+pooling into the paged cache and the prefill attention, through the C ABI,
+against the fp64 multi-run oracle (oracle/segments.py), on adversarial
+shapes (empty segments, runs shorter than w, ragged last windows, text-only
+and speech-only sequences, many segments) and a multi-turn workload; and a
+table holding one run per sequence must give the bits of the one-run calls.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import segments as seg
+from helpers import TOL, f64, gather, rel_err
+from paper_2607_06827_amd import inputs
+from paper_2607_06827_amd import speechkv as skv
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def build(segs, Hq=4, Hkv=2, D=64, dtype="bf16", page_size=16, w=4, layer=1, l0=0, seed=0,
+          zero_gate=False):
+    B = len(segs)
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    rows = [seg.raw_len(s) for s in segs]
+    S = max(max(rows), 1)
+    s0 = 5000 + seed * 10
+    x = dict(B=B, S=S, dt=dt, rows=rows)
+    x["k"] = inputs.normal((B, S, Hkv, D), s0 + 1, dtype=dt)
+    x["v"] = inputs.normal((B, S, Hkv, D), s0 + 2, dtype=dt)
+    x["u"] = None if zero_gate else inputs.normal((Hkv, D), s0 + 3, scale=1 / math.sqrt(D))
+    x["q"] = inputs.normal((B, S, Hq, D), s0 + 4, dtype=dt)
+    x["clen"] = [seg.compressed_len(s, w, layer, l0) for s in segs]
+    pages = max(1, -(-max(max(x["clen"]), 1) // page_size))
+    table, total = inputs.block_table(B, pages, seed, shuffle=True, spare_pages=2)
+    nan = lambda: torch.full((total, Hkv, page_size, D), float("nan"), dtype=dt, device="cuda")
+    x["cache"] = skv.PagedKV(nan(), nan(), table.cuda())
+    x["segs"] = skv.Segments.from_lists(segs)
+    return x
+
+
+def run_segments(x, segs, w, layer, l0, mode):
+    dev = torch.device("cuda")
+    B, S = x["B"], x["S"]
+    Hq, D = x["q"].shape[2], x["q"].shape[3]
+    clen = torch.full((B,), -7, dtype=torch.int32, device=dev)
+    u = None if x["u"] is None else x["u"].cuda()
+    skv.speechkv_pool_kv_segments(x["k"].cuda(), x["v"].cuda(), x["segs"], w, u, layer, l0,
+                                  x["cache"], clen)
+    out = torch.full((B, S, Hq, D), float("nan"), dtype=x["dt"], device=dev)
+    lse = torch.full((B, Hq, S), float("nan"), dtype=torch.float32, device=dev)
+    skv.speechkv_prefill_attn_segments(x["q"].cuda(), x["cache"], x["segs"], w, layer, l0, out,
+                                       mask_mode=mode, scale=D ** -0.5, lse=lse)
+    torch.cuda.synchronize()
+    return clen.cpu().tolist(), out, lse
+
+
+def check(segs, w=4, layer=1, l0=0, mode=0, **kw):
+    x = build(segs, w=w, layer=layer, l0=l0, **kw)
+    clen, out, lse = run_segments(x, segs, w, layer, l0, mode)
+    assert clen == x["clen"]
+    tol = TOL["bf16" if x["dt"] == torch.bfloat16 else "f32"]
+    u64 = None if x["u"] is None else f64(x["u"])
+    kh, vh, oclen = seg.pool(f64(x["k"]), f64(x["v"]), segs, w, layer, l0, u64)
+    assert oclen.tolist() == x["clen"]
+    D = x["q"].shape[3]
+    ref, ref_lse = seg.attention(f64(x["q"]), kh, vh, segs, w, layer, l0, mode, D ** -0.5)
+    errs = {}
+    for b, s in enumerate(segs):
+        L, R = x["clen"][b], x["rows"][b]
+        if L:
+            gk, gv = gather(x["cache"], b, L)
+            errs[f"pool_k[{b}]"] = rel_err(f64(gk), kh[b, :L])
+            errs[f"pool_v[{b}]"] = rel_err(f64(gv), vh[b, :L])
+            # text rows are copies, bit for bit
+            slots, _ = seg.layout(s, w if layer >= l0 else 1)
+            for c, (first, n, _, _) in enumerate(slots):
+                if n == 1:
+                    assert torch.equal(gk[c].cpu(), x["k"][b, first])
+        if R:
+            go = f64(out[b, :R])
+            assert np.all(np.isfinite(go))
+            errs[f"prefill[{b}]"] = rel_err(go, ref[b, :R])
+            gl, rl = f64(lse[b, :, :R]), ref_lse[b, :, :R]
+            assert np.array_equal(np.isneginf(gl), np.isneginf(rl))
+            fin = np.isfinite(rl)
+            if fin.any():
+                errs[f"lse[{b}]"] = float(np.max(np.abs(gl[fin] - rl[fin])))
+        if R < x["S"]:
+            assert torch.isnan(out[b, R:]).all()
+    bad = {k: e for k, e in errs.items() if not e <= tol}
+    assert not bad, f"{segs}: above {tol}: {bad}"
+    return x, clen, out, lse
+
+
+CASES = {
+    "three-turns": dict(segs=[[(8, 60), (5, 33), (6, 0)]], D=128),
+    "turns-varlen": dict(segs=[[(4, 17), (2, 9), (0, 30), (7, 0)], [(0, 41)], [(3, 0)],
+                               [(1, 2), (1, 3), (1, 5), (1, 7), (2, 0)]]),
+    "empty-and-zero-segments": dict(segs=[[], [(0, 0), (0, 0)], [(0, 0), (5, 12), (0, 0), (0, 3)]]),
+    "runs-shorter-than-w": dict(segs=[[(2, 3), (1, 2), (4, 1), (2, 0)]], w=8),
+    "speech-first-rows-see-nothing": dict(segs=[[(0, 30), (4, 25)], [(0, 7), (0, 9), (3, 0)]]),
+    "window-start-mask": dict(segs=[[(3, 41), (2, 30), (7, 0)], [(9, 30), (1, 1)]], mode=1),
+    "identity-below-l0": dict(segs=[[(6, 50), (3, 20), (4, 0)]], layer=2, l0=5),
+    "w1": dict(segs=[[(6, 50), (3, 20), (4, 0)]], w=1),
+    "w16": dict(segs=[[(3, 200), (5, 77), (2, 0)]], w=16, D=128),
+    "many-segments": dict(segs=[[(2, 5)] * 40 + [(6, 0)], [(1, 11)] * 25]),
+    "g8-d128": dict(segs=[[(4, 90), (3, 80), (3, 0)]], Hq=8, Hkv=1, D=128),
+    "g1": dict(segs=[[(4, 90), (3, 80), (3, 0)]], Hq=2, Hkv=2, D=128),
+    "fp32": dict(segs=[[(8, 60), (5, 33), (6, 0)], [(0, 17), (2, 0)]], dtype="f32"),
+    "fp32-d128-g4": dict(segs=[[(8, 160), (5, 33), (6, 0)]], dtype="f32", D=128, Hq=8, Hkv=2),
+    "page8": dict(segs=[[(5, 77), (2, 30), (1, 0)], [(2, 64), (6, 1)]], page_size=8),
+    "zero-gate": dict(segs=[[(4, 70), (3, 21), (3, 0)]], zero_gate=True),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_segments_match_oracle(name):
+    print(f"case {name}", flush=True)
+    kw = dict(CASES[name])
+    check(kw.pop("segs"), **kw)
+
+
+@pytest.mark.parametrize("dtype,D,mode", [("bf16", 128, 0), ("bf16", 64, 1), ("f32", 64, 0)])
+def test_one_run_table_equals_one_run_calls(dtype, D, mode):
+    """{(P, T), (N, 0)} per sequence gives the bits of the one-run calls."""
+    P, T, N, w = [8, 0, 5], [60, 37, 0], [5, 3, 9], 4
+    segs = [[(p, t), (n, 0)] for p, t, n in zip(P, T, N)]
+    x = build(segs, D=D, dtype=dtype, Hq=8, Hkv=2, w=w)
+    clen_s, out_s, lse_s = run_segments(x, segs, w, 1, 0, mode)
+    B, S = x["B"], x["S"]
+    cache = skv.PagedKV(torch.full_like(x["cache"].k_pages, float("nan")),
+                        torch.full_like(x["cache"].v_pages, float("nan")), x["cache"].block_table)
+    i32 = lambda v: torch.tensor(v, dtype=torch.int32, device="cuda")
+    spans = skv.Spans(i32(P), i32(T), i32(N), max(T), max(p + t + n for p, t, n in zip(P, T, N)))
+    clen = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    u = x["u"].cuda()
+    skv.speechkv_pool_kv(x["k"].cuda(), x["v"].cuda(), spans, w, u, 1, 0, cache, clen)
+    out = torch.full_like(out_s, float("nan"))
+    lse = torch.full_like(lse_s, float("nan"))
+    skv.speechkv_prefill_attn(x["q"].cuda(), cache, spans, w, 1, 0, out, mask_mode=mode,
+                              scale=D ** -0.5, lse=lse)
+    torch.cuda.synchronize()
+    assert clen.cpu().tolist() == clen_s
+    for b in range(B):
+        L, R = clen_s[b], x["rows"][b]
+        ka, va = gather(x["cache"], b, L)
+        kb, vb = gather(cache, b, L)
+        assert torch.equal(ka, kb) and torch.equal(va, vb)
+        assert torch.equal(out_s[b, :R], out[b, :R])
+        fin = torch.isfinite(lse_s[b, :, :R])
+        assert torch.equal(fin, torch.isfinite(lse[b, :, :R]))
+        assert torch.equal(lse_s[b, :, :R][fin], lse[b, :, :R][fin])
+
+
+def test_decode_after_segment_pooling():
+    """Decoding needs only the cache length: after the multi-run pooling a
+    decode step attends over exactly the pooled rows and the new token."""
+    segs = [[(8, 60), (5, 33), (6, 0)], [(0, 17), (2, 40)]]
+    x, clen, _, _ = check(segs, D=128, Hq=8, Hkv=2)
+    B, Hq, Hkv, D = 2, 8, 2, 128
+    q = inputs.normal((B, Hq, D), 5101, dtype=x["dt"])
+    kn = inputs.normal((B, Hkv, D), 5102, dtype=x["dt"])
+    vn = inputs.normal((B, Hkv, D), 5103, dtype=x["dt"])
+    lens = [c + 1 for c in clen]
+    out = torch.empty(B, Hq, D, dtype=x["dt"], device="cuda")
+    ws_bytes = skv.speechkv_decode_workspace_bytes(B, Hq, Hkv, D, max(lens), 0)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    skv.speechkv_decode_attn(q.cuda(), x["cache"], torch.tensor(lens, dtype=torch.int32).cuda(),
+                             max(lens), out, k_new=kn.cuda(), v_new=vn.cuda(), scale=D ** -0.5,
+                             workspace=ws)
+    torch.cuda.synchronize()
+    kh, vh, _ = seg.pool(f64(x["k"]), f64(x["v"]), segs, 4, 1, 0, f64(x["u"]))
+    K = np.zeros((B, max(lens), Hkv, D))
+    V = np.zeros((B, max(lens), Hkv, D))
+    for b in range(B):
+        K[b, :clen[b]] = kh[b, :clen[b]]
+        V[b, :clen[b]] = vh[b, :clen[b]]
+        K[b, clen[b]] = f64(kn[b])
+        V[b, clen[b]] = f64(vn[b])
+    ref, _ = oracle.decode(f64(q), K, V, lens, D ** -0.5)
+    assert rel_err(f64(out), ref) <= TOL["bf16"]
+
+
+def test_multi_turn_workload():
+    """A multi-turn batch at full size: 16 sequences of three speech turns
+    (30 s, 20 s and 40 s of 80 ms frames) between text, 16/8 heads, d=128,
+    every pooled row and prefill output against the oracle."""
+    turns = [(32, 375), (24, 250), (16, 500), (64, 0)]
+    segs = [list(turns) for _ in range(16)]
+    segs[3] = [(32, 375), (64, 0)]          # one turn only
+    segs[7] = [(0, 500), (24, 250), (8, 0)]  # speech first
+    check(segs, Hq=16, Hkv=8, D=128, seed=3)
