@@ -331,6 +331,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-full", action="store_true", help="skip the uncompressed run")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time the benchmark step only (no fused, multi-turn, adaptive-window, "
+                         "HS-pooling or training figures), e.g. for a kernel trace of that step")
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--traffic", action="store_true",
                     help="counter-collection run: the job's launches and one HS pooling launch "
@@ -409,17 +412,20 @@ def main():
         del fjob
         torch.cuda.empty_cache()
 
-    fused = measure_fused(job, args.steps)
-    torch.cuda.empty_cache()
-    segments = measure_segments(args.steps)
-    torch.cuda.empty_cache()
-    adaptive = measure_adaptive(job, args.steps, args.warmup, args.num_splits)
-    adaptive["speedup_over_uniform_w"] = adaptive["tokens_per_s"] / pooled["tokens_per_s"]
-    torch.cuda.empty_cache()
-    hs_pool = measure_hs_pool(wl, args.steps)
-    torch.cuda.empty_cache()
-    train_bwd = measure_train_bwd(args.steps)
-    torch.cuda.empty_cache()
+    extras = {}
+    if not args.no_extras:
+        extras["fused_prefill"] = measure_fused(job, args.steps)
+        torch.cuda.empty_cache()
+        extras["multi_turn"] = measure_segments(args.steps)
+        torch.cuda.empty_cache()
+        adaptive = measure_adaptive(job, args.steps, args.warmup, args.num_splits)
+        adaptive["speedup_over_uniform_w"] = adaptive["tokens_per_s"] / pooled["tokens_per_s"]
+        extras["adaptive_w"] = adaptive
+        torch.cuda.empty_cache()
+        extras["hs_pool"] = measure_hs_pool(wl, args.steps)
+        torch.cuda.empty_cache()
+        extras["train_bwd"] = measure_train_bwd(args.steps)
+        torch.cuda.empty_cache()
 
     dec_bytes, launches = decode_launch_stats(job)
     avg_launch_ms = pooled["decode_ms"] / launches
@@ -453,11 +459,7 @@ def main():
         "prefill_ms": pooled["prefill_ms"],
         "pool": pooled["pool"],
         "prefill_attn": pooled["prefill_attn"],
-        "fused_prefill": fused,
-        "multi_turn": segments,
-        "adaptive_w": adaptive,
-        "hs_pool": hs_pool,
-        "train_bwd": train_bwd,
+        **extras,
     }
     if full:
         result["full_kv"] = {"tokens_per_s": full["tokens_per_s"], "ms_per_step": full["ms_per_step"],
