@@ -125,3 +125,77 @@ def attention(q, k_hat, v_hat, segs_list: List[Segs], w, layer, l0, mask_mode=0,
             out[b, :R, h] = o
             lse[b, h, :R] = np.where(seen, m + np.log(np.where(seen, l, 1.0)), -np.inf)
     return out, lse
+
+
+def attention_bwd(q, k_hat, v_hat, segs_list: List[Segs], w, layer, l0, dout, mask_mode=0,
+                  scale=None):
+    """Gradients of attention() (the chain rule of Eq. 5 under the mask):
+    with P the row softmax over visible keys, dV = P^T dO, dP = dO V^T,
+    dZ = P o (dP - rowsum(P o dP)), dQ = scale dZ K, dK = scale dZ^T Q (key
+    gradients summed over the query heads of a KV head).  Returns
+    (dq [B, Sq, Hq, D], dk [B, Lc, Hkv, D], dv [B, Lc, Hkv, D])."""
+    q = np.asarray(q, np.float64)
+    kh = np.asarray(k_hat, np.float64)
+    vh = np.asarray(v_hat, np.float64)
+    do = np.asarray(dout, np.float64)
+    B, Sq, Hq, D = q.shape
+    Hkv = kh.shape[2]
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    we = w_eff(w, layer, l0)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(kh)
+    dv = np.zeros_like(vh)
+    for b, segs in enumerate(segs_list):
+        R = raw_len(segs)
+        tau = visible_from(segs, we, mask_mode)
+        L = len(tau)
+        vis = tau[None, :] <= np.arange(R)[:, None]
+        for h in range(Hq):
+            g = h // G
+            s = np.where(vis, scale * (q[b, :R, h] @ kh[b, :L, g].T), -np.inf)
+            m = s.max(axis=1, initial=-np.inf)
+            seen = np.isfinite(m)
+            p = np.where(vis, np.exp(s - np.where(seen, m, 0.0)[:, None]), 0.0)
+            l = p.sum(axis=1)
+            p[seen] /= l[seen][:, None]
+            dp = do[b, :R, h] @ vh[b, :L, g].T
+            dz = p * (dp - (p * dp).sum(axis=1, keepdims=True))
+            dv[b, :L, g] += p.T @ do[b, :R, h]
+            dq[b, :R, h] = scale * (dz @ kh[b, :L, g])
+            dk[b, :L, g] += scale * (dz.T @ q[b, :R, h])
+    return dq, dk, dv
+
+
+def pool_bwd(k_raw, v_raw, segs_list: List[Segs], w, layer, l0, u, dk_hat, dv_hat):
+    """Gradients of pool() (the chain rule of Eq. 4): for a window with
+    weights a = softmax(u . k_j), da_j = dK^ . k_j + dV^ . v_j and
+    ds_j = a_j (da_j - sum_i a_i da_i); dk_j = a_j dK^ + ds_j u,
+    dv_j = a_j dV^, du = sum over windows of ds_j k_j.  Returns
+    (dk_raw, dv_raw [B, S, Hkv, D], du [Hkv, D])."""
+    k = np.asarray(k_raw, np.float64)
+    v = np.asarray(v_raw, np.float64)
+    gk = np.asarray(dk_hat, np.float64)
+    gv = np.asarray(dv_hat, np.float64)
+    B, S, H, D = k.shape
+    uu = np.zeros((H, D)) if u is None else np.asarray(u, np.float64)
+    we = w_eff(w, layer, l0)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    du = np.zeros((H, D))
+    for b, segs in enumerate(segs_list):
+        slots, _ = layout(segs, we)
+        for c, (first, n, _, _) in enumerate(slots):
+            kw = k[b, first:first + n]
+            vw = v[b, first:first + n]
+            for g in range(H):
+                logits = kw[:, g] @ uu[g]
+                a = np.exp(logits - logits.max())
+                a /= a.sum()
+                da = kw[:, g] @ gk[b, c, g] + vw[:, g] @ gv[b, c, g]
+                ds = a * (da - a @ da)
+                dk[b, first:first + n, g] = a[:, None] * gk[b, c, g][None] + ds[:, None] * uu[g][None]
+                dv[b, first:first + n, g] = a[:, None] * gv[b, c, g][None]
+                du[g] += ds @ kw[:, g]
+    return dk, dv, du

@@ -181,3 +181,62 @@ def test_pins_catch_planted_mistakes(mutant, monkeypatch):
         except (AssertionError, IndexError, ValueError):
             caught += 1
     assert caught > 0, f"{mutant.__name__} passed every pin"
+
+
+# ------------------------------------------------------------------ backward
+
+@pytest.mark.parametrize("P,T,N,w,mode", [(8, 30, 5, 4, 0), (0, 19, 3, 4, 1), (3, 11, 2, 1, 0),
+                                          (2, 7, 5, 4, 0)])
+def test_one_run_backward_equals_single_span_oracle(P, T, N, w, mode):
+    S, H, Hq, D = P + T + N, 2, 4, 8
+    k, v = rand((1, S, H, D), 31), rand((1, S, H, D), 32)
+    u, q, do = rand((H, D), 33, 0.5), rand((1, S, Hq, D), 34), rand((1, S, Hq, D), 35)
+    segs = [[(P, T), (N, 0)]]
+    kh, vh, clen = seg.pool(k, v, segs, w, 1, 0, u)
+    dq, dkh, dvh = seg.attention_bwd(q, kh, vh, segs, w, 1, 0, do, mode)
+    rq, rk, rv = oracle.attention_bwd(q, kh, vh, [P], [T], [N], w, 1, 0, do, mode)
+    L = int(clen[0])
+    np.testing.assert_allclose(dq[0, :S], rq[0, :S], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(dkh[0, :L], rk[0, :L], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(dvh[0, :L], rv[0, :L], rtol=1e-9, atol=1e-12)
+    dk, dv, du = seg.pool_bwd(k, v, segs, w, 1, 0, u, dkh, dvh)
+    pk, pv, pu = oracle.pool_bwd(k, v, [P], [T], [N], w, 1, 0, u, dkh, dvh)
+    np.testing.assert_allclose(dk[0, :S], pk[0, :S], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(dv[0, :S], pv[0, :S], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(du, pu, rtol=1e-9, atol=1e-12)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_backward_finite_differences_several_runs(mode):
+    """The chain pool -> attention over three runs: the gradients of
+    L = sum(dout * out) match central differences of the pinned forward in
+    random directions, for q, the raw keys and values, and the gate."""
+    segs = [[(2, 9), (3, 6), (0, 5), (2, 0)], [(0, 7), (1, 2)]]
+    S = max(seg.raw_len(s) for s in segs)
+    B, H, Hq, D, w = 2, 2, 4, 8, 3
+    k, v = rand((B, S, H, D), 41), rand((B, S, H, D), 42)
+    u, q, do = rand((H, D), 43, 0.7), rand((B, S, Hq, D), 44), rand((B, S, Hq, D), 45)
+    rows = [seg.raw_len(s) for s in segs]
+    for b, R in enumerate(rows):  # rows past a sequence carry no gradient
+        do[b, R:] = 0.0
+
+    def loss(q_, k_, v_, u_):
+        kh, vh, _ = seg.pool(k_, v_, segs, w, 1, 0, u_)
+        out, _ = seg.attention(q_, kh, vh, segs, w, 1, 0, mode)
+        return float((out * do).sum())
+
+    kh, vh, _ = seg.pool(k, v, segs, w, 1, 0, u)
+    dq, dkh, dvh = seg.attention_bwd(q, kh, vh, segs, w, 1, 0, do, mode)
+    dk, dv, du = seg.pool_bwd(k, v, segs, w, 1, 0, u, dkh, dvh)
+    eps = 1e-5
+    for name, x, grad in (("q", q, dq), ("k", k, dk), ("v", v, dv), ("u", u, du)):
+        dirn = rand(x.shape, 46 + len(name))
+        args = dict(q_=q, k_=k, v_=v, u_=u)
+        key = name + "_"
+        args[key] = x + eps * dirn
+        lp = loss(**args)
+        args[key] = x - eps * dirn
+        lm = loss(**args)
+        fd = (lp - lm) / (2 * eps)
+        an = float((grad * dirn).sum())
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(fd)), (name, fd, an)
