@@ -25,6 +25,10 @@
  *   speechkv_prefill_attn_bwd  gradients of speechkv_prefill_attn: dQ, dK^, dV^
  *   speechkv_pool_kv_bwd       gradients of the pooling: raw dK, dV and the
  *                              gate's du
+ * Sequences with several speech runs (multi-turn inputs) take a segment table
+ * instead of the one-run spans: speechkv_pool_kv_segments,
+ * speechkv_prefill_attn_segments and their backward
+ * speechkv_prefill_attn_bwd_segments and speechkv_pool_kv_bwd_segments.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -431,6 +435,22 @@ int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads,
                               void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/*
+ * speechkv_prefill_attn_bwd_segments - speechkv_prefill_attn_bwd for
+ * sequences with several speech runs (the forward's
+ * speechkv_prefill_attn_segments); segs (host pointer) replaces spans and
+ * segs->max_total_len must not exceed q_len.  Everything else as above.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, ALIAS, HIP.
+ */
+int speechkv_prefill_attn_bwd_segments(const void* q, int32_t batch, int32_t num_q_heads,
+                                       int32_t q_len, const speechkv_paged_kv* cache,
+                                       const speechkv_segments* segs, int32_t w,
+                                       int32_t layer, int32_t l0, int32_t mask_mode,
+                                       float scale, const void* out, const float* lse,
+                                       const void* dout, void* dq, float* dk_hat,
+                                       float* dv_hat, int32_t hat_capacity, void* workspace,
+                                       size_t workspace_bytes, void* stream);
+
 /* Workspace bytes of speechkv_prefill_attn_bwd (one fp32 per query row and
  * head), or 0 for invalid arguments.  Host only. */
 size_t speechkv_prefill_attn_bwd_workspace_bytes(int32_t batch,
@@ -479,6 +499,25 @@ int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw,
                          int32_t hat_capacity, void* dk_raw, void* dv_raw,
                          float* du, void* workspace, size_t workspace_bytes,
                          void* stream);
+
+/*
+ * speechkv_pool_kv_bwd_segments - speechkv_pool_kv_bwd for sequences with
+ * several speech runs (the forward's speechkv_pool_kv_segments); segs (host
+ * pointer) replaces spans and segs->max_total_len must not exceed raw_len.
+ * The workspace size is speechkv_pool_kv_bwd_workspace_bytes with
+ * max_total_len = segs->max_total_len.  Everything else as above.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, ALIAS, HIP.
+ */
+int speechkv_pool_kv_bwd_segments(const void* k_raw, const void* v_raw,
+                                  int64_t stride_b, int64_t stride_s, int64_t stride_h,
+                                  int32_t batch, int32_t raw_len, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t dtype,
+                                  const speechkv_segments* segs, int32_t w,
+                                  const float* gate_u, int32_t layer, int32_t l0,
+                                  const float* dk_hat, const float* dv_hat,
+                                  int32_t hat_capacity, void* dk_raw, void* dv_raw,
+                                  float* du, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /* Workspace bytes of speechkv_pool_kv_bwd with a gate gradient, for
  * max_total_len = spans->max_total_len, or 0 for invalid or unsupported

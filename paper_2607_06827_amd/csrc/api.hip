@@ -502,12 +502,14 @@ size_t speechkv_prefill_attn_bwd_workspace_bytes(int32_t batch, int32_t num_q_he
   return (size_t)batch * num_q_heads * q_len * sizeof(float);
 }
 
-int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
-                              const speechkv_paged_kv* cache, const speechkv_spans* spans, int32_t w,
-                              int32_t layer, int32_t l0, int32_t mask_mode, float scale,
-                              const void* out, const float* lse, const void* dout, void* dq,
-                              float* dk_hat, float* dv_hat, int32_t hat_capacity, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+// speechkv_prefill_attn_bwd and speechkv_prefill_attn_bwd_segments (segs set)
+static int prefill_attn_bwd_impl(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                                 const speechkv_paged_kv* cache, const speechkv_spans* spans,
+                                 const skv::SegmentTable* segs, int32_t w, int32_t layer, int32_t l0,
+                                 int32_t mask_mode, float scale, const void* out, const float* lse,
+                                 const void* dout, void* dq, float* dk_hat, float* dv_hat,
+                                 int32_t hat_capacity, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
   if (!q || !out || !lse || !dout || !dq || !dk_hat || !dv_hat) return SPEECHKV_ERR_INVALID_ARG;
   int st = check_cache(cache);
   if (st) return st;
@@ -578,8 +580,36 @@ int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads,
   a.dk_hat = dk_hat;
   a.dv_hat = dv_hat;
   a.hat_cap = hat_capacity;
+  if (segs) a.segs = *segs;
   return status_of(skv::launch_prefill_bwd(a, cache->dtype, cache->head_dim, group, batch,
                                            static_cast<hipStream_t>(stream)));
+}
+
+int speechkv_prefill_attn_bwd(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
+                              const speechkv_paged_kv* cache, const speechkv_spans* spans, int32_t w,
+                              int32_t layer, int32_t l0, int32_t mask_mode, float scale,
+                              const void* out, const float* lse, const void* dout, void* dq,
+                              float* dk_hat, float* dv_hat, int32_t hat_capacity, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  return prefill_attn_bwd_impl(q, batch, num_q_heads, q_len, cache, spans, nullptr, w, layer, l0,
+                               mask_mode, scale, out, lse, dout, dq, dk_hat, dv_hat, hat_capacity,
+                               workspace, workspace_bytes, stream);
+}
+
+int speechkv_prefill_attn_bwd_segments(const void* q, int32_t batch, int32_t num_q_heads,
+                                       int32_t q_len, const speechkv_paged_kv* cache,
+                                       const speechkv_segments* segs, int32_t w, int32_t layer,
+                                       int32_t l0, int32_t mask_mode, float scale, const void* out,
+                                       const float* lse, const void* dout, void* dq,
+                                       float* dk_hat, float* dv_hat, int32_t hat_capacity,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  const int st = check_segments(segs);
+  if (st) return st;
+  const speechkv_spans sp = spans_of(segs);
+  const skv::SegmentTable t = table_of(segs);
+  return prefill_attn_bwd_impl(q, batch, num_q_heads, q_len, cache, &sp, &t, w, layer, l0,
+                               mask_mode, scale, out, lse, dout, dq, dk_hat, dv_hat, hat_capacity,
+                               workspace, workspace_bytes, stream);
 }
 
 size_t speechkv_pool_kv_bwd_workspace_bytes(int32_t batch, int32_t max_total_len,
@@ -591,12 +621,14 @@ size_t speechkv_pool_kv_bwd_workspace_bytes(int32_t batch, int32_t max_total_len
   return (size_t)batch * blocks * num_kv_heads * head_dim * sizeof(float);
 }
 
-int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
-                         int64_t stride_h, int32_t batch, int32_t raw_len, int32_t num_kv_heads,
-                         int32_t head_dim, int32_t dtype, const speechkv_spans* spans, int32_t w,
-                         const float* gate_u, int32_t layer, int32_t l0, const float* dk_hat,
-                         const float* dv_hat, int32_t hat_capacity, void* dk_raw, void* dv_raw,
-                         float* du, void* workspace, size_t workspace_bytes, void* stream) {
+// speechkv_pool_kv_bwd and speechkv_pool_kv_bwd_segments (segs set)
+static int pool_kv_bwd_impl(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
+                            int64_t stride_h, int32_t batch, int32_t raw_len, int32_t num_kv_heads,
+                            int32_t head_dim, int32_t dtype, const speechkv_spans* spans,
+                            const skv::SegmentTable* segs, int32_t w, const float* gate_u,
+                            int32_t layer, int32_t l0, const float* dk_hat, const float* dv_hat,
+                            int32_t hat_capacity, void* dk_raw, void* dv_raw, float* du,
+                            void* workspace, size_t workspace_bytes, void* stream) {
   if (!k_raw || !v_raw || !dk_hat || !dv_hat || !dk_raw || !dv_raw) return SPEECHKV_ERR_INVALID_ARG;
   int st = check_spans(spans);
   if (st) return st;
@@ -659,7 +691,36 @@ int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw, int64_t stride_b,
   a.max_out = spans->max_total_len;
   a.slots_per_block = spb;
   a.blocks_per_seq = spans->max_total_len > 0 ? (spans->max_total_len + spb - 1) / spb : 1;
+  if (segs) a.segs = *segs;
   return status_of(skv::launch_pool_bwd(a, dtype, head_dim, batch, static_cast<hipStream_t>(stream)));
+}
+
+int speechkv_pool_kv_bwd(const void* k_raw, const void* v_raw, int64_t stride_b, int64_t stride_s,
+                         int64_t stride_h, int32_t batch, int32_t raw_len, int32_t num_kv_heads,
+                         int32_t head_dim, int32_t dtype, const speechkv_spans* spans, int32_t w,
+                         const float* gate_u, int32_t layer, int32_t l0, const float* dk_hat,
+                         const float* dv_hat, int32_t hat_capacity, void* dk_raw, void* dv_raw,
+                         float* du, void* workspace, size_t workspace_bytes, void* stream) {
+  return pool_kv_bwd_impl(k_raw, v_raw, stride_b, stride_s, stride_h, batch, raw_len, num_kv_heads,
+                          head_dim, dtype, spans, nullptr, w, gate_u, layer, l0, dk_hat, dv_hat,
+                          hat_capacity, dk_raw, dv_raw, du, workspace, workspace_bytes, stream);
+}
+
+int speechkv_pool_kv_bwd_segments(const void* k_raw, const void* v_raw, int64_t stride_b,
+                                  int64_t stride_s, int64_t stride_h, int32_t batch,
+                                  int32_t raw_len, int32_t num_kv_heads, int32_t head_dim,
+                                  int32_t dtype, const speechkv_segments* segs, int32_t w,
+                                  const float* gate_u, int32_t layer, int32_t l0,
+                                  const float* dk_hat, const float* dv_hat, int32_t hat_capacity,
+                                  void* dk_raw, void* dv_raw, float* du, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  const int st = check_segments(segs);
+  if (st) return st;
+  const speechkv_spans sp = spans_of(segs);
+  const skv::SegmentTable t = table_of(segs);
+  return pool_kv_bwd_impl(k_raw, v_raw, stride_b, stride_s, stride_h, batch, raw_len, num_kv_heads,
+                          head_dim, dtype, &sp, &t, w, gate_u, layer, l0, dk_hat, dv_hat,
+                          hat_capacity, dk_raw, dv_raw, du, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

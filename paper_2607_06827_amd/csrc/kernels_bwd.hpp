@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include "common.hpp"
+#include "spans.hpp"
 
 namespace skv {
 
@@ -36,6 +37,7 @@ struct PrefillBwdArgs {
   float* dk_hat;      // [B][hat_cap][Hkv][D] fp32
   float* dv_hat;
   int hat_cap;
+  SegmentTable segs;  // several speech runs per sequence when segs.seg_start is set
 };
 
 // Window pooling backward (Eq. 4): raw K/V gradients and the gate's.
@@ -60,6 +62,7 @@ struct PoolBwdArgs {
   int max_out;          // bound on the compressed length
   int slots_per_block;
   int blocks_per_seq;
+  SegmentTable segs;    // several speech runs per sequence when segs.seg_start is set
 };
 
 int prefill_bwd_rows_per_tile(int group);

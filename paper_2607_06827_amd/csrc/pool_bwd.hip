@@ -32,7 +32,7 @@ constexpr int kTargetBlocks = 1024;  // about four blocks per CU, and as many ga
 template <int D>
 constexpr int lanes_per_head() { return D / 8; }
 
-template <typename T, int D, bool kGate>
+template <typename T, int D, bool kGate, bool kRuns>
 __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
   constexpr int kLanes = lanes_per_head<D>();
   const int heads = a.kv_heads;
@@ -43,12 +43,8 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
   const int g = u / kLanes, j = u % kLanes;
   const int b = blockIdx.y;
 
-  const int P = max(a.prefix_len[b], 0);
-  const int S = max(a.speech_len[b], 0);
-  const int N = max(a.suffix_len[b], 0);
-  const int w = a.w_eff;
-  const int nW = (S + w - 1) / w;
-  const int len = min(min(P + nW + N, a.max_out), a.hat_cap);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int len = min(min(sp.clen(), a.max_out), a.hat_cap);
 
   const int64_t base = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h + 8 * j;
   const T* kr = static_cast<const T*>(a.k_raw) + base;
@@ -75,9 +71,8 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
   for (int k = 0; k < iters; ++k) {
     const int c = (blockIdx.x * iters + k) * slot_lanes + sl;
     if (sl >= slot_lanes || c >= len) continue;
-    const bool text_before = c < P, text_after = c >= P + nW;
-    const int src = text_before ? c : text_after ? P + S + (c - P - nW) : P + (c - P) * w;
-    const int n = (text_before || text_after) ? 1 : min(w, P + S - src);
+    const SlotSource slot = sp.slot(c);
+    const int src = slot.first, n = slot.frames;
     if (src + n > a.raw_len) continue;  // a broken caller obligation: rows left alone
 
     // gradient of pooled row c (fp32)
@@ -217,8 +212,13 @@ __global__ __launch_bounds__(256) void du_reduce_kernel(const float* part, int p
 template <typename T, int D>
 hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
   const dim3 grid((unsigned)a.blocks_per_seq, batch);
-  hipError_t e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true>, grid, dim3(256), s, a)
-                        : launch_struct(pool_bwd_kernel<T, D, false>, grid, dim3(256), s, a);
+  hipError_t e;
+  if (a.segs.seg_start)
+    e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true, true>, grid, dim3(256), s, a)
+               : launch_struct(pool_bwd_kernel<T, D, false, true>, grid, dim3(256), s, a);
+  else
+    e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true, false>, grid, dim3(256), s, a)
+               : launch_struct(pool_bwd_kernel<T, D, false, false>, grid, dim3(256), s, a);
   if (e != hipSuccess || !a.du) return e;
   const int n = a.kv_heads * D;
   hipLaunchKernelGGL(du_reduce_kernel, dim3((n + kReduceOut - 1) / kReduceOut), dim3(256), 0, s,

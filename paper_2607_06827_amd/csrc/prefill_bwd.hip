@@ -52,18 +52,6 @@ constexpr float kLog2eF = 1.4426950408889634f;
 constexpr int wait_vmcnt(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
 static_assert(wait_vmcnt(0) == kWaitVmcnt0, "vmcnt(0) encoding");
 
-// Full-resolution position from which compressed key c may be attended (the
-// visibility rule of the forward): row p sees key c iff p >= tau(c).
-__device__ __forceinline__ int key_visible_from(int c, int P, int T, int nW, int w, int mode) {
-  if (c < P) return c;
-  if (c < P + nW) {
-    const int i = c - P;
-    if (mode == 1) return P + i * w;
-    return min(P + (i + 1) * w, P + T) - 1;
-  }
-  return P + T + (c - P - nW);
-}
-
 __device__ __forceinline__ float frag_dot(bf16x8_t x, bf16x8_t y) {
   float s = 0.f;
 #pragma unroll
@@ -74,7 +62,7 @@ __device__ __forceinline__ float frag_dot(float x, float y) { return x * y; }
 
 // ------------------------------------------------------------------ dQ
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool kRuns>
 __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_bwd_dq_kernel(PrefillBwdArgs a) {
   typedef Mfma<T> M;
   typedef typename M::Frag Frag;
@@ -102,16 +90,12 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_bwd_dq_kern
   const int g = (item / a.num_q_tiles) % heads;
   const int b = item / a.num_q_tiles / heads;
 
-  const int P = max(a.prefix_len[b], 0);
-  const int T_ = max(a.speech_len[b], 0);
-  const int N = max(a.suffix_len[b], 0);
-  const int w = a.w_eff;
-  const int nW = (T_ + w - 1) / w;
-  const int rows = min(P + T_ + N, a.q_len);
-  const int clen = min(P + nW + N, a.pv.max_pages << a.pv.page_shift);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
   if (p0 >= rows) return;
-  const int kmax = min(visible_keys(min(p0 + kRows, rows) - 1, P, T_, nW, w, a.mask_mode), clen);
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = g * G + wave % G;
@@ -119,7 +103,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_bwd_dq_kern
   const int wrow0 = p0 + (wave / G) * 32;
   const int p = wrow0 + col;
   const bool qvalid = p < rows;
-  const int nvis = qvalid ? min(visible_keys(p, P, T_, nW, w, a.mask_mode), clen) : 0;
+  const int nvis = qvalid ? min(sp.visible(p, a.mask_mode), clen) : 0;
   const int hq = a.num_q_heads;
   const int slot_mask = (1 << a.pv.page_shift) - 1;
 
@@ -328,7 +312,7 @@ struct KvBwdShape {
   static constexpr int kKeys = 32 * kWaves;  // keys per block, 32 per wave
 };
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool kRuns>
 __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv_kernel(PrefillBwdArgs a) {
   typedef Mfma<T> M;
   typedef typename M::Frag Frag;
@@ -371,13 +355,9 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
   const int g = (item / a.num_key_tiles) % heads;
   const int b = item / a.num_key_tiles / heads;
 
-  const int P = max(a.prefix_len[b], 0);
-  const int T_ = max(a.speech_len[b], 0);
-  const int N = max(a.suffix_len[b], 0);
-  const int w = a.w_eff;
-  const int nW = (T_ + w - 1) / w;
-  const int rows = min(P + T_ + N, a.q_len);
-  const int clen = min(min(P + nW + N, a.pv.max_pages << a.pv.page_shift), a.hat_cap);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(min(sp.clen(), a.pv.max_pages << a.pv.page_shift), a.hat_cap);
   const int kb0 = kt * kBlockKeys;
   if (kb0 >= clen) return;  // block-uniform
 
@@ -386,9 +366,9 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
   const int hq = a.num_q_heads;
   const int kb = kb0 + 32 * wave;  // this wave's keys
   const int key = kb + col;       // this lane's key (C-layout column)
-  const int tau = key < clen ? key_visible_from(key, P, T_, nW, w, a.mask_mode) : INT_MAX;
+  const int tau = key < clen ? sp.visible_from(key, a.mask_mode) : INT_MAX;
   // first row that sees a key of this wave (none: INT_MAX)
-  const int wave_from = kb < clen ? key_visible_from(kb, P, T_, nW, w, a.mask_mode) : INT_MAX;
+  const int wave_from = kb < clen ? sp.visible_from(kb, a.mask_mode) : INT_MAX;
 
   // this lane's K and V rows, the B operands of S = Q K^T and dP = dO V^T,
   // in registers for every step (a key past the compressed length or without
@@ -410,7 +390,7 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
 
   // query rows that see some key of the block: from tau(kb0) (tau grows with
   // c); one step per (query head, 32-row tile) pair
-  const int q_first = key_visible_from(kb0, P, T_, nW, w, a.mask_mode);
+  const int q_first = sp.visible_from(kb0, a.mask_mode);
   const int t0 = q_first / kQ, t1 = (rows + kQ - 1) / kQ;
   const int n_steps = max(t1 - t0, 0) * G;
 
@@ -545,15 +525,21 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
     }
 }
 
-template <typename T, int D, int G>
-hipError_t launch_bwd_g(const PrefillBwdArgs& a, int batch, hipStream_t s) {
+template <typename T, int D, int G, bool kRuns>
+hipError_t launch_bwd_r(const PrefillBwdArgs& a, int batch, hipStream_t s) {
   const unsigned qitems = (unsigned)(batch * a.pv.kv_heads * a.num_q_tiles);
-  hipError_t e = launch_struct(prefill_bwd_dq_kernel<T, D, G>, dim3(qitems),
+  hipError_t e = launch_struct(prefill_bwd_dq_kernel<T, D, G, kRuns>, dim3(qitems),
                                dim3(PrefillShape<G>::kThreads), s, a);
   if (e != hipSuccess) return e;
   const unsigned kitems = (unsigned)(batch * a.pv.kv_heads * a.num_key_tiles);
-  return launch_struct(prefill_bwd_dkdv_kernel<T, D, G>, dim3(kitems),
+  return launch_struct(prefill_bwd_dkdv_kernel<T, D, G, kRuns>, dim3(kitems),
                        dim3(KvBwdShape<T, D>::kThreads), s, a);
+}
+
+template <typename T, int D, int G>
+hipError_t launch_bwd_g(const PrefillBwdArgs& a, int batch, hipStream_t s) {
+  return a.segs.seg_start ? launch_bwd_r<T, D, G, true>(a, batch, s)
+                          : launch_bwd_r<T, D, G, false>(a, batch, s);
 }
 
 template <typename T, int D>

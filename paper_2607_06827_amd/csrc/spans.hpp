@@ -11,9 +11,9 @@
 //            sequence's segments.
 // A view answers: rows() and clen() (raw and compressed lengths), slot(c)
 // (first raw row and frame count of compressed slot c; one frame for a text
-// row) and visible(p, mode) (how many compressed keys row p sees: they are a
+// row), visible(p, mode) (how many compressed keys row p sees: they are a
 // prefix of the cache, as the position a key becomes visible at grows with
-// c).  Mask modes: 0 = a window is visible from its last frame, 1 = from its
+// c) and visible_from(c, mode) (that position).  Mask modes: 0 = a window is visible from its last frame, 1 = from its
 // first frame.
 #pragma once
 
@@ -43,6 +43,17 @@ __device__ __forceinline__ int visible_keys(int p, int P, int T, int nW, int w, 
   return P + nW + (t - T) + 1;
 }
 
+// Full-resolution row from which compressed key c of one run is visible.
+__device__ __forceinline__ int key_visible_from(int c, int P, int T, int nW, int w, int mode) {
+  if (c < P) return c;
+  if (c < P + nW) {
+    const int i = c - P;
+    if (mode == 1) return P + i * w;
+    return min(P + (i + 1) * w, P + T) - 1;
+  }
+  return P + T + (c - P - nW);
+}
+
 // Several speech runs per sequence (segments in a table).
 struct SegmentTable {
   const int32_t* seg_start = nullptr;   // [batch + 1]: sequence b owns segments [seg_start[b], seg_start[b+1])
@@ -68,6 +79,9 @@ struct OneRun {
   __device__ __forceinline__ SlotSource slot(int c) const { return SlotSource(c, P, T, nW, w); }
   __device__ __forceinline__ int visible(int p, int mode) const {
     return visible_keys(p, P, T, nW, w, mode);
+  }
+  __device__ __forceinline__ int visible_from(int c, int mode) const {
+    return key_visible_from(c, P, T, nW, w, mode);
   }
 };
 
@@ -150,6 +164,24 @@ struct Runs {
       cc += tl + nw;
     }
     return cc;
+  }
+
+  // row from which key c is visible (past the sequence: its row count)
+  __device__ __forceinline__ int visible_from(int c, int mode) const {
+    int r = 0, cc = 0;
+    for (int i = s0; i < s1; ++i) {
+      int tl, sl;
+      lengths(i, r, tl, sl);
+      const int nw = (sl + w - 1) / w;
+      if (c < cc + tl) return r + (c - cc);
+      if (c < cc + tl + nw) {
+        const int f = (c - cc - tl) * w;
+        return r + tl + (mode == 1 ? f : min(f + w, sl) - 1);
+      }
+      r += tl + sl;
+      cc += tl + nw;
+    }
+    return r;
   }
 };
 

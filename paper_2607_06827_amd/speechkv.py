@@ -91,12 +91,21 @@ _lib.speechkv_prefill_attn_bwd.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER
                                            ctypes.POINTER(_Spans), _i32, _i32, _i32, _i32, _f32,
                                            _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _sz, _vp]
 _lib.speechkv_prefill_attn_bwd.restype = ctypes.c_int
+_lib.speechkv_prefill_attn_bwd_segments.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_PagedKV),
+                                                    ctypes.POINTER(_Segments), _i32, _i32, _i32,
+                                                    _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
+                                                    _vp, _sz, _vp]
+_lib.speechkv_prefill_attn_bwd_segments.restype = ctypes.c_int
 _lib.speechkv_prefill_attn_bwd_workspace_bytes.argtypes = [_i32, _i32, _i32]
 _lib.speechkv_prefill_attn_bwd_workspace_bytes.restype = _sz
 _lib.speechkv_pool_kv_bwd.argtypes = [_vp, _vp, _i64, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
                                       ctypes.POINTER(_Spans), _i32, _vp, _i32, _i32, _vp, _vp, _i32,
                                       _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.speechkv_pool_kv_bwd.restype = ctypes.c_int
+_lib.speechkv_pool_kv_bwd_segments.argtypes = [_vp, _vp, _i64, _i64, _i64, _i32, _i32, _i32, _i32,
+                                               _i32, ctypes.POINTER(_Segments), _i32, _vp, _i32,
+                                               _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.speechkv_pool_kv_bwd_segments.restype = ctypes.c_int
 _lib.speechkv_pool_kv_bwd_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32]
 _lib.speechkv_pool_kv_bwd_workspace_bytes.restype = _sz
 _lib.speechkv_compressed_len.argtypes = [_i32] * 6
@@ -379,6 +388,25 @@ def speechkv_prefill_attn_bwd(q: torch.Tensor, cache: PagedKV, spans: Spans, w: 
                               scale: Optional[float] = None, stream=None) -> None:
     """q, out, dout, dq: [B, q_len, Hq, D]; lse: [B, Hq, q_len] fp32;
     dk_hat, dv_hat: [B, hat_capacity, Hkv, D] fp32; workspace: device bytes."""
+    _prefill_attn_bwd(_lib.speechkv_prefill_attn_bwd, "speechkv_prefill_attn_bwd", q, cache,
+                      spans, w, layer, l0, out, lse, dout, dq, dk_hat, dv_hat, workspace,
+                      mask_mode, scale, stream)
+
+
+def speechkv_prefill_attn_bwd_segments(q: torch.Tensor, cache: PagedKV, segs: Segments, w: int,
+                                       layer: int, l0: int, out: torch.Tensor, lse: torch.Tensor,
+                                       dout: torch.Tensor, dq: torch.Tensor, dk_hat: torch.Tensor,
+                                       dv_hat: torch.Tensor, workspace: torch.Tensor,
+                                       mask_mode: int = MASK_WINDOW_END,
+                                       scale: Optional[float] = None, stream=None) -> None:
+    """speechkv_prefill_attn_bwd for sequences given as segment tables."""
+    _prefill_attn_bwd(_lib.speechkv_prefill_attn_bwd_segments, "speechkv_prefill_attn_bwd_segments",
+                      q, cache, segs, w, layer, l0, out, lse, dout, dq, dk_hat, dv_hat, workspace,
+                      mask_mode, scale, stream)
+
+
+def _prefill_attn_bwd(fn, name, q, cache, spans, w, layer, l0, out, lse, dout, dq, dk_hat, dv_hat,
+                      workspace, mask_mode, scale, stream):
     for x in (q, out, dout, dq, lse, dk_hat, dv_hat, workspace):
         if not x.is_contiguous():
             raise ValueError("backward tensors must be contiguous")
@@ -391,13 +419,11 @@ def speechkv_prefill_attn_bwd(q: torch.Tensor, cache: PagedKV, spans: Spans, w: 
         scale = D ** -0.5
     c = cache._c()
     s = spans._c()
-    st = _lib.speechkv_prefill_attn_bwd(q.data_ptr(), B, Hq, q_len, ctypes.byref(c), ctypes.byref(s),
-                                        w, layer, l0, mask_mode, scale, out.data_ptr(),
-                                        lse.data_ptr(), dout.data_ptr(), dq.data_ptr(),
-                                        dk_hat.data_ptr(), dv_hat.data_ptr(), dk_hat.shape[1],
-                                        workspace.data_ptr(),
-                                        workspace.numel() * workspace.element_size(), _stream(stream))
-    _check(st, "speechkv_prefill_attn_bwd")
+    st = fn(q.data_ptr(), B, Hq, q_len, ctypes.byref(c), ctypes.byref(s), w, layer, l0, mask_mode,
+            scale, out.data_ptr(), lse.data_ptr(), dout.data_ptr(), dq.data_ptr(),
+            dk_hat.data_ptr(), dv_hat.data_ptr(), dk_hat.shape[1], workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, name)
 
 
 def speechkv_pool_kv_bwd_workspace_bytes(batch: int, max_total_len: int, num_kv_heads: int,
@@ -414,6 +440,23 @@ def speechkv_pool_kv_bwd(k_raw: torch.Tensor, v_raw: torch.Tensor, spans: Spans,
     """k_raw, v_raw, dk_raw, dv_raw: [B, S_raw, Hkv, D] with one stride and a
     contiguous last axis; dk_hat, dv_hat: [B, capacity, Hkv, D] fp32; du:
     [Hkv, D] fp32 or None."""
+    _pool_kv_bwd(_lib.speechkv_pool_kv_bwd, "speechkv_pool_kv_bwd", k_raw, v_raw, spans, w, gate_u,
+                 layer, l0, dk_hat, dv_hat, dk_raw, dv_raw, du, workspace, stream)
+
+
+def speechkv_pool_kv_bwd_segments(k_raw: torch.Tensor, v_raw: torch.Tensor, segs: Segments,
+                                  w: int, gate_u: Optional[torch.Tensor], layer: int, l0: int,
+                                  dk_hat: torch.Tensor, dv_hat: torch.Tensor,
+                                  dk_raw: torch.Tensor, dv_raw: torch.Tensor,
+                                  du: Optional[torch.Tensor] = None,
+                                  workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """speechkv_pool_kv_bwd for sequences given as segment tables."""
+    _pool_kv_bwd(_lib.speechkv_pool_kv_bwd_segments, "speechkv_pool_kv_bwd_segments", k_raw, v_raw,
+                 segs, w, gate_u, layer, l0, dk_hat, dv_hat, dk_raw, dv_raw, du, workspace, stream)
+
+
+def _pool_kv_bwd(fn, name, k_raw, v_raw, spans, w, gate_u, layer, l0, dk_hat, dv_hat, dk_raw,
+                 dv_raw, du, workspace, stream):
     for x in (v_raw, dk_raw, dv_raw):
         if x.shape != k_raw.shape or x.stride() != k_raw.stride() or x.dtype != k_raw.dtype:
             raise ValueError("k_raw, v_raw, dk_raw and dv_raw must share shape, stride and dtype")
@@ -426,12 +469,11 @@ def speechkv_pool_kv_bwd(k_raw: torch.Tensor, v_raw: torch.Tensor, spans: Spans,
     sb, ss, sh, _ = k_raw.stride()
     s = spans._c()
     ws = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    st = _lib.speechkv_pool_kv_bwd(k_raw.data_ptr(), v_raw.data_ptr(), sb, ss, sh, B, S, H, D,
-                                   _dtype_code(k_raw.dtype), ctypes.byref(s), w, _ptr(gate_u),
-                                   layer, l0, dk_hat.data_ptr(), dv_hat.data_ptr(), dk_hat.shape[1],
-                                   dk_raw.data_ptr(), dv_raw.data_ptr(), _ptr(du), _ptr(workspace),
-                                   ws, _stream(stream))
-    _check(st, "speechkv_pool_kv_bwd")
+    st = fn(k_raw.data_ptr(), v_raw.data_ptr(), sb, ss, sh, B, S, H, D, _dtype_code(k_raw.dtype),
+            ctypes.byref(s), w, _ptr(gate_u), layer, l0, dk_hat.data_ptr(), dv_hat.data_ptr(),
+            dk_hat.shape[1], dk_raw.data_ptr(), dv_raw.data_ptr(), _ptr(du), _ptr(workspace), ws,
+            _stream(stream))
+    _check(st, name)
 
 
 def speechkv_compressed_len(prefix_len: int, speech_len: int, suffix_len: int, w: int,

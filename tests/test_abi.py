@@ -28,7 +28,8 @@ def test_every_declared_symbol_is_exported():
     assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
                           "speechkv_pool_hidden", "speechkv_pool_prefill_attn",
                           "speechkv_pool_kv_segments", "speechkv_prefill_attn_segments",
-                          "speechkv_compressed_len_segments",
+                          "speechkv_compressed_len_segments", "speechkv_prefill_attn_bwd_segments",
+                          "speechkv_pool_kv_bwd_segments",
                           "speechkv_prefill_attn_bwd",
                           "speechkv_prefill_attn_bwd_workspace_bytes", "speechkv_pool_kv_bwd",
                           "speechkv_pool_kv_bwd_workspace_bytes",
@@ -422,3 +423,32 @@ def test_segment_calls_check_the_cache():
     assert pool_seg(c=cache(head_dim=96)) == E_UNS
     assert prefill_seg(c=cache(dtype=7)) == E_UNS
     assert pool_seg(c=cache(k_pages=None)) == E_ARG
+
+
+def test_backward_segment_calls_check_their_tables():
+    g = segments(seg_start=None)
+    ws = FAKE + (22 << 24)
+    st = lib.speechkv_prefill_attn_bwd_segments(FAKE + (15 << 24), 2, 4, 60, ctypes.byref(cache()),
+                                                ctypes.byref(g), 4, 1, 0, 0, 0.125, FAKE + (16 << 24),
+                                                FAKE + (17 << 24), FAKE + (18 << 24), FAKE + (19 << 24),
+                                                FAKE + (20 << 24), FAKE + (21 << 24), 60, ws, 1 << 20,
+                                                None)
+    assert st == E_ARG
+    st = lib.speechkv_pool_kv_bwd_segments(RAW, RAW + (1 << 22), 60 * 2 * 64, 2 * 64, 64, 2, 60, 2, 64,
+                                           skv.DTYPE_BF16, ctypes.byref(segments(max_segments=-1)), 4,
+                                           None, 1, 0, FAKE + (20 << 24), FAKE + (21 << 24), 60,
+                                           FAKE + (26 << 24), FAKE + (27 << 24), None, None, 0, None)
+    assert st == E_ARG
+    # a valid table with a broken cache or window is still rejected
+    st = lib.speechkv_prefill_attn_bwd_segments(FAKE + (15 << 24), 2, 4, 60,
+                                                ctypes.byref(cache(head_dim=96)),
+                                                ctypes.byref(segments()), 4, 1, 0, 0, 0.125,
+                                                FAKE + (16 << 24), FAKE + (17 << 24), FAKE + (18 << 24),
+                                                FAKE + (19 << 24), FAKE + (20 << 24), FAKE + (21 << 24),
+                                                60, ws, 1 << 20, None)
+    assert st == E_UNS
+    st = lib.speechkv_pool_kv_bwd_segments(RAW, RAW + (1 << 22), 60 * 2 * 64, 2 * 64, 64, 2, 60, 2, 64,
+                                           skv.DTYPE_BF16, ctypes.byref(segments()), 0, None, 1, 0,
+                                           FAKE + (20 << 24), FAKE + (21 << 24), 60, FAKE + (26 << 24),
+                                           FAKE + (27 << 24), None, None, 0, None)
+    assert st == E_ARG

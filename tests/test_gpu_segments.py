@@ -2,8 +2,10 @@
 pooling into the paged cache and the prefill attention, through the C ABI,
 against the fp64 multi-run oracle (oracle/segments.py), on adversarial
 shapes (empty segments, runs shorter than w, ragged last windows, text-only
-and speech-only sequences, many segments) and a multi-turn workload; and a
-table holding one run per sequence must give the bits of the one-run calls.
+and speech-only sequences, many segments) and a multi-turn workload; then
+the training backward of both (attention, then pooling down to the raw K/V
+and the gate) against the oracle's backward.  A table holding one run per
+sequence must give the bits of the one-run calls, forward and backward.
 """
 import math
 
@@ -13,7 +15,7 @@ import torch
 
 import oracle
 from oracle import segments as seg
-from helpers import TOL, f64, gather, rel_err
+from helpers import GRAD_TOL, TOL, f64, gather, grad_err, rel_err
 from paper_2607_06827_amd import inputs
 from paper_2607_06827_amd import speechkv as skv
 
@@ -194,3 +196,126 @@ def test_multi_turn_workload():
     segs[3] = [(32, 375), (64, 0)]          # one turn only
     segs[7] = [(0, 500), (24, 250), (8, 0)]  # speech first
     check(segs, Hq=16, Hkv=8, D=128, seed=3)
+
+
+# ------------------------------------------------------------------ backward
+
+BWD_CASES = {
+    "three-turns-d128": dict(segs=[[(8, 60), (5, 33), (6, 0)], [(0, 41), (2, 9)]], D=128),
+    "turns-varlen-g4": dict(segs=[[(4, 17), (2, 9), (0, 30), (7, 0)], [(1, 2), (1, 3), (1, 5), (2, 0)]],
+                            Hq=8, Hkv=2, D=128),
+    "window-start-w5": dict(segs=[[(3, 41), (2, 30), (7, 0)]], mode=1, w=5, D=64),
+    "w16": dict(segs=[[(3, 70), (5, 37), (2, 0)]], w=16, D=128),
+    "fp32": dict(segs=[[(8, 60), (5, 33), (6, 0)], [(0, 17), (2, 0)]], dtype="f32"),
+    "identity-below-l0": dict(segs=[[(6, 50), (3, 20), (4, 0)]], layer=2, l0=5, D=128),
+}
+
+
+def run_backward(segs, w=4, layer=1, l0=0, mode=0, **kw):
+    x = build(segs, w=w, layer=layer, l0=l0, **kw)
+    clen, out, lse = run_segments(x, segs, w, layer, l0, mode)
+    B, S = x["B"], x["S"]
+    Hq, D = x["q"].shape[2], x["q"].shape[3]
+    Hkv = x["k"].shape[2]
+    dev = torch.device("cuda")
+    dout = inputs.normal((B, S, Hq, D), 5200, dtype=x["dt"]).to(dev)
+    for b, R in enumerate(x["rows"]):
+        dout[b, R:] = 0
+    cap = max(clen) + 2
+    dq = torch.full_like(out, float("nan"))
+    dkh = torch.full((B, cap, Hkv, D), float("nan"), dtype=torch.float32, device=dev)
+    dvh = torch.full_like(dkh, float("nan"))
+    ws = torch.empty(skv.speechkv_prefill_attn_bwd_workspace_bytes(B, Hq, S), dtype=torch.uint8,
+                     device=dev)
+    skv.speechkv_prefill_attn_bwd_segments(x["q"].cuda(), x["cache"], x["segs"], w, layer, l0, out,
+                                           lse, dout, dq, dkh, dvh, ws, mask_mode=mode,
+                                           scale=D ** -0.5)
+    k, v = x["k"].cuda(), x["v"].cuda()
+    dkr = torch.full_like(k, float("nan"))
+    dvr = torch.full_like(v, float("nan"))
+    du = torch.full((Hkv, D), float("nan"), dtype=torch.float32, device=dev)
+    nb = skv.speechkv_pool_kv_bwd_workspace_bytes(B, x["segs"].max_total_len, Hkv, D)
+    pws = torch.empty(max(nb, 16), dtype=torch.uint8, device=dev)
+    u = None if x["u"] is None else x["u"].cuda()
+    # the pooling backward from the attention's key gradients (rows past the
+    # compressed lengths are zero: they reach no raw row)
+    dkh_in, dvh_in = torch.nan_to_num(dkh, nan=0.0), torch.nan_to_num(dvh, nan=0.0)
+    skv.speechkv_pool_kv_bwd_segments(k, v, x["segs"], w, u, layer, l0, dkh_in, dvh_in, dkr, dvr,
+                                      du, pws)
+    torch.cuda.synchronize()
+    return x, clen, dout, dict(dq=dq, dkh=dkh, dvh=dvh, dkr=dkr, dvr=dvr, du=du, dkh_in=dkh_in,
+                               dvh_in=dvh_in)
+
+
+@pytest.mark.parametrize("name", sorted(BWD_CASES))
+def test_segments_backward_matches_oracle(name):
+    print(f"case {name}", flush=True)
+    kw = dict(BWD_CASES[name])
+    segs = kw.pop("segs")
+    w, layer, l0, mode = kw.get("w", 4), kw.get("layer", 1), kw.get("l0", 0), kw.get("mode", 0)
+    x, clen, dout, g = run_backward(segs, **kw)
+    D = x["q"].shape[3]
+    tol = GRAD_TOL["bf16" if x["dt"] == torch.bfloat16 else "f32"]
+    # attention backward: the oracle on the GPU's cache rows (what the kernel reads)
+    Lmax = max(max(clen), 1)
+    kh = np.zeros((x["B"], Lmax) + tuple(x["k"].shape[2:]))
+    vh = np.zeros_like(kh)
+    for b, L in enumerate(clen):
+        if L:
+            gk, gv = gather(x["cache"], b, L)
+            kh[b, :L], vh[b, :L] = f64(gk), f64(gv)
+    rq, rk, rv = seg.attention_bwd(f64(x["q"]), kh, vh, segs, w, layer, l0, f64(dout), mode,
+                                   D ** -0.5)
+    for b, (L, R) in enumerate(zip(clen, x["rows"])):
+        if R:
+            assert grad_err(f64(g["dq"][b, :R]), rq[b, :R]) <= tol["dq"]
+        if L:
+            assert grad_err(f64(g["dkh"][b, :L]), rk[b, :L]) <= tol["dkv_hat"]
+            assert grad_err(f64(g["dvh"][b, :L]), rv[b, :L]) <= tol["dkv_hat"]
+    # pooling backward: the oracle on the same raw K/V, gate and fp32 key gradients
+    u64 = None if x["u"] is None else f64(x["u"])
+    pk, pv, pu = seg.pool_bwd(f64(x["k"]), f64(x["v"]), segs, w, layer, l0, u64,
+                              f64(g["dkh_in"]), f64(g["dvh_in"]))
+    for b, R in enumerate(x["rows"]):
+        if R:
+            assert grad_err(f64(g["dkr"][b, :R]), pk[b, :R]) <= tol["dkv_raw"]
+            assert grad_err(f64(g["dvr"][b, :R]), pv[b, :R]) <= tol["dkv_raw"]
+        if R < x["S"]:
+            assert torch.isnan(g["dkr"][b, R:]).all()
+    assert grad_err(f64(g["du"]), pu) <= tol["du"]
+
+
+def test_one_run_table_backward_equals_one_run_calls():
+    """{(P, T), (N, 0)} per sequence: the backward calls give the bits of the
+    one-run backward calls."""
+    P, T, N, w = [8, 0, 5], [60, 37, 0], [5, 3, 9], 4
+    segs = [[(p, t), (n, 0)] for p, t, n in zip(P, T, N)]
+    x, clen, dout, g = run_backward(segs, D=128, Hq=8, Hkv=2)
+    B, S = x["B"], x["S"]
+    Hq, D, Hkv = 8, 128, 2
+    i32 = lambda v: torch.tensor(v, dtype=torch.int32, device="cuda")
+    spans = skv.Spans(i32(P), i32(T), i32(N), max(T), max(p + t + n for p, t, n in zip(P, T, N)))
+    out = torch.empty(B, S, Hq, D, dtype=x["dt"], device="cuda")
+    lse = torch.empty(B, Hq, S, dtype=torch.float32, device="cuda")
+    skv.speechkv_prefill_attn(x["q"].cuda(), x["cache"], spans, w, 1, 0, out, scale=D ** -0.5, lse=lse)
+    dq = torch.full_like(out, float("nan"))
+    dkh = torch.full_like(g["dkh"], float("nan"))
+    dvh = torch.full_like(dkh, float("nan"))
+    ws = torch.empty(skv.speechkv_prefill_attn_bwd_workspace_bytes(B, Hq, S), dtype=torch.uint8,
+                     device="cuda")
+    skv.speechkv_prefill_attn_bwd(x["q"].cuda(), x["cache"], spans, w, 1, 0, out, lse, dout, dq,
+                                  dkh, dvh, ws, scale=D ** -0.5)
+    k, v = x["k"].cuda(), x["v"].cuda()
+    dkr, dvr = torch.full_like(k, float("nan")), torch.full_like(v, float("nan"))
+    du = torch.empty(Hkv, D, dtype=torch.float32, device="cuda")
+    nb = skv.speechkv_pool_kv_bwd_workspace_bytes(B, spans.max_total_len, Hkv, D)
+    pws = torch.empty(max(nb, 16), dtype=torch.uint8, device="cuda")
+    skv.speechkv_pool_kv_bwd(k, v, spans, w, x["u"].cuda(), 1, 0, g["dkh_in"], g["dvh_in"], dkr,
+                             dvr, du, pws)
+    torch.cuda.synchronize()
+    for b in range(B):
+        R, L = x["rows"][b], clen[b]
+        assert torch.equal(dq[b, :R], g["dq"][b, :R])
+        assert torch.equal(dkh[b, :L], g["dkh"][b, :L]) and torch.equal(dvh[b, :L], g["dvh"][b, :L])
+        assert torch.equal(dkr[b, :R], g["dkr"][b, :R]) and torch.equal(dvr[b, :R], g["dvr"][b, :R])
+    assert torch.equal(du, g["du"])
