@@ -318,10 +318,21 @@ def cpu_baseline(job, budget_s=15.0):
         "value": seqs * wl.decode_steps / spent,
         "unit": "tokens/s",
         "cores": oracle.num_threads(),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": (f"{seqs} of {wl.batch} sequences, whole job (28 layers: pool, prefill "
                    f"attention, {wl.decode_steps} decode steps), fp64, {spent:.1f} s"),
     }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
