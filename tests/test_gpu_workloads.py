@@ -4,7 +4,8 @@ tiny fp32 (1 layer, b=1), 30 s layer (b=32) and prefill (b=8, 1596 queries
 over 471 keys) are checked on every output; the 28-layer 60 s stack (b=64) and
 the 10-minute decode (b=16, w in {2,4,8}) are run whole, in the launch
 configuration the benchmark times, and checked on sampled (layer, step,
-sequence) outputs the oracle computes one by one.
+sequence) outputs the oracle computes one by one; the 10-minute prefill
+(7532 rows) on two whole sequences of a full and a pooled layer.
 """
 import numpy as np
 import pytest
@@ -127,3 +128,19 @@ def test_long_10min_sampled(w):
             check_decode(job, i, b, (0, 127, 255), errs)
         check_pool(job, i, [9], errs)
     assert_ok(errs, TOL["bf16"], f"{wl.name}-w{w}")
+
+
+def test_long_10min_prefill_sampled():
+    """Prefill at the 10-minute workload's full size (b=16, 32 + 7500 rows,
+    w=4): a full layer (7532 keys, causal) and a pooled layer (1907 keys), in
+    the launch configuration the benchmark uses, checked on two whole
+    sequences against the oracle."""
+    wl = inputs.LONG_10MIN.with_(decode_steps=0)
+    job = Job(wl, layers=[0, 14])
+    errs = []
+    for l in (0, 14):
+        job.run_prefill(layers=[l])
+        torch.cuda.synchronize()
+        check_prefill(job, job.layers.index(l), [0, 15], errs)
+        check_pool(job, job.layers.index(l), [15], errs)
+    assert_ok(errs, TOL["bf16"], f"{wl.name}-prefill")
