@@ -8,7 +8,8 @@
 //   dk_j     = alpha_j dK^_i + ds_j u_g,    dv_j = alpha_j dV^_i
 //   du_g    += ds_j k_j                    (over every sequence and window)
 // A text row (or a one-frame window) was copied, so its gradient is that of
-// the row it became.
+// the row it became.  The slots' source rows come from the span view
+// (spans.hpp): one run per sequence, or the runs of a segment table (kRuns).
 //
 // Layout: each thread owns 8 consecutive elements of one KV head; D/8 threads
 // cover a head, kv_heads * D/8 a slot of the compressed sequence, and a block

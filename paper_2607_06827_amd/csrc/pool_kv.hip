@@ -9,6 +9,9 @@
 //   slot P + i, i < nW         softmax-of-gate-logits weighted sum over the
 //                              window [P + i*w, min(P + (i+1)*w, P + T))
 //   slot P + nW + m            copy raw row P + T + m                (bitwise)
+// For sequences with several speech runs (kRuns, a segment table) the slots
+// follow the segments in order, each run with its own windows; the span view
+// (spans.hpp) gives every slot's source rows either way.
 // The gate logit u_g . k_j is a 16-lane (8-lane for D = 64) DPP reduction.
 // The window softmax is computed online over groups of four frames so that
 // eight loads are in flight per lane; a one-frame window is a copy.  The

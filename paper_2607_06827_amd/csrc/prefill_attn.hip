@@ -8,7 +8,9 @@
 // frame (WINDOW_START), suffix key m at P + T + m.  tau is increasing, so row
 // p sees the prefix [0, n_vis(p)) of the cache: a query tile needs only the
 // key tiles below n_vis of its last row, and only the tiles that straddle the
-// n_vis of some row of a wave are masked element by element.
+// n_vis of some row of a wave are masked element by element.  With several
+// speech runs per sequence (kRuns) the same holds run by run, and n_vis comes
+// from a scan of the sequence's segments (spans.hpp).
 //
 // Tiling (wave64, 32x32 MFMA).  A block owns one (sequence, KV head) and 32*RB
 // query rows for all G query heads of the group (G*RB waves, RB = max(1, 4/G)),

@@ -33,6 +33,8 @@
 //   starting S and dP from -LSE/scale and -Delta of their rows.
 // All products run on the 32x32 MFMAs (bf16 operands with P and dZ rounded to
 // bf16, or fp32), accumulating in fp32; dK^ and dV^ are written in fp32.
+// The mask's visibility rule comes from the span view (spans.hpp): one run
+// per sequence, or the runs of a segment table (kRuns).
 #include <climits>
 #include <type_traits>
 
