@@ -272,7 +272,15 @@ struct QTile {
   static constexpr int kRowsPerLoad = 64 / kChunks;         // rows per wave-wide load
   static constexpr int kLoads = 32 / kRowsPerLoad;          // wave-wide loads per tile
   static constexpr int kElems = 32 * D;
-  static __device__ __forceinline__ int swz(int r) { return r & (kChunks >= 16 ? 15 : kChunks - 1); }
+  // XOR swizzle of the 16-byte chunks of row r.  With 16 chunks per row
+  // (bf16, D = 128) the tile is read both row-wise (A operands: 16 rows x one
+  // chunk per pass) and transposed (ds_read_b64_tr_b16: 4 rows x 4 chunks per
+  // 32 lanes); ((r & 3) << 2) | ((r >> 2) & 3) gives distinct chunk positions
+  // to both patterns (a plain r & 15 folds the transposed one onto 4 chunks).
+  static __device__ __forceinline__ int swz(int r) {
+    if constexpr (kChunks == 16) return ((r & 3) << 2) | ((r >> 2) & 3);
+    return r & (kChunks >= 16 ? 15 : kChunks - 1);
+  }
   // element e of row r
   static __device__ __forceinline__ int at(int r, int e) {
     return r * D + (((e / kElems16) ^ swz(r)) * kElems16) + (e % kElems16);
