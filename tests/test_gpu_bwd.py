@@ -72,8 +72,11 @@ def attention_bwd(case, x, out, lse, dout, cap):
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_attention_bwd_matches_oracle(name):
-    case = CASES[name]
     print(f"case {name}", flush=True)
+    check_attention_bwd(CASES[name])
+
+
+def check_attention_bwd(case):
     x = build(case)
     B, Hq, Hkv, D = case.B, case.Hq, case.Hkv, case.D
     out, lse = forward(case, x)
@@ -123,8 +126,11 @@ def pool_bwd(case, x, dkh, dvh, with_du=True):
 
 @pytest.mark.parametrize("name", list(POOL_CASES))
 def test_pool_bwd_matches_oracle(name):
-    case = POOL_CASES[name]
     print(f"case {name}", flush=True)
+    check_pool_bwd(POOL_CASES[name])
+
+
+def check_pool_bwd(case):
     x = build(case)
     B, Hkv, D = case.B, case.Hkv, case.D
     cap = max(x["clen"]) + 2

@@ -251,7 +251,11 @@ def run_backward(segs, w=4, layer=1, l0=0, mode=0, **kw):
 def test_segments_backward_matches_oracle(name):
     print(f"case {name}", flush=True)
     kw = dict(BWD_CASES[name])
-    segs = kw.pop("segs")
+    check_backward(kw.pop("segs"), **kw)
+
+
+def check_backward(segs, **kw):
+    """Both backward calls on segment tables against the multi-run oracle."""
     w, layer, l0, mode = kw.get("w", 4), kw.get("layer", 1), kw.get("l0", 0), kw.get("mode", 0)
     x, clen, dout, g = run_backward(segs, **kw)
     D = x["q"].shape[3]
