@@ -11,11 +11,12 @@
 // log-sum-exp reduction in fixed split order.
 //
 // Key ranges are cut from the host-known bound on the cache length, so the
-// block-table entries, the queries, the cache length and the new token's K/V
-// are all requested at once and the first K/V loads wait on a single memory
-// round trip.  The wave's table entries sit one per lane and are read back
-// with readlane, so every load address is a wave-uniform page base (SGPRs)
-// plus a fixed 32-bit per-lane offset.
+// first K/V loads wait only on the block-table entries: the first batches
+// are requested from the bound before the device cache length arrives, and
+// the queries and the new token's K/V go out behind them.  The wave's table
+// entries sit one per lane and are read back with readlane, so every load
+// address is a wave-uniform page base (SGPRs) plus a fixed 32-bit per-lane
+// offset.
 //
 // Lane layout: kLanes = D/8 lanes per key row, 8 elements (16 bytes of bf16,
 // 32 of fp32) per lane, so kRows = 64 / kLanes consecutive keys of one page
@@ -41,8 +42,7 @@
 // waves' states merge through LDS in one step.
 //
 // If k_new/v_new are given, the wave whose range holds slot L-1 stores them
-// there as soon as the page is known, and that key is read from k_new/v_new
-// directly.  The kernel moves each K/V byte once: it is bound by HBM
+// there after its stream, and that key is read from k_new/v_new directly.  The kernel moves each K/V byte once: it is bound by HBM
 // bandwidth.
 #include "kernels.hpp"
 
@@ -406,6 +406,7 @@ __device__ __forceinline__ void sum_rows(float* l, float (*acc)[E]) {
 #define SKV_DECODE_DEPTH 2
 #endif
 constexpr int kDepth = SKV_DECODE_DEPTH;  // load batches in flight per wave
+static_assert(kDepth >= 2, "the stream keeps at least one batch in flight");
 
 template <typename T, int D, int G, int NW, int U, int E>
 __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(DecodeArgs a) {
@@ -438,20 +439,20 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   const int g_begin = min(s_begin + wave * per_wave, s_end);
   const int g_end = min(s_end, g_begin + per_wave);
 
-  // independent prologue loads: cache length, queries, block-table entries
-  const int L = min(max(a.cache_len[b], 0), cap);
+  // Prologue.  Only the block-table entries gate the first K/V loads: the
+  // first kDepth - 1 batches are requested from the host bound before the
+  // cache length arrives (when the length is below the bound, those that turn
+  // out to lie past the unmasked range are simply never reduced), and the
+  // queries, the new token's K/V and the masked tail follow them.
   const int first_page = (g_begin * kRows) >> shift;
   const int32_t* table = a.table + (int64_t)b * a.pv.max_pages;
   int tbl = -1;
   if (g_begin < g_end && first_page + lane < a.pv.max_pages) tbl = table[first_page + lane];
+  const int L = min(max(a.cache_len[b], 0), cap);
   const int64_t num_pages = a.pv.num_pages;
   auto checked = [num_pages](int page) { return (page >= 0 && page < num_pages) ? page : -1; };
-  tbl = checked(tbl);
 
   W st;
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-    st.qs[h].q.load(static_cast<const T*>(a.q) + ((int64_t)b * hq + g * G + h) * D, j);
   st.scale_log2 = a.scale_log2;
   st.lane = lane;
   st.init();
@@ -459,19 +460,9 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   T* kpool = static_cast<T*>(a.k_pages);
   T* vpool = static_cast<T*>(a.v_pages);
   const bool has_new = a.k_new != nullptr;
-  const int last = L - 1;
   const int64_t new_row = ((int64_t)b * heads + g) * D;
   // byte offset of this lane's first piece inside a group (consecutive rows)
   uint32_t lane_off = (uint32_t)((r * D + R::elem(0, j, 0)) * sizeof(T));
-
-  // lanes of row 0 of the wave whose range holds slot L-1 will store the new
-  // token's K/V; request it with the other prologue loads
-  const bool stores_new = has_new && L > 0 && g_begin * kRows <= last && last < g_end * kRows && r == 0;
-  R kn, vn;
-  if (stores_new) {
-    kn.load(static_cast<const T*>(a.k_new) + new_row, j);
-    vn.load(static_cast<const T*>(a.v_new) + new_row, j);
-  }
 
   // page of group grp (wave-uniform), or -1 when the table entry is bad
   auto group_page = [&](int grp) -> int {
@@ -483,12 +474,6 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   auto group_base = [&](int page, int grp) -> int64_t {
     return ((((int64_t)page * heads + g) << shift) + ((grp * kRows) & slot_mask)) * D;
   };
-
-  // keys [0, Lc) come from the cache; with k_new, key L-1 comes from k_new
-  const int Lc = has_new ? max(L - 1, 0) : L;
-  // groups wholly inside [0, Lc) take the unmasked path, U at a time
-  const int g_full = max(g_begin, min(g_end, Lc / kRows));
-  const int nbatch = (g_full - g_begin) / U;
 
   auto issue_full = [&](int gs, R* kc, R* vc) -> bool {
     bool ok = true;
@@ -507,6 +492,53 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
     }
     return ok;
   };
+
+  // Software pipeline over the nbatch unmasked batches, kDepth buffers deep:
+  // while batch k is reduced, batches k+1 .. k+kDepth-1 are in flight.  The
+  // steady-state loop issues unconditionally (so the wait before each
+  // reduction covers only the batch being reduced); buffer indices are
+  // compile-time constants throughout, so the buffers stay in registers.
+  R kb[kDepth][U], vb[kDepth][U];
+  tbl = checked(tbl);
+  // The block-table entries are needed before the first batch anyway;
+  // waiting for them here once keeps the compiler from re-waiting on them,
+  // conservatively, at the head of every loop iteration.  (The cache length
+  // is a scalar load with a counter of its own: it stays in flight.)
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+
+  // The first batches, from the host bound: groups wholly below its last
+  // unmasked key.  With the device length L <= bound, every batch the stream
+  // below reduces among them is one of these.
+  const int bound_unmasked = has_new ? max(cap - 1, 0) : cap;
+  const int nbatch_bound = (max(g_begin, min(g_end, bound_unmasked / kRows)) - g_begin) / U;
+  bool ok_first[kDepth - 1];
+#pragma unroll
+  for (int d = 0; d < kDepth - 1; ++d)
+    ok_first[d] = d < nbatch_bound ? issue_full(g_begin + d * U, kb[d], vb[d]) : true;
+
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+    st.qs[h].q.load(static_cast<const T*>(a.q) + ((int64_t)b * hq + g * G + h) * D, j);
+
+  // keys [0, Lc) come from the cache; with k_new, key L-1 comes from k_new
+  const int last = L - 1;
+  const int Lc = has_new ? max(L - 1, 0) : L;
+  // groups wholly inside [0, Lc) take the unmasked path, U at a time
+  const int g_full = max(g_begin, min(g_end, Lc / kRows));
+  const int nbatch = (g_full - g_begin) / U;
+  bool all_ok = true;
+#pragma unroll
+  for (int d = 0; d < kDepth - 1; ++d)
+    if (d < nbatch) all_ok = all_ok && ok_first[d];
+
+  // lanes of row 0 of the wave whose range holds slot L-1 store the new
+  // token's K/V there after the stream
+  const bool stores_new = has_new && L > 0 && g_begin * kRows <= last && last < g_end * kRows && r == 0;
+  R kn, vn;
+  if (stores_new) {
+    kn.load(static_cast<const T*>(a.k_new) + new_row, j);
+    vn.load(static_cast<const T*>(a.v_new) + new_row, j);
+  }
 
   // Masked batch starting at group gs: keys >= L (and groups past the tail)
   // are invalid; key L-1 comes from k_new when given.
@@ -544,39 +576,13 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
     }
   };
 
-  // Software pipeline over the nbatch unmasked batches, kDepth buffers deep:
-  // while batch k is reduced, batches k+1 .. k+kDepth-1 are in flight.  The
-  // steady-state loop issues unconditionally (so the wait before each
-  // reduction covers only the batch being reduced); buffer indices are
-  // compile-time constants throughout, so the buffers stay in registers.
-  R kb[kDepth][U], vb[kDepth][U];
-  bool all_ok = true;
-  // The prologue loads (block-table entries, queries) are needed before the
-  // first batch anyway; waiting for them here once keeps the compiler from
-  // re-waiting on them, conservatively, at the head of every loop iteration.
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-
-  // The wave holding slot L-1 stores the newest token's K/V there (loaded in
-  // the prologue); no load of this launch reads that slot from the cache (key
-  // L-1 comes from k_new), so the store can go out at once.
-  if (stores_new) {
-    const int page = group_page(last / kRows);
-    if (page >= 0) {
-      const int64_t off = group_base(page, last / kRows) + (int64_t)(last % kRows) * D;
-      kn.store(kpool + off, j);
-      vn.store(vpool + off, j);
-    }
-  }
   // The masked tail (at most U groups: the leftover full groups of the
-  // batching plus the one group holding key L-1) is loaded now, beside the
-  // first full batch, so that its round trip is not added after the stream.
+  // batching plus the one group holding key L-1) is requested now, so that
+  // its round trip is not added after the stream.
   const int tail_begin = g_begin + nbatch * U;
   R kt[U], vt[U];
   bool tvalid[U];
   load_masked(tail_begin, kt, vt, tvalid);
-#pragma unroll
-  for (int d = 0; d < kDepth - 1; ++d)
-    if (d < nbatch) all_ok = issue_full(g_begin + d * U, kb[d], vb[d]) && all_ok;
   int bi = 0;
   for (; bi + 2 * kDepth - 2 < nbatch; bi += kDepth) {
 #pragma unroll
@@ -596,6 +602,16 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
         all_ok = issue_full(g_begin + (bi + d + kDepth - 1) * U, kb[(d + kDepth - 1) % kDepth],
                             vb[(d + kDepth - 1) % kDepth]) && all_ok;
       st.template consume<U, false>(kb[d % kDepth], vb[d % kDepth], nullptr);
+    }
+  }
+  // The wave holding slot L-1 stores the newest token's K/V there; no load
+  // of this launch reads that slot from the cache (key L-1 comes from k_new).
+  if (stores_new) {
+    const int page = group_page(last / kRows);
+    if (page >= 0) {
+      const int64_t off = group_base(page, last / kRows) + (int64_t)(last % kRows) * D;
+      kn.store(kpool + off, j);
+      vn.store(vpool + off, j);
     }
   }
   // A block-table entry out of range (a caller error) was read as page 0:

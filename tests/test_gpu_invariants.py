@@ -3,7 +3,8 @@
 - decode output does not depend on the split count (and equals the oracle);
 - V == 1 gives O == 1 on every row that sees a key;
 - a decode step equals the prefill row of the same query at the same position;
-- page placement changes nothing (shuffled vs identity block tables);
+- page placement changes nothing (shuffled vs identity block tables), nor do
+  block-table entries past a sequence's last page;
 - repeated runs are bit-for-bit identical;
 - invalid calls with real device buffers return their error and write nothing.
 """
@@ -118,6 +119,44 @@ def test_page_placement_does_not_matter():
         kb, vb = gather(b["cache"], s, b["clen"][s])
         assert torch.equal(ka, kb) and torch.equal(va, vb)
     assert torch.equal(pa, pb) and torch.equal(da, db)
+
+
+def test_table_entries_past_a_sequence_do_not_matter():
+    """Decode over sequences of unequal length reads no block-table entry past
+    a sequence's last page: with those entries out of range (-1, or an id past
+    the pool) every split count gives the bits of the run with a full table,
+    also when the call appends the new token's K/V."""
+    x = setup()
+    pool(x)
+    cache = x["cache"]
+    ps, total = cache.k_pages.shape[2], cache.k_pages.shape[0]
+    lens = x["clen"]
+    B, Hq, Hkv, D = x["B"], x["Hq"], x["Hkv"], x["D"]
+    q = x["q"][:, 2].contiguous()
+    kn = inputs.normal((B, Hkv, D), 71, dtype=x["dtype"]).to(DEV)
+    vn = inputs.normal((B, Hkv, D), 72, dtype=x["dtype"]).to(DEV)
+    cut = cache.block_table.clone()
+    for b, L in enumerate(lens):
+        cut[b, -(-(L + 1) // ps):] = -1 if b % 2 == 0 else total + 5
+    assert (cut < 0).any() and (cut >= total).any()
+
+    def run(table, splits, append):
+        c = skv.PagedKV(cache.k_pages, cache.v_pages, table)
+        n = [L + 1 for L in lens] if append else lens
+        out = torch.zeros(B, Hq, D, dtype=x["dtype"], device=DEV)
+        nb = skv.speechkv_decode_workspace_bytes(B, Hq, Hkv, D, max(n), splits)
+        ws = torch.empty(max(nb, 16) // 4 + 4, dtype=torch.float32, device=DEV)
+        skv.speechkv_decode_attn(q, c, torch.tensor(n, dtype=torch.int32, device=DEV), max(n), out,
+                                 k_new=kn if append else None, v_new=vn if append else None,
+                                 num_splits=splits, workspace=ws)
+        return out
+
+    for splits in (0, 1, 3):
+        for append in (False, True):
+            full, part = run(cache.block_table, splits, append), run(cut, splits, append)
+            torch.cuda.synchronize()
+            assert torch.equal(full, part), (splits, append)
+            assert torch.isfinite(full.float()).all()
 
 
 def test_runs_are_bitwise_repeatable():
