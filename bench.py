@@ -14,7 +14,8 @@ full resolution) is measured beside it.
 
 Also reported: the decode kernel's achieved HBM bandwidth against the 8 TB/s
 peak (algorithmic bytes: every cached K/V row once, plus q, the new K/V and
-the output); the pooling kernel's achieved HBM bandwidth (raw K/V read once,
+the output) and against the attainable rate of a plain streaming read of the
+same byte counts, measured in the same run; the pooling kernel's achieved HBM bandwidth (raw K/V read once,
 cache rows written once) and the prefill attention's achieved bf16 TFLOP/s
 against the 2.5 PFLOP/s dense MFMA peak (FLOPs of the visible (row, key) pairs
 only), each from a graph of that kernel alone; HS Compression's pooling of
@@ -108,6 +109,58 @@ def decode_launch_stats(job):
     total = sum(job.decode_bytes(s) for s in range(job.wl.decode_steps))
     launches = job.wl.decode_steps * len(job.layers)
     return total, launches
+
+
+# (blocks, threads, loads in flight per buffer): the fastest of a sweep over
+# 256..8192 blocks x 256..1024 threads x 1..8 loads at both launch sizes
+STREAM_SHAPES = ((8192, 256, 1), (8192, 256, 2), (8192, 512, 1), (8192, 512, 2), (4096, 256, 2),
+                 (4096, 512, 2), (1024, 1024, 4), (512, 512, 2))
+
+
+def stream_ceiling(job, reps=3, copies=14):
+    """Attainable HBM read rate for the decode launches of one step: a plain
+    non-temporal streaming read of two buffers (bench-only kernel,
+    libskv_bench.so) at the average K+V size of a pooled-layer and of a
+    full-layer launch, best of a few launch shapes, rotating `copies` buffer
+    pairs so the 256 MB last-level cache holds none of them.  Each launch of
+    the step is then priced at its class's rate."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_06827_amd", "libskv_bench.so"))
+    f = lib.skv_stream_read
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                  ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    f.restype = ctypes.c_int
+    wl = job.wl
+    classes = {}
+    for i, l in enumerate(job.layers):
+        key = "pooled" if l >= job.l0 else "full"
+        classes.setdefault(key, []).extend(job.decode_bytes_layer(i, s) for s in range(wl.decode_steps))
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    rates = {}
+    for key, sizes in classes.items():
+        half = int(sum(sizes) / len(sizes) / 2) // 1024 * 1024
+        bufs = [(torch.empty(half, dtype=torch.uint8, device="cuda"),
+                 torch.empty(half, dtype=torch.uint8, device="cuda")) for _ in range(copies)]
+        best = 0.0
+        for blocks, threads, depth in STREAM_SHAPES:
+            def run():
+                st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+                for a, b in bufs:
+                    rc = f(a.data_ptr(), b.data_ptr(), half, blocks, threads, depth, sink.data_ptr(), st)
+                    if rc:
+                        raise RuntimeError(f"skv_stream_read failed ({rc})")
+            ms = time_graph(capture(run), reps) / copies
+            best = max(best, 2 * half / (ms * 1e-3) / 1e9)
+        rates[key] = best
+        del bufs
+        torch.cuda.empty_cache()
+    total = sum(sum(v) for v in classes.values())
+    seconds = sum(sum(v) / (rates[k] * 1e9) for k, v in classes.items())
+    return {"gbps": total / seconds / 1e9,
+            "pooled_launch_gbps": rates.get("pooled"), "full_launch_gbps": rates.get("full"),
+            "probe": f"non-temporal streaming read of two buffers, best of {len(STREAM_SHAPES)} launch "
+                     f"shapes, {copies} rotated buffer pairs"}
 
 
 def measure(job, steps, warmup, label):
@@ -441,6 +494,8 @@ def main():
     dec_bytes, launches = decode_launch_stats(job)
     avg_launch_ms = pooled["decode_ms"] / launches
     achieved = dec_bytes / launches / (avg_launch_ms * 1e-3) / 1e9
+    log("measuring the attainable streaming-read rate")
+    ceiling = stream_ceiling(job)
     result = {
         "metric": METRIC,
         "value": pooled["tokens_per_s"],
@@ -464,7 +519,8 @@ def main():
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(),
                      "kernel": "decode_kernel (+ split merge)",
                      "avg_launch_us": avg_launch_ms * 1e3,
-                     "bytes_per_launch": dec_bytes / launches},
+                     "bytes_per_launch": dec_bytes / launches,
+                     "attainable": dict(ceiling, frac=achieved / ceiling["gbps"])},
         "decode": {"pooled_tokens_per_s": pooled["decode_tokens_per_s"],
                    "pooled_gbps": pooled["decode_gbps"], "pooled_ms_per_step": pooled["decode_ms"]},
         "prefill_ms": pooled["prefill_ms"],

@@ -3,8 +3,10 @@
     python -m paper_2607_06827_amd.build
 
 Every HIP source under csrc/ is compiled to an object in _build/ and linked
-into paper_2607_06827_amd/libspeechkv.so.  Packed fp32 instructions are
-disabled for every device compile.
+into paper_2607_06827_amd/libspeechkv.so; the benchmark's streaming-read
+ceiling kernel (csrc_bench/) goes into its own libskv_bench.so, which only
+bench.py loads.  Packed fp32 instructions are disabled for every device
+compile.
 """
 from __future__ import annotations
 
@@ -15,8 +17,10 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
+CSRC_BENCH = os.path.join(HERE, "csrc_bench")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libspeechkv.so")
+BENCH_LIB = os.path.join(HERE, "libskv_bench.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -30,10 +34,7 @@ DEVICE_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip and link libspeechkv.so.  Returns its path."""
-    os.makedirs(BUILD, exist_ok=True)
-    sources = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+def _compile_and_link(sources, lib, verbose):
     procs = []
     objs = []
     for src in sources:
@@ -56,10 +57,18 @@ def build(verbose: bool = False) -> str:
             failed.append(src)
     if failed:
         raise RuntimeError(f"hipcc failed for {failed}")
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every csrc/*.hip and link libspeechkv.so, then the benchmark's
+    libskv_bench.so.  Returns the path of libspeechkv.so."""
+    os.makedirs(BUILD, exist_ok=True)
+    _compile_and_link(sorted(glob.glob(os.path.join(CSRC, "*.hip"))), LIB, verbose)
+    _compile_and_link(sorted(glob.glob(os.path.join(CSRC_BENCH, "*.hip"))), BENCH_LIB, verbose)
     return LIB
 
 
