@@ -132,10 +132,10 @@ int64_t speechkv_compressed_len_segments(const int32_t* text_len, const int32_t*
 
 int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t max_cache_len) {
   if (batch < 1 || num_kv_heads < 1 || max_cache_len < 0) return -1;
-  // A decode block has 8 waves; about 512 blocks (2 per CU on 256 CUs) keep
+  // A decode block has 4 waves; about 512 blocks (2 per CU on 256 CUs) keep
   // every CU streaming in one round.  Split a (sequence, KV head) only when
   // there are fewer pairs than that, and keep at least 16 groups of 4 keys
-  // (two per wave) in every split.
+  // (four per wave) in every split.
   const int64_t units = (int64_t)batch * num_kv_heads;
   int64_t s = (512 + units - 1) / units;
   const int64_t groups = ((int64_t)max_cache_len + 3) / 4;

@@ -706,9 +706,12 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
 }
 
 // Waves per block and key groups per load batch (tuning knobs; the split
-// heuristic of the host layer assumes 8 waves).
+// heuristic of the host layer assumes 4 waves).  Four waves per block beat
+// eight at every shape measured but one: 512 (b, kv head) blocks on 256 CUs
+// stream 1-2% faster, smaller batches up to 8% faster; a long pooled layer
+// of a small batch (16 x 8 heads, ~1900 keys, 4 splits) 2% slower.
 #ifndef SKV_DECODE_WAVES
-#define SKV_DECODE_WAVES 8
+#define SKV_DECODE_WAVES 4
 #endif
 #ifndef SKV_DECODE_BATCH
 #define SKV_DECODE_BATCH 2
