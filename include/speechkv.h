@@ -290,6 +290,8 @@ int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s,
  * q, out         device, element type cache->dtype, [batch][num_q_heads][head_dim].
  * cache_len      device int32 [batch].  Caller obligations: 0 <= cache_len[b]
  *                <= max_cache_len and the sequence has pages for them.
+ *                Block-table entries past a sequence's last page do not
+ *                affect the result (they may hold any value).
  * max_cache_len  host bound on cache_len (sizes the split-K grid).
  * k_new, v_new   device [batch][num_kv_heads][head_dim] of cache->dtype, or
  *                both NULL.
