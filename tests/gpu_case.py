@@ -40,6 +40,7 @@ class Case:
     shuffle: bool = True
     num_splits: int = 0
     zero_gate: bool = False
+    bound_slack: int = 0  # decode's host bound exceeds the longest cache by this (capped by capacity)
 
     @property
     def B(self):
@@ -62,7 +63,7 @@ def build(case: Case, device="cuda"):
     vn = inputs.normal((max(steps, 1), B, Hkv, D), s0 + 7, dtype=dt)
     clen = [skv.speechkv_compressed_len(p, t, n, case.w, case.layer, case.l0)
             for p, t, n in zip(case.P, case.T, case.N)]
-    pages = max(1, -(-(max(clen) + steps) // case.page_size))
+    pages = max(1, -(-(max(clen) + steps + case.bound_slack) // case.page_size))
     table, total = inputs.block_table(B, pages, case.seed, shuffle=case.shuffle, spare_pages=3)
     dev = torch.device(device)
     t = lambda x: None if x is None else x.to(dev)
@@ -139,14 +140,17 @@ def run_and_check(case: Case, check_prefill: bool = True, device="cuda") -> dict
     kn, vn, qd = x["kn"], x["vn"], x["qd"]
     kext = [list(kh[b, :x["clen"][b]]) for b in range(B)]
     vext = [list(vh[b, :x["clen"][b]]) for b in range(B)]
-    ws_bytes = skv.speechkv_decode_workspace_bytes(B, Hq, Hkv, D, max(x["clen"]) + case.decode_steps,
+    capacity = cache.block_table.shape[1] * cache.k_pages.shape[2]
+    bound = lambda n: min(n + case.bound_slack, capacity)
+    ws_bytes = skv.speechkv_decode_workspace_bytes(B, Hq, Hkv, D,
+                                                   bound(max(x["clen"]) + case.decode_steps),
                                                    case.num_splits)
     ws = torch.empty(max(ws_bytes, 16) // 4 + 4, dtype=torch.float32, device=dev)
     for s in range(case.decode_steps):
         lens = [c + s + 1 for c in x["clen"]]
         out = torch.full((B, Hq, D), float("nan"), dtype=x["dt"], device=dev)
         skv.speechkv_decode_attn(t(qd[s]), cache, torch.tensor(lens, dtype=torch.int32, device=dev),
-                                 max(lens), out, k_new=t(kn[s]), v_new=t(vn[s]), scale=scale,
+                                 bound(max(lens)), out, k_new=t(kn[s]), v_new=t(vn[s]), scale=scale,
                                  num_splits=case.num_splits, workspace=ws)
         torch.cuda.synchronize()
         for b in range(B):

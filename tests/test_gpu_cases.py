@@ -39,6 +39,12 @@ CASES = {
     "long-split": Case(P=[32, 0], T=[1100, 700], N=[10, 0], D=128, Hq=16, Hkv=8, decode_steps=2),
     "forced-splits": Case(P=[32, 5], T=[500, 130], N=[10, 2], D=128, num_splits=7),
     "f32-d128-split": Case(P=[3], T=[400], N=[2], D=128, dtype="f32", num_splits=3),
+    # decode's host bound well above every cache length: the batches requested
+    # from the bound before the lengths arrive must not be reduced
+    "loose-decode-bound": Case(P=[8, 0, 30], T=[300, 45, 9], N=[5, 3, 0], D=128, Hq=8, Hkv=2,
+                               bound_slack=200),
+    "loose-decode-bound-split": Case(P=[8, 2], T=[300, 45], N=[5, 3], D=128, num_splits=3,
+                                     bound_slack=150),
 }
 
 

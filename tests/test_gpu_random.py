@@ -3,7 +3,8 @@
 Each case draws, from its own seed, a batch of 1-4 sequences with random
 prefix, speech and suffix lengths (empty spans included), a window of 1-9
 frames, a layer below or above l0, a group size, head size, element type,
-page size, mask mode, gate scale and split count, and runs pool -> prefill
+page size, mask mode, gate scale, split count and how far decode's host
+bound on the cache length exceeds the longest cache, and runs pool -> prefill
 -> decode steps through the C ABI against the fp64 oracle (tests/gpu_case.py).
 A second set draws multi-run sequences (segment tables) and checks pooling
 and prefill against the multi-run oracle; a third draws cases for the two
@@ -39,7 +40,8 @@ def draw_case(seed: int) -> Case:
     return Case(P=P, T=T, N=N, w=int(r.integers(1, 10)), layer=layer, l0=l0, Hq=G * Hkv, Hkv=Hkv,
                 D=D, dtype=dtype, page_size=int(r.choice([8, 16, 32, 64])), mode=int(r.integers(0, 2)),
                 decode_steps=2, seed=seed, gate_scale=float(r.choice([0.5, 1.0, 4.0])),
-                num_splits=int(r.choice([0, 0, 1, 3])), zero_gate=bool(r.random() < 0.1))
+                num_splits=int(r.choice([0, 0, 1, 3])), zero_gate=bool(r.random() < 0.1),
+                bound_slack=int(r.choice([0, 0, 3, 50])))
 
 
 @pytest.mark.parametrize("seed", range(24))
