@@ -6,6 +6,8 @@
 
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "kernels.hpp"
 #include "kernels_bwd.hpp"
 #include "kernels_fused.hpp"
@@ -132,18 +134,32 @@ int64_t speechkv_compressed_len_segments(const int32_t* text_len, const int32_t*
 
 int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t max_cache_len) {
   if (batch < 1 || num_kv_heads < 1 || max_cache_len < 0) return -1;
-  // A decode block has 4 waves; about 512 blocks (2 per CU on 256 CUs) keep
-  // every CU streaming in one round.  Split a (sequence, KV head) only when
-  // there are fewer pairs than that, and keep at least 16 groups of 4 keys
-  // (four per wave) in every split.
-  const int64_t units = (int64_t)batch * num_kv_heads;
-  int64_t s = (512 + units - 1) / units;
+  // Pick the split count with the smallest estimated launch time.  Model
+  // (measured on MI355X with bf16 rows of 128, i.e. 512 bytes of K and V per
+  // key and KV head): a 4-wave block streams its keys at ~0.017 us per key
+  // after ~3 us of fixed cost; a launch moves at most ~5.5 TB/s; with more
+  // than one split, the merge launch and the partials add ~2.5 us + 0.4 us
+  // per split.  A short cache is therefore not split at all (the merge costs
+  // more than the extra parallelism saves), a long cache of few sequences is.
+  // Each split keeps at least 16 groups of 4 keys (four per wave), and the
+  // grid at most ~1024 blocks.
+  const double units = (double)batch * num_kv_heads;
+  const double L = max_cache_len;
+  const double t_stream = units * L * 512.0 / 5.5e6;  // us at the bandwidth bound
   const int64_t groups = ((int64_t)max_cache_len + 3) / 4;
-  const int64_t by_len = groups / 16;
-  if (s > by_len) s = by_len;
-  if (s > 64) s = 64;
-  if (s < 1) s = 1;
-  return (int32_t)s;
+  int64_t s_max = groups / 16;
+  s_max = std::min<int64_t>(s_max, std::max<int64_t>(1, (int64_t)((1024 + units - 1) / units)));
+  s_max = std::min<int64_t>(std::max<int64_t>(s_max, 1), 64);
+  int32_t best = 1;
+  double best_t = 0.0;
+  for (int64_t s = 1; s <= s_max; ++s) {
+    const double t = std::max(3.0 + 0.017 * L / (double)s, t_stream) + (s > 1 ? 2.5 + 0.4 * (double)s : 0.0);
+    if (s == 1 || t < best_t) {
+      best = (int32_t)s;
+      best_t = t;
+    }
+  }
+  return best;
 }
 
 size_t speechkv_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
