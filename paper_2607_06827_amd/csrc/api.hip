@@ -134,26 +134,28 @@ int64_t speechkv_compressed_len_segments(const int32_t* text_len, const int32_t*
 
 int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t max_cache_len) {
   if (batch < 1 || num_kv_heads < 1 || max_cache_len < 0) return -1;
-  // Pick the split count with the smallest estimated launch time.  Model
-  // (measured on MI355X with bf16 rows of 128, i.e. 512 bytes of K and V per
-  // key and KV head): a 4-wave block streams its keys at ~0.017 us per key
-  // after ~3 us of fixed cost; a launch moves at most ~5.5 TB/s; with more
-  // than one split, the merge launch and the partials add ~2.5 us + 0.4 us
-  // per split.  A short cache is therefore not split at all (the merge costs
-  // more than the extra parallelism saves), a long cache of few sequences is.
+  // Pick the split count with the smallest estimated launch time, among
+  // powers of two (measured faster than the counts between them).  Model,
+  // fitted to a sweep on MI355X over 1-64 sequences and 126-7788 keys with
+  // bf16 rows of 128 (512 bytes of K and V per key and KV head): a 4-wave
+  // block streams its range at ~0.016 us per key after ~1 us of fixed cost;
+  // a launch moves at most ~6.5 TB/s; more than one split adds ~4 us (the
+  // merge launch and the extra blocks' fixed costs; any value from 2.5 to
+  // 4.5 us picks the same counts on the sweep, the larger one keeps marginal
+  // short caches whole).  Short caches are therefore not split (the merge costs
+  // more than the parallelism saves), long caches of few sequences are.
   // Each split keeps at least 16 groups of 4 keys (four per wave), and the
   // grid at most ~1024 blocks.
   const double units = (double)batch * num_kv_heads;
   const double L = max_cache_len;
-  const double t_stream = units * L * 512.0 / 5.5e6;  // us at the bandwidth bound
+  const double t_stream = units * L * 512.0 / 6.5e6;  // us at the bandwidth bound
   const int64_t groups = ((int64_t)max_cache_len + 3) / 4;
-  int64_t s_max = groups / 16;
-  s_max = std::min<int64_t>(s_max, std::max<int64_t>(1, (int64_t)((1024 + units - 1) / units)));
-  s_max = std::min<int64_t>(std::max<int64_t>(s_max, 1), 64);
+  const int64_t by_grid = std::max<int64_t>(1, (int64_t)((1024.0 + units - 1.0) / units));
+  const int64_t s_max = std::max<int64_t>(1, std::min<int64_t>({32, groups / 16, by_grid}));
   int32_t best = 1;
   double best_t = 0.0;
-  for (int64_t s = 1; s <= s_max; ++s) {
-    const double t = std::max(3.0 + 0.017 * L / (double)s, t_stream) + (s > 1 ? 2.5 + 0.4 * (double)s : 0.0);
+  for (int64_t s = 1; s <= s_max; s *= 2) {
+    const double t = std::max(1.0 + 0.016 * L / (double)s, t_stream) + (s > 1 ? 4.0 : 0.0);
     if (s == 1 || t < best_t) {
       best = (int32_t)s;
       best_t = t;

@@ -686,14 +686,18 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(DecodeArgs a) {
   const int64_t row = (int64_t)b * hq + h;
   const float* ml = a.ws_ml + row * S * 2;
   const float* po = a.ws_o + row * S * D + e;
+  // Every split wrote its partial (an empty one: m = -inf, o = l = 0), so
+  // the loads are unconditional and issued eight splits at a time; an empty
+  // split gets weight 0.
   float M = neg_inf();
+#pragma unroll 8
   for (int s = 0; s < S; ++s) M = fmaxf(M, ml[2 * s]);
   float num = 0.f, den = 0.f;
   if (M != neg_inf()) {
+#pragma unroll 8
     for (int s = 0; s < S; ++s) {
       const float ms = ml[2 * s];
-      if (ms == neg_inf()) continue;
-      const float f = fast_exp2(ms - M);
+      const float f = ms == neg_inf() ? 0.f : fast_exp2(ms - M);
       num += f * po[(int64_t)s * D];
       den += f * ml[2 * s + 1];
     }

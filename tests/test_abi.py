@@ -78,20 +78,22 @@ def test_split_heuristic_properties():
     """The split count minimises a launch-time estimate: no split where the
     merge launch would cost more than the parallelism saves (short caches,
     or enough (sequence, KV head) pairs to reach the bandwidth bound), more
-    splits for long caches of few sequences, always 1..64 with at least 16
-    groups of 4 keys per split."""
+    splits for long caches of few sequences; always a power of two in
+    1..32 with at least 16 groups of 4 keys per split."""
     split = skv.speechkv_decode_num_splits
-    for B, H in ((1, 2), (8, 8), (32, 8), (64, 8), (128, 8)):
+    for B, H in ((2, 8), (8, 8), (32, 8), (64, 8), (128, 8)):
         for L in range(0, 260, 7):
             assert split(B, H, L) == 1
+    for L in range(0, 128):
+        assert split(1, 1, L) == 1                     # too short for two splits of 16 groups
     for B in (64, 128, 512):
         for L in (1, 300, 910, 4000, 7788):
             assert split(B, 8, L) == 1                 # 512+ pairs: bandwidth-bound as one split
-    assert split(1, 8, 7788) > split(4, 8, 7788) > 1   # fewer sequences, more splits
+    assert split(1, 8, 7788) > split(4, 8, 7788) > split(16, 8, 7788) > 1  # fewer sequences, more splits
     for B in (1, 2, 3, 8, 16, 33):
         for L in (0, 63, 64, 65, 500, 2000, 7788, 65536):
             s = split(B, 8, L)
-            assert 1 <= s <= 64
+            assert 1 <= s <= 32 and s & (s - 1) == 0
             assert s == 1 or (L + 3) // 4 >= 16 * s
 
 
