@@ -239,7 +239,7 @@ def measure_adaptive(base, steps, warmup, num_splits):
     return res
 
 
-def measure_fused(base, steps, copies=3):
+def measure_fused(base, steps, copies=4):
     """Pooling and prefill attention as one launch (pooling on the fly inside
     the attention, Sec. III-C) against the two launches: at the 1596-query
     workload (one layer, `copies` jobs in turn so that no launch finds its
@@ -266,7 +266,7 @@ def measure_fused(base, steps, copies=3):
             "stack_prefill_fused_ms": ms_fused, "stack_prefill_split_ms": ms_split}
 
 
-def measure_segments(steps, copies=3):
+def measure_segments(steps, copies=4):
     """Pooling + prefill attention of a multi-turn batch (three speech turns
     per sequence, segment tables) against a batch of the same rows and
     compressed length laid out as one run per sequence."""
@@ -303,7 +303,7 @@ def measure_hs_pool(wl, steps, copies=4):
     return res
 
 
-def measure_train_bwd(steps, copies=3):
+def measure_train_bwd(steps, copies=4):
     """The training backward of one layer (Sec. III-C) at the 1596-query x
     471-key prefill workload: attention backward (dQ, dK^, dV^) and pooling
     backward (raw dK, dV and the gate's du).  `copies` independent jobs run in
