@@ -41,8 +41,9 @@
 // 2^8), so the rows' states add up at the end (DPP / permlane swaps) and the
 // waves' states merge through LDS in one step.
 //
-// If k_new/v_new are given, the wave whose range holds slot L-1 stores them
-// there after its stream, and that key is read from k_new/v_new directly.  The kernel moves each K/V byte once: it is bound by HBM
+// If k_new/v_new are given, key L-1 is read from k_new/v_new directly (in the
+// masked tail of the wave whose range holds it), and the lanes holding it
+// store it into slot L-1 after the stream.  The kernel moves each K/V byte once: it is bound by HBM
 // bandwidth.
 #include "kernels.hpp"
 
@@ -531,15 +532,6 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   for (int d = 0; d < kDepth - 1; ++d)
     if (d < nbatch) all_ok = all_ok && ok_first[d];
 
-  // lanes of row 0 of the wave whose range holds slot L-1 store the new
-  // token's K/V there after the stream
-  const bool stores_new = has_new && L > 0 && g_begin * kRows <= last && last < g_end * kRows && r == 0;
-  R kn, vn;
-  if (stores_new) {
-    kn.load(static_cast<const T*>(a.k_new) + new_row, j);
-    vn.load(static_cast<const T*>(a.v_new) + new_row, j);
-  }
-
   // Masked batch starting at group gs: keys >= L (and groups past the tail)
   // are invalid; key L-1 comes from k_new when given.
   const int g_tail_end = min(g_end, (L + kRows - 1) / kRows);
@@ -576,6 +568,22 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
     }
   };
 
+  // The lanes that read key L-1 from k_new/v_new (a masked batch holds it)
+  // store that row into slot L-1 of the cache.  No load of this launch reads
+  // the slot from the cache, so the store can wait until after the stream.
+  auto store_new = [&](int gs, const R* kc, const R* vc, const bool* valid) {
+    if (!has_new || last < gs * kRows || last >= (gs + U) * kRows) return;  // wave-uniform
+    const int u = last / kRows - gs, grp = gs + u;
+    const int page = group_page(grp);
+#pragma unroll
+    for (int v = 0; v < U; ++v)  // (compile-time register indices)
+      if (v == u && valid[v] && r == last % kRows && page >= 0) {
+        const int64_t off = group_base(page, grp) + (int64_t)r * D;
+        kc[v].store(kpool + off, j);
+        vc[v].store(vpool + off, j);
+      }
+  };
+
   // The masked tail (at most U groups: the leftover full groups of the
   // batching plus the one group holding key L-1) is requested now, so that
   // its round trip is not added after the stream.
@@ -604,16 +612,7 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
       st.template consume<U, false>(kb[d % kDepth], vb[d % kDepth], nullptr);
     }
   }
-  // The wave holding slot L-1 stores the newest token's K/V there; no load
-  // of this launch reads that slot from the cache (key L-1 comes from k_new).
-  if (stores_new) {
-    const int page = group_page(last / kRows);
-    if (page >= 0) {
-      const int64_t off = group_base(page, last / kRows) + (int64_t)(last % kRows) * D;
-      kn.store(kpool + off, j);
-      vn.store(vpool + off, j);
-    }
-  }
+  store_new(tail_begin, kt, vt, tvalid);
   // A block-table entry out of range (a caller error) was read as page 0:
   // drop what the unmasked path accumulated rather than mix in that page.
   if (!all_ok) st.init();
@@ -623,6 +622,7 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   st.template consume<U, true>(kt, vt, tvalid);
   for (int gs = tail_begin + U; gs < g_tail_end; gs += U) {
     load_masked(gs, kt, vt, tvalid);
+    store_new(gs, kt, vt, tvalid);
     st.template consume<U, true>(kt, vt, tvalid);
   }
 
