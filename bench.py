@@ -21,7 +21,8 @@ against the 2.5 PFLOP/s dense MFMA peak (FLOPs of the visible (row, key) pairs
 only), each from a graph of that kernel alone; HS Compression's pooling of
 the whole hidden state (hidden 2048) on the same batch and spans, in GB/s;
 the training backward of one layer (attention and pooling gradients) at the
-1596-query prefill workload; and the fp64 CPU oracle timed on a bounded
+1596-query prefill workload; decode over 10-minute audio at batch 16 (split
+keys and their merge); and the fp64 CPU oracle timed on a bounded
 sample of the same job.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-full]
@@ -303,6 +304,32 @@ def measure_hs_pool(wl, steps, copies=4):
     return res
 
 
+def measure_long_decode(steps, layers=(0, 13, 14, 27)):
+    """Decode over 10-minute audio at a small batch (16 sequences, 7532
+    full-resolution rows, w = 4 from layer 14): layers 0 and 13 (full
+    resolution) and 14 and 27 (pooled) of the 28-layer stack, every decode
+    step, as one graph.  With 16 x 8 (sequence, KV head) pairs the keys are
+    split (split-K) and merged, with the split count the library picks."""
+    from paper_2607_06827_amd import inputs
+    from paper_2607_06827_amd.speechkv import speechkv_decode_num_splits
+    from paper_2607_06827_amd.workload import Job
+
+    wl = inputs.LONG_10MIN
+    job = Job(wl, layers=list(layers), with_prefill=False)
+    job.run_prefill()
+    g = capture(lambda: [job.run_decode_step(s) for s in range(wl.decode_steps)])
+    ms = time_graph(g, max(2, steps))
+    launches = wl.decode_steps * len(job.layers)
+    total = sum(job.decode_bytes(s) for s in range(wl.decode_steps))
+    gbps = total / (ms * 1e-3) / 1e9
+    splits = {l: speechkv_decode_num_splits(wl.batch, wl.num_kv_heads, job.prefill_clen[i] + wl.decode_steps)
+              for i, l in enumerate(job.layers)}
+    log(f"long decode ({wl.name}, layers {list(layers)}): {ms / launches * 1e3:.1f} us per launch, {gbps:.0f} GB/s")
+    return {"workload": wl.name, "layers": list(layers), "avg_launch_us": ms / launches * 1e3,
+            "achieved_gbps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBPS,
+            "splits_per_layer": splits, "tokens_per_s": wl.batch * wl.decode_steps / (ms * 1e-3)}
+
+
 def measure_train_bwd(steps, copies=4):
     """The training backward of one layer (Sec. III-C) at the 1596-query x
     471-key prefill workload: attention backward (dQ, dK^, dV^) and pooling
@@ -489,6 +516,8 @@ def main():
         extras["hs_pool"] = measure_hs_pool(wl, args.steps)
         torch.cuda.empty_cache()
         extras["train_bwd"] = measure_train_bwd(args.steps)
+        torch.cuda.empty_cache()
+        extras["long_decode"] = measure_long_decode(args.steps)
         torch.cuda.empty_cache()
 
     dec_bytes, launches = decode_launch_stats(job)
