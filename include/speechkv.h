@@ -542,8 +542,11 @@ int64_t speechkv_compressed_len_segments(const int32_t* text_len, const int32_t*
                                          int32_t num_segments, int32_t w, int32_t layer,
                                          int32_t l0);
 
-/* Split count chosen by speechkv_decode_attn when num_splits = 0, from the
- * number of (sequence, KV head) pairs and the longest cache.  Host only;
+/* Split count chosen by speechkv_decode_attn when num_splits = 0: the power
+ * of two, at most 32, that minimises an estimate of the launch time from the
+ * number of (sequence, KV head) pairs and the longest cache (a split costs a
+ * merge launch, so short caches and large batches stay whole, long caches of
+ * few sequences are split; every split keeps at least 64 keys).  Host only;
  * returns -1 on a non-positive batch/num_kv_heads or a negative length. */
 int32_t speechkv_decode_num_splits(int32_t batch, int32_t num_kv_heads,
                                    int32_t max_cache_len);
