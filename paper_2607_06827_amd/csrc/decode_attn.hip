@@ -13,10 +13,10 @@
 // Key ranges are cut from the host-known bound on the cache length, so the
 // first K/V loads wait only on the block-table entries: the first batches
 // are requested from the bound before the device cache length arrives, and
-// the queries and the new token's K/V go out behind them.  The wave's table
-// entries sit one per lane and are read back with readlane, so every load
-// address is a wave-uniform page base (SGPRs) plus a fixed 32-bit per-lane
-// offset.
+// the queries and the masked tail (with the new token's K/V) go out behind
+// them.  The wave's table entries sit one per lane and are read back with
+// readlane, so every load address is a wave-uniform page base (SGPRs) plus
+// a fixed 32-bit per-lane offset.
 //
 // Lane layout: kLanes = D/8 lanes per key row, 8 elements (16 bytes of bf16,
 // 32 of fp32) per lane, so kRows = 64 / kLanes consecutive keys of one page
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(NW * 64, (G <= 2 ? 4 : 2)) void decode_kernel(Decod
   // first kDepth - 1 batches are requested from the host bound before the
   // cache length arrives (when the length is below the bound, those that turn
   // out to lie past the unmasked range are simply never reduced), and the
-  // queries, the new token's K/V and the masked tail follow them.
+  // queries and the masked tail (which reads the new token's K/V) follow.
   const int first_page = (g_begin * kRows) >> shift;
   const int32_t* table = a.table + (int64_t)b * a.pv.max_pages;
   int tbl = -1;
