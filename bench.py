@@ -20,10 +20,11 @@ cache rows written once) and the prefill attention's achieved bf16 TFLOP/s
 against the 2.5 PFLOP/s dense MFMA peak (FLOPs of the visible (row, key) pairs
 only), each from a graph of that kernel alone; HS Compression's pooling of
 the whole hidden state (hidden 2048) on the same batch and spans, in GB/s;
-the training backward of one layer (attention and pooling gradients) at the
-1596-query prefill workload; decode over 10-minute audio at batch 16 (split
-keys and their merge); and the fp64 CPU oracle timed on a bounded
-sample of the same job.
+the training backward of one layer (attention and pooling gradients) and the
+prefill attention alone at the 1596-query prefill workload; decode over
+10-minute audio at batch 16 (all 28 layers, w = 2, 4 and 8 against no
+compression); and the fp64 CPU oracle timed on a bounded sample of the same
+job.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-full]
     python bench.py --traffic [--workload NAME]   # eager launches for counter runs
@@ -170,6 +171,15 @@ def measure(job, steps, warmup, label):
     g_pre = capture(job.run_prefill)
     g_pool = capture(job.run_pool)
     g_attn = capture(job.run_prefill_attn)
+    wl = job.wl
+    nl = len(job.layers)
+    # the decode launches of each layer class on their own (same order and
+    # cache contents as in the step)
+    classes = {"pooled": [i for i, l in enumerate(job.layers) if l >= job.l0],
+               "full": [i for i, l in enumerate(job.layers) if l < job.l0]}
+    g_cls = {k: capture(lambda ix=ix: [job.decode_layer(i, s) for s in range(wl.decode_steps)
+                                       for i in ix])
+             for k, ix in classes.items() if ix}
     for _ in range(warmup):
         g_step.replay()
     ms_step = time_graph(g_step, steps)
@@ -177,9 +187,16 @@ def measure(job, steps, warmup, label):
     ms_pre = time_graph(g_pre, max(2, steps))
     ms_pool = time_graph(g_pool, max(2, steps))
     ms_attn = time_graph(g_attn, max(2, steps))
+    dec_cls = {}
+    for k, g in g_cls.items():
+        ms = time_graph(g, max(2, steps))
+        n = len(classes[k]) * wl.decode_steps
+        nbytes = sum(job.decode_bytes_layer(i, s) for i in classes[k] for s in range(wl.decode_steps))
+        dec_cls[k] = {"layers": len(classes[k]), "avg_launch_us": ms / n * 1e3,
+                      "bytes_per_launch": nbytes / n,
+                      "achieved_gbps": nbytes / (ms * 1e-3) / 1e9}
+    del g_cls
     dec_bytes, launches = decode_launch_stats(job)
-    wl = job.wl
-    nl = len(job.layers)
     pool_bytes = sum(job.pool_bytes_layer(i) for i in range(nl))
     attn_flops = sum(job.prefill_flops_layer(i) for i in range(nl))
     attn_bytes = sum(job.prefill_bytes_layer(i) for i in range(nl))
@@ -191,6 +208,7 @@ def measure(job, steps, warmup, label):
         "decode_gbps": dec_bytes / (ms_dec * 1e-3) / 1e9,
         "decode_bytes_per_step": dec_bytes,
         "decode_launches": launches,
+        "decode_classes": dec_cls,
         "prefill_ms": ms_pre,
         "pool": {"avg_launch_us": ms_pool / nl * 1e3,
                  "achieved_gbps": pool_bytes / (ms_pool * 1e-3) / 1e9,
@@ -267,6 +285,35 @@ def measure_fused(base, steps, copies=4):
             "stack_prefill_fused_ms": ms_fused, "stack_prefill_split_ms": ms_split}
 
 
+def measure_prefill_1596(steps, copies=4):
+    """Prefill attention alone at the 1596-query x 471-key workload (b=8,
+    16/8 heads): `copies` independent jobs, pooled once beforehand, run in
+    turn so that no launch finds its 120 MB of inputs and outputs in the
+    256 MB last-level cache."""
+    from paper_2607_06827_amd import inputs
+    from paper_2607_06827_amd.workload import Job
+
+    wl = inputs.PREFILL_1500
+    jobs = [Job(wl.with_(seed=wl.seed + i)) for i in range(copies)]
+    for j in jobs:
+        j.run_pool()
+    g = capture(lambda: [j.run_prefill_attn() for j in jobs])
+    ms = time_graph(g, max(10, steps)) / copies
+    j = jobs[0]
+    flops, nbytes = j.prefill_flops_layer(0), j.prefill_bytes_layer(0)
+    t_floor = max(flops / (BF16_MFMA_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBPS * 1e9))
+    tflops = flops / (ms * 1e-3) / 1e12
+    log(f"prefill attention ({wl.name}, rotated): {ms * 1e3:.1f} us, {tflops:.0f} TFLOP/s, "
+        f"roofline fraction {t_floor / (ms * 1e-3):.3f}")
+    del g, jobs
+    return {"workload": wl.name, "avg_launch_us": ms * 1e3, "flops_per_launch": flops,
+            "bytes_per_launch": nbytes, "achieved_tflops": tflops,
+            "frac_of_bf16_mfma_peak": tflops / BF16_MFMA_PEAK_TFLOPS,
+            "achieved_gbps": nbytes / (ms * 1e-3) / 1e9,
+            "floor_us": t_floor * 1e6, "roofline_frac": t_floor / (ms * 1e-3),
+            "buffers": f"{copies} rotated jobs"}
+
+
 def measure_segments(steps, copies=4):
     """Pooling + prefill attention of a multi-turn batch (three speech turns
     per sequence, segment tables) against a batch of the same rows and
@@ -304,30 +351,60 @@ def measure_hs_pool(wl, steps, copies=4):
     return res
 
 
-def measure_long_decode(steps, layers=(0, 13, 14, 27)):
-    """Decode over 10-minute audio at a small batch (16 sequences, 7532
-    full-resolution rows, w = 4 from layer 14): layers 0 and 13 (full
-    resolution) and 14 and 27 (pooled) of the 28-layer stack, every decode
-    step, as one graph.  With 16 x 8 (sequence, KV head) pairs the keys are
-    split (split-K) and merged, with the split count the library picks."""
+def measure_long_sweep(steps, windows=(2, 4, 8)):
+    """Decode over 10-minute audio (16 sequences, 32 + 7500 rows, 256 decode
+    steps, all 28 layers) for each window w with layers 14..27 pooled, and
+    the same job with no compression.  Raw K/V are generated once and shared;
+    each configuration pools its caches, then its 256 x 28 decode launches
+    are captured as one graph and timed.  The split count is the library's
+    choice (split-K with a log-sum-exp merge where it pays)."""
+    import torch
     from paper_2607_06827_amd import inputs
     from paper_2607_06827_amd.speechkv import speechkv_decode_num_splits
     from paper_2607_06827_amd.workload import Job
 
     wl = inputs.LONG_10MIN
-    job = Job(wl, layers=list(layers), with_prefill=False)
-    job.run_prefill()
-    g = capture(lambda: [job.run_decode_step(s) for s in range(wl.decode_steps)])
-    ms = time_graph(g, max(2, steps))
-    launches = wl.decode_steps * len(job.layers)
-    total = sum(job.decode_bytes(s) for s in range(wl.decode_steps))
-    gbps = total / (ms * 1e-3) / 1e9
-    splits = {l: speechkv_decode_num_splits(wl.batch, wl.num_kv_heads, job.prefill_clen[i] + wl.decode_steps)
-              for i, l in enumerate(job.layers)}
-    log(f"long decode ({wl.name}, layers {list(layers)}): {ms / launches * 1e3:.1f} us per launch, {gbps:.0f} GB/s")
-    return {"workload": wl.name, "layers": list(layers), "avg_launch_us": ms / launches * 1e3,
-            "achieved_gbps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBPS,
-            "splits_per_layer": splits, "tokens_per_s": wl.batch * wl.decode_steps / (ms * 1e-3)}
+    base = None
+    res = {"workload": wl.name, "batch": wl.batch, "layers": wl.num_layers, "l0": wl.l0,
+           "decode_steps": wl.decode_steps, "configs": {}}
+    for w in (None,) + tuple(windows):
+        name = "no_compression" if w is None else f"w{w}"
+        job = Job(wl.with_(w=w or wl.w), l0=wl.num_layers if w is None else wl.l0,
+                  with_prefill=False, share_inputs=base)
+        if base is None:
+            base = job
+        job.run_prefill()
+        g = capture(lambda: [job.run_decode_step(s) for s in range(wl.decode_steps)])
+        ms = time_graph(g, max(2, steps // 2))
+        del g
+        total = sum(job.decode_bytes(s) for s in range(wl.decode_steps))
+        pooled = [i for i, l in enumerate(job.layers) if l >= job.l0]
+        full = [i for i, l in enumerate(job.layers) if l < job.l0]
+        cfg = {"ms_per_decode_step": ms / wl.decode_steps,
+               "gb_per_decode_step": total / wl.decode_steps / 1e9,
+               "achieved_gbps": total / (ms * 1e-3) / 1e9,
+               "frac_of_hbm_peak": total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+               "tokens_per_s": wl.batch * wl.decode_steps / (ms * 1e-3),
+               "cache_rows": {"pooled": job.prefill_clen[pooled[0]] if pooled else None,
+                              "full": job.prefill_clen[full[0]] if full else None},
+               "splits": {"pooled": speechkv_decode_num_splits(
+                              wl.batch, wl.num_kv_heads, job.prefill_clen[pooled[0]] + wl.decode_steps)
+                          if pooled else None,
+                          "full": speechkv_decode_num_splits(
+                              wl.batch, wl.num_kv_heads, job.prefill_clen[full[0]] + wl.decode_steps)
+                          if full else None}}
+        res["configs"][name] = cfg
+        log(f"10-minute decode {name}: {cfg['ms_per_decode_step']:.3f} ms per step "
+            f"({cfg['gb_per_decode_step']:.2f} GB, {cfg['achieved_gbps']:.0f} GB/s)")
+        if job is not base:
+            del job
+        torch.cuda.empty_cache()
+    full_ms = res["configs"]["no_compression"]["ms_per_decode_step"]
+    for name, cfg in res["configs"].items():
+        cfg["speedup_over_no_compression"] = full_ms / cfg["ms_per_decode_step"]
+    del base
+    torch.cuda.empty_cache()
+    return res
 
 
 def measure_train_bwd(steps, copies=4):
@@ -517,7 +594,9 @@ def main():
         torch.cuda.empty_cache()
         extras["train_bwd"] = measure_train_bwd(args.steps)
         torch.cuda.empty_cache()
-        extras["long_decode"] = measure_long_decode(args.steps)
+        extras["prefill_1596"] = measure_prefill_1596(args.steps)
+        torch.cuda.empty_cache()
+        extras["long_10min"] = measure_long_sweep(args.steps)
         torch.cuda.empty_cache()
 
     dec_bytes, launches = decode_launch_stats(job)
@@ -525,6 +604,7 @@ def main():
     achieved = dec_bytes / launches / (avg_launch_ms * 1e-3) / 1e9
     log("measuring the attainable streaming-read rate")
     ceiling = stream_ceiling(job)
+    cls = pooled["decode_classes"]
     result = {
         "metric": METRIC,
         "value": pooled["tokens_per_s"],
@@ -549,7 +629,16 @@ def main():
                      "kernel": "decode_kernel (+ split merge)",
                      "avg_launch_us": avg_launch_ms * 1e3,
                      "bytes_per_launch": dec_bytes / launches,
-                     "attainable": dict(ceiling, frac=achieved / ceiling["gbps"])},
+                     "attainable": dict(ceiling, frac=achieved / ceiling["gbps"]),
+                     "pooled_frac": cls.get("pooled", {}).get("achieved_gbps", 0) / HBM_PEAK_GBPS,
+                     "full_frac": cls.get("full", {}).get("achieved_gbps", 0) / HBM_PEAK_GBPS,
+                     "pooled_frac_of_attainable": (cls.get("pooled", {}).get("achieved_gbps", 0)
+                                                   / ceiling["pooled_launch_gbps"]
+                                                   if ceiling.get("pooled_launch_gbps") else None),
+                     "full_frac_of_attainable": (cls.get("full", {}).get("achieved_gbps", 0)
+                                                 / ceiling["full_launch_gbps"]
+                                                 if ceiling.get("full_launch_gbps") else None),
+                     "classes": cls},
         "decode": {"pooled_tokens_per_s": pooled["decode_tokens_per_s"],
                    "pooled_gbps": pooled["decode_gbps"], "pooled_ms_per_step": pooled["decode_ms"]},
         "prefill_ms": pooled["prefill_ms"],

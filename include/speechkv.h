@@ -203,8 +203,9 @@ typedef struct speechkv_segments {
  * cache          host pointer to the destination cache description.  Caller
  *                obligation: each sequence has pages for P + nW + N slots.
  * cache_len_out  device int32 [batch] receiving P + nW + N, or NULL.
- * Errors: INVALID_ARG, UNSUPPORTED, ALIAS (the raw K/V byte range overlaps
- *         the page pool it would write), HIP.
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP; ALIAS when a page pool or
+ *         cache_len_out overlaps the raw K/V byte range, the gate, the block
+ *         table, the span lengths or another of the three.
  */
 int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
                      int64_t stride_s, int64_t stride_h, int32_t batch,
@@ -305,7 +306,11 @@ int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s,
  *                speechkv_decode_workspace_bytes(...) bytes (16-byte
  *                aligned); may be NULL when that size is 0.  Its contents on
  *                entry do not matter.
- * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP; ALIAS when out or the
+ * workspace overlaps q, k_new, v_new, cache_len, the block table, a page
+ * pool or each other, or (with k_new given, so the pools are written) when a
+ * page pool overlaps q, k_new, v_new, cache_len, the block table or the
+ * other pool.
  */
 int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
                          const speechkv_paged_kv* cache,
@@ -341,7 +346,8 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
  * scale          logit scale, finite and > 0; 1/sqrt(head_dim) in the paper.
  * lse            device fp32 [batch][num_q_heads][q_len] receiving the
  *                natural-log log-sum-exp of each row's scaled logits, or NULL.
- * Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP; ALIAS when out or lse overlaps q, a
+ *         page pool, the block table, the span lengths or each other.
  */
 int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
                           int32_t q_len, const speechkv_paged_kv* cache,
@@ -358,7 +364,7 @@ int speechkv_prefill_attn(const void* q, int32_t batch, int32_t num_q_heads,
  * of the cache.
  * Arguments as for speechkv_prefill_attn, with segs (host pointer) in place
  * of spans; segs->max_total_len must not exceed q_len.
- * Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ * Errors: INVALID_ARG, UNSUPPORTED, ALIAS, HIP.
  */
 int speechkv_prefill_attn_segments(const void* q, int32_t batch, int32_t num_q_heads,
                                    int32_t q_len, const speechkv_paged_kv* cache,

@@ -106,6 +106,24 @@ bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
 
 int status_of(hipError_t e) { return e == hipSuccess ? SPEECHKV_OK : SPEECHKV_ERR_HIP; }
 
+// A byte range of one argument; a null pointer takes no part in the checks.
+struct Region {
+  const void* p;
+  int64_t n;
+};
+
+// True when a written region overlaps a read region or another written one.
+bool aliased(const Region* wr, int nw, const Region* rd, int nr) {
+  for (int i = 0; i < nw; ++i) {
+    if (!wr[i].p) continue;
+    for (int k = 0; k < nr; ++k)
+      if (rd[k].p && overlaps(wr[i].p, wr[i].n, rd[k].p, rd[k].n)) return true;
+    for (int k = i + 1; k < nw; ++k)
+      if (wr[k].p && overlaps(wr[i].p, wr[i].n, wr[k].p, wr[k].n)) return true;
+  }
+  return false;
+}
+
 }  // namespace
 
 extern "C" {
@@ -217,11 +235,17 @@ static int pool_kv_impl(const void* k_raw, const void* v_raw, int64_t stride_b, 
                        (int64_t)(cache->num_kv_heads - 1) * stride_h + D;
   const int64_t raw_bytes = last * esz;
   const int64_t pool_bytes = page_pool_bytes(cache);
-  if (overlaps(k_raw, raw_bytes, cache->k_pages, pool_bytes) ||
-      overlaps(k_raw, raw_bytes, cache->v_pages, pool_bytes) ||
-      overlaps(v_raw, raw_bytes, cache->k_pages, pool_bytes) ||
-      overlaps(v_raw, raw_bytes, cache->v_pages, pool_bytes))
-    return SPEECHKV_ERR_ALIAS;
+  // the pools and the lengths written may not overlap what is read (raw K/V,
+  // gate, block table, span lengths) or each other
+  const int64_t lens = (int64_t)batch * 4;
+  const Region rd[] = {{k_raw, raw_bytes}, {v_raw, raw_bytes},
+                       {gate_u, (int64_t)cache->num_kv_heads * D * 4},
+                       {cache->block_table, (int64_t)batch * cache->max_pages_per_seq * 4},
+                       {spans->prefix_len, lens}, {spans->speech_len, lens},
+                       {spans->suffix_len, lens}};
+  const Region wr[] = {{cache->k_pages, pool_bytes}, {cache->v_pages, pool_bytes},
+                       {cache_len_out, lens}};
+  if (aliased(wr, 3, rd, 7)) return SPEECHKV_ERR_ALIAS;
   skv::PoolArgs a;
   a.k_raw = k_raw;
   a.v_raw = v_raw;
@@ -309,30 +333,32 @@ int speechkv_pool_hidden(const void* h, int64_t stride_b, int64_t stride_s, int3
   return status_of(skv::launch_pool_hidden(a, dtype, hidden, batch, static_cast<hipStream_t>(stream)));
 }
 
-int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
-                         const speechkv_paged_kv* cache, const int32_t* cache_len,
-                         int32_t max_cache_len, const void* k_new, const void* v_new, float scale,
-                         int32_t num_splits, void* out, void* workspace, size_t workspace_bytes,
-                         void* stream) {
-  if (!q || !out || !cache_len) return SPEECHKV_ERR_INVALID_ARG;
-  int st = check_cache(cache);
-  if (st) return st;
-  if (batch < 1 || batch > kMaxGrid || max_cache_len < 0 || num_splits < 0 || num_splits > kMaxGrid)
-    return SPEECHKV_ERR_INVALID_ARG;
-  if ((k_new == nullptr) != (v_new == nullptr)) return SPEECHKV_ERR_INVALID_ARG;
-  if (!(scale > 0.f) || scale > 3.0e38f) return SPEECHKV_ERR_INVALID_ARG;  // finite, > 0
-  if ((int64_t)max_cache_len > (int64_t)cache->max_pages_per_seq * cache->page_size)
-    return SPEECHKV_ERR_INVALID_ARG;
+// Checks and launches of speechkv_decode_attn.  `workspace` holds the split
+// partials when the step is split; its size has been checked by the caller.
+static int decode_attn_impl(const void* q, int32_t batch, int32_t num_q_heads,
+                            const speechkv_paged_kv* cache, const int32_t* cache_len,
+                            int32_t max_cache_len, const void* k_new, const void* v_new,
+                            float scale, int32_t splits, void* out, void* workspace, size_t need,
+                            void* stream) {
   const int group = group_of(num_q_heads, cache->num_kv_heads);
-  if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
-  if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
-  if (!aligned16(q) || !aligned16(out) || (k_new && (!aligned16(k_new) || !aligned16(v_new))))
-    return SPEECHKV_ERR_INVALID_ARG;
-  const int splits = num_splits ? num_splits
-                                : speechkv_decode_num_splits(batch, cache->num_kv_heads, max_cache_len);
-  const size_t need = speechkv_decode_workspace_bytes(batch, num_q_heads, cache->num_kv_heads,
-                                                      cache->head_dim, max_cache_len, splits);
-  if (need && (!workspace || workspace_bytes < need || !aligned16(workspace))) return SPEECHKV_ERR_WORKSPACE;
+  const int esz = elt_size(cache->dtype);
+  const int D = cache->head_dim;
+  // nothing written (out, the split partials, and the pools when the new
+  // token is stored) may overlap anything read or another written region
+  const int64_t qo_bytes = (int64_t)batch * num_q_heads * D * esz;
+  const int64_t new_bytes = (int64_t)batch * cache->num_kv_heads * D * esz;
+  const int64_t pool_bytes = page_pool_bytes(cache);
+  const int64_t table_bytes = (int64_t)batch * cache->max_pages_per_seq * 4;
+  // (the pools count as written when the new token is stored, else as read)
+  const bool store = k_new != nullptr;
+  const Region rd[] = {{q, qo_bytes}, {k_new, new_bytes}, {v_new, new_bytes},
+                       {cache_len, (int64_t)batch * 4}, {cache->block_table, table_bytes},
+                       {store ? nullptr : cache->k_pages, pool_bytes},
+                       {store ? nullptr : cache->v_pages, pool_bytes}};
+  const Region wr[] = {{out, qo_bytes}, {need ? workspace : nullptr, (int64_t)need},
+                       {store ? cache->k_pages : nullptr, pool_bytes},
+                       {store ? cache->v_pages : nullptr, pool_bytes}};
+  if (aliased(wr, 4, rd, 7)) return SPEECHKV_ERR_ALIAS;
   skv::DecodeArgs a;
   a.q = q;
   a.k_pages = cache->k_pages;
@@ -362,6 +388,48 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
   return status_of(e);
 }
 
+// Argument checks of both decode entry points; on success *splits holds the
+// split count and *need the workspace bytes it takes.
+static int check_decode(const void* q, int32_t batch, int32_t num_q_heads,
+                        const speechkv_paged_kv* cache, const int32_t* cache_len,
+                        int32_t max_cache_len, const void* k_new, const void* v_new, float scale,
+                        int32_t num_splits, const void* out, int32_t* splits, size_t* need) {
+  if (!q || !out || !cache_len) return SPEECHKV_ERR_INVALID_ARG;
+  int st = check_cache(cache);
+  if (st) return st;
+  if (batch < 1 || batch > kMaxGrid || max_cache_len < 0 || num_splits < 0 || num_splits > kMaxGrid)
+    return SPEECHKV_ERR_INVALID_ARG;
+  if ((k_new == nullptr) != (v_new == nullptr)) return SPEECHKV_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || scale > 3.0e38f) return SPEECHKV_ERR_INVALID_ARG;  // finite, > 0
+  if ((int64_t)max_cache_len > (int64_t)cache->max_pages_per_seq * cache->page_size)
+    return SPEECHKV_ERR_INVALID_ARG;
+  const int group = group_of(num_q_heads, cache->num_kv_heads);
+  if (num_q_heads < 1 || num_q_heads % cache->num_kv_heads) return SPEECHKV_ERR_INVALID_ARG;
+  if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(out) || (k_new && (!aligned16(k_new) || !aligned16(v_new))))
+    return SPEECHKV_ERR_INVALID_ARG;
+  *splits = num_splits ? num_splits
+                       : speechkv_decode_num_splits(batch, cache->num_kv_heads, max_cache_len);
+  *need = speechkv_decode_workspace_bytes(batch, num_q_heads, cache->num_kv_heads,
+                                          cache->head_dim, max_cache_len, *splits);
+  return SPEECHKV_OK;
+}
+
+int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
+                         const speechkv_paged_kv* cache, const int32_t* cache_len,
+                         int32_t max_cache_len, const void* k_new, const void* v_new, float scale,
+                         int32_t num_splits, void* out, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  int32_t splits = 0;
+  size_t need = 0;
+  const int st = check_decode(q, batch, num_q_heads, cache, cache_len, max_cache_len, k_new, v_new,
+                              scale, num_splits, out, &splits, &need);
+  if (st) return st;
+  if (need && (!workspace || workspace_bytes < need || !aligned16(workspace))) return SPEECHKV_ERR_WORKSPACE;
+  return decode_attn_impl(q, batch, num_q_heads, cache, cache_len, max_cache_len, k_new, v_new,
+                          scale, splits, out, workspace, need, stream);
+}
+
 // speechkv_prefill_attn and speechkv_prefill_attn_segments (segs set)
 static int prefill_attn_impl(const void* q, int32_t batch, int32_t num_q_heads, int32_t q_len,
                              const speechkv_paged_kv* cache, const speechkv_spans* spans,
@@ -383,6 +451,18 @@ static int prefill_attn_impl(const void* q, int32_t batch, int32_t num_q_heads, 
   if (group < 0) return SPEECHKV_ERR_UNSUPPORTED;
   if (!aligned16(q) || !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
     return SPEECHKV_ERR_INVALID_ARG;
+  // out and lse may not overlap what is read (queries, pools, block table,
+  // span lengths) or each other
+  const int64_t qo_bytes =
+      (int64_t)batch * q_len * num_q_heads * cache->head_dim * elt_size(cache->dtype);
+  const int64_t pool_bytes = page_pool_bytes(cache);
+  const int64_t lens = (int64_t)batch * 4;
+  const Region rd[] = {{q, qo_bytes}, {cache->k_pages, pool_bytes}, {cache->v_pages, pool_bytes},
+                       {cache->block_table, (int64_t)batch * cache->max_pages_per_seq * 4},
+                       {spans->prefix_len, lens}, {spans->speech_len, lens},
+                       {spans->suffix_len, lens}};
+  const Region wr[] = {{out, qo_bytes}, {lse, (int64_t)batch * num_q_heads * q_len * 4}};
+  if (aliased(wr, 2, rd, 7)) return SPEECHKV_ERR_ALIAS;
   if (spans->max_total_len == 0) return SPEECHKV_OK;
   const int rows_per_tile = skv::prefill_rows_per_tile(group);
   const int64_t tiles = (spans->max_total_len + rows_per_tile - 1) / rows_per_tile;

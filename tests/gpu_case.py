@@ -14,7 +14,7 @@ import numpy as np
 import torch
 
 import oracle
-from helpers import TOL, f64, gather, rel_err, rms_err, tensor_err
+from helpers import TOL, f64, fwd_err, fwd_parts, gather, rms_err, tensor_err
 from paper_2607_06827_amd import inputs
 from paper_2607_06827_amd import speechkv as skv
 
@@ -45,6 +45,34 @@ class Case:
     @property
     def B(self):
         return len(self.P)
+
+
+GUARD = 4096  # bytes of fixed pattern on each side of a guarded output
+GUARD_BYTE = 0xA5
+
+
+def guarded(shape, dtype, dev, fill=float("nan")):
+    """A tensor of `shape` (filled with `fill`) inside a larger allocation
+    whose GUARD bytes before and after it hold GUARD_BYTE.  Returns the
+    tensor and a function asserting that the guards are intact."""
+    n = 1
+    for d in shape:
+        n *= d
+    esz = torch.tensor([], dtype=dtype).element_size()
+    g = GUARD // esz
+    buf = torch.empty(n + 2 * g, dtype=dtype, device=dev)
+    raw = buf.view(torch.uint8)
+    raw[:GUARD] = GUARD_BYTE
+    raw[GUARD + n * esz:] = GUARD_BYTE
+    t = buf[g:g + n].view(shape)
+    t.fill_(fill)
+
+    def check(what):
+        torch.cuda.synchronize()
+        assert bool(torch.all(raw[:GUARD] == GUARD_BYTE)), f"{what}: guard before it overwritten"
+        assert bool(torch.all(raw[GUARD + n * esz:] == GUARD_BYTE)), f"{what}: guard after it overwritten"
+
+    return t, check
 
 
 def build(case: Case, device="cuda"):
@@ -102,20 +130,28 @@ def run_and_check(case: Case, check_prefill: bool = True, device="cuda") -> dict
         if L == 0:
             continue
         gk, gv = gather(cache, b, L)
-        errs[f"pool_k[{b}]"] = rel_err(f64(gk), kh[b, :L])
-        errs[f"pool_v[{b}]"] = rel_err(f64(gv), vh[b, :L])
+        errs[f"pool_k[{b}]"] = fwd_err(f64(gk), kh[b, :L], case.dtype)
+        errs[f"pool_v[{b}]"] = fwd_err(f64(gv), vh[b, :L], case.dtype)
         # text rows are copies: bit for bit
         P, T = case.P[b], case.T[b]
         nW = L - P - case.N[b]
         assert torch.equal(gk[:P].cpu(), x["k_raw"][b, :P])
         assert torch.equal(gv[nW + P:].cpu(), x["v_raw"][b, P + T:P + T + case.N[b]])
 
+    # pages that no sequence's table names are never written
+    named = set(cache.block_table.flatten().tolist())
+    spare = [p for p in range(cache.k_pages.shape[0]) if p not in named]
+    assert spare
+    assert torch.isnan(cache.k_pages[spare].float()).all() and torch.isnan(cache.v_pages[spare].float()).all()
+
     if check_prefill:
-        out = torch.full((B, x["S"], Hq, D), float("nan"), dtype=x["dt"], device=dev)
-        lse = torch.full((B, Hq, x["S"]), float("nan"), dtype=torch.float32, device=dev)
+        out, out_guard = guarded((B, x["S"], Hq, D), x["dt"], dev)
+        lse, lse_guard = guarded((B, Hq, x["S"]), torch.float32, dev)
         skv.speechkv_prefill_attn(t(x["q"]), cache, spans, case.w, case.layer, case.l0, out,
                                   mask_mode=case.mode, scale=scale, lse=lse)
         torch.cuda.synchronize()
+        out_guard("prefill out")
+        lse_guard("prefill lse")
         ref, ref_lse = oracle.attention(f64(x["q"]), kh, vh, case.P, case.T, case.N, case.w,
                                         case.layer, case.l0, case.mode, scale)
         for b in range(B):
@@ -124,8 +160,11 @@ def run_and_check(case: Case, check_prefill: bool = True, device="cuda") -> dict
                 continue
             go = f64(out[b, :R])
             assert np.all(np.isfinite(go)), "prefill wrote non-finite values"
-            errs[f"prefill[{b}]"] = rel_err(go, ref[b, :R])
-            print(f"prefill[{b}] parity {errs[f'prefill[{b}]']:.3e} rms-only "
+            errs[f"prefill[{b}]"] = fwd_err(go, ref[b, :R], case.dtype)
+            parts = fwd_parts(go, ref[b, :R], case.dtype)
+            print(f"prefill[{b}] parity {errs[f'prefill[{b}]']:.3e} (element {parts['elem']:.3e} "
+                  f"scale {parts['scale']:.2e} bias {parts['bias']:.2e} per head "
+                  f"{parts['group_scale']:.1e}/{parts['group_bias']:.1e}) rms-only "
                   f"{rms_err(go, ref[b, :R]):.3e} tensor-wide {tensor_err(go, ref[b, :R]):.3e}",
                   flush=True)
             gl = f64(lse[b, :, :R])
@@ -145,14 +184,16 @@ def run_and_check(case: Case, check_prefill: bool = True, device="cuda") -> dict
     ws_bytes = skv.speechkv_decode_workspace_bytes(B, Hq, Hkv, D,
                                                    bound(max(x["clen"]) + case.decode_steps),
                                                    case.num_splits)
-    ws = torch.empty(max(ws_bytes, 16) // 4 + 4, dtype=torch.float32, device=dev)
+    ws, ws_guard = guarded((max(ws_bytes, 16) // 4,), torch.float32, dev)
     for s in range(case.decode_steps):
         lens = [c + s + 1 for c in x["clen"]]
-        out = torch.full((B, Hq, D), float("nan"), dtype=x["dt"], device=dev)
+        out, out_guard = guarded((B, Hq, D), x["dt"], dev)
         skv.speechkv_decode_attn(t(qd[s]), cache, torch.tensor(lens, dtype=torch.int32, device=dev),
                                  bound(max(lens)), out, k_new=t(kn[s]), v_new=t(vn[s]), scale=scale,
                                  num_splits=case.num_splits, workspace=ws)
         torch.cuda.synchronize()
+        out_guard(f"decode out, step {s}")
+        ws_guard(f"decode workspace, step {s}")
         for b in range(B):
             kext[b].append(f64(kn[s, b]))
             vext[b].append(f64(vn[s, b]))
@@ -163,12 +204,14 @@ def run_and_check(case: Case, check_prefill: bool = True, device="cuda") -> dict
             K[b, :lens[b]] = np.array(kext[b])
             V[b, :lens[b]] = np.array(vext[b])
         ref, _ = oracle.decode(f64(qd[s]), K, V, lens, scale)
-        errs[f"decode[{s}]"] = rel_err(f64(out), ref)
+        errs[f"decode[{s}]"] = fwd_err(f64(out), ref, case.dtype)
         # the new token landed in its slot
         for b in range(B):
             gk, gv = gather(cache, b, lens[b])
             assert torch.equal(gk[-1].cpu(), kn[s, b]) and torch.equal(gv[-1].cpu(), vn[s, b])
 
+    # the spare pages are still untouched after the decode steps stored their tokens
+    assert torch.isnan(cache.k_pages[spare].float()).all() and torch.isnan(cache.v_pages[spare].float()).all()
     bad = {k: v for k, v in errs.items() if v > tol}
     assert not bad, f"{case}: errors above tolerance {tol}: {bad}"
     return errs

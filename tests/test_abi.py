@@ -177,6 +177,17 @@ def test_pool_rejects(kw, code):
     assert pool(**kw) == code
 
 
+@pytest.mark.parametrize("kw,ckw", [
+    (dict(clen=FAKE + 256), {}), (dict(clen=FAKE + (3 << 24)), {}), (dict(clen=RAW + 64), {}),
+    (dict(gate=FAKE + (1 << 24) + 1024), {}), ({}, dict(block_table=FAKE + 2048)),
+    ({}, dict(v_pages=FAKE + 4096)), (dict(clen=FAKE + (2 << 24) + 16), {}),
+])
+def test_pool_rejects_overlaps(kw, ckw):
+    """The pools and cache_len_out may not overlap the raw K/V, the gate, the
+    block table, the span lengths or each other."""
+    assert pool(c=cache(**ckw), **kw) == E_ALIAS
+
+
 HID = FAKE + (14 << 24)
 
 
@@ -237,6 +248,33 @@ def test_decode_rejects(kw, code):
     assert decode(**kw) == code
 
 
+Q, CLEN, OUT, WS = FAKE + (9 << 24), FAKE + (10 << 24), FAKE + (11 << 24), FAKE + (14 << 24)
+KN, VN = FAKE + (15 << 24), FAKE + (16 << 24)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(out=Q + 256), dict(out=FAKE + 4096), dict(out=FAKE + (1 << 24)), dict(out=CLEN - 64),
+    dict(out=FAKE + (2 << 24)), dict(out=KN, kn=KN - 256, vn=VN),
+    dict(splits=4, ws=Q, ws_bytes=1 << 20), dict(splits=4, ws=OUT - 4096, ws_bytes=1 << 20),
+    dict(splits=4, ws=FAKE + 8192, ws_bytes=1 << 20),
+    dict(kn=FAKE + 1024, vn=VN), dict(kn=KN, vn=FAKE + (1 << 24) + 512),
+    dict(kn=KN, vn=VN, q=FAKE + 2048), dict(kn=KN, vn=VN, clen=FAKE + (1 << 24)),
+])
+def test_decode_rejects_overlaps(kw):
+    """out, the split partials and (with a new token to store) the page pools
+    may not overlap anything the step reads or each other."""
+    assert decode(**kw) == E_ALIAS
+
+
+def test_decode_pools_written_only_with_a_new_token():
+    # the block table inside a pool is only an error when the pool is written
+    c = cache(block_table=FAKE + 4096)
+    assert decode(c=c, kn=KN, vn=VN) == E_ALIAS
+    assert decode(c=cache(v_pages=FAKE + 8192), kn=KN, vn=VN) == E_ALIAS
+
+
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(q=None), E_ARG), (dict(out=None), E_ARG), (dict(q_len=59), E_ARG), (dict(mode=2), E_ARG),
     (dict(w=0), E_ARG), (dict(hq=6), E_UNS), (dict(hq=5), E_ARG), (dict(lse=FAKE + 2), E_ARG),
@@ -245,6 +283,19 @@ def test_decode_rejects(kw, code):
 ])
 def test_prefill_rejects(kw, code):
     assert prefill(**kw) == code
+
+
+@pytest.mark.parametrize("kw", [
+    dict(out=FAKE + (12 << 24) + 512), dict(out=FAKE + 64), dict(out=FAKE + (1 << 24) + 64),
+    dict(out=FAKE + (2 << 24)), dict(out=FAKE + (3 << 24) + 64), dict(lse=FAKE + (12 << 24)),
+    dict(lse=FAKE + (13 << 24) + 128), dict(lse=FAKE + 1024), dict(lse=FAKE + (3 << 24)),
+])
+def test_prefill_rejects_overlaps(kw):
+    """out and lse may not overlap the queries, the pools, the block table,
+    the span lengths or each other."""
+    assert prefill(**kw) == E_ALIAS
+    assert prefill_seg(**{k: (v if v != FAKE + (3 << 24) + 64 and v != FAKE + (3 << 24) else SEG)
+                          for k, v in kw.items()}) == E_ALIAS
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -285,8 +336,8 @@ def test_binding_constants_match_header():
     import re
     defs = dict(re.findall(r"#define SPEECHKV_(\w+) \(?(-?\d+)\)?", open(HEADER).read()))
     for name in ("OK", "ERR_INVALID_ARG", "ERR_UNSUPPORTED", "ERR_WORKSPACE", "ERR_ALIAS", "ERR_HIP",
-                 "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START", "MAX_WINDOW",
-                 "MAX_SEGMENTS"):
+                 "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START",
+                 "MAX_WINDOW", "MAX_SEGMENTS"):
         assert int(defs[name]) == getattr(skv, name), name
 
 
@@ -475,3 +526,30 @@ def test_backward_segment_calls_check_their_tables():
                                            FAKE + (20 << 24), FAKE + (21 << 24), 60, FAKE + (26 << 24),
                                            FAKE + (27 << 24), None, None, 0, None)
     assert st == E_ARG
+
+
+# ------------------------------------------------ valid calls pass validation
+
+NO_GPU = pytest.mark.skipif(__import__("torch").cuda.device_count() > 0,
+                            reason="valid calls would launch kernels on the fake pointers")
+
+
+@NO_GPU
+def test_valid_calls_pass_every_check():
+    """Valid arguments (the fake, non-overlapping layout above) get past every
+    host check, so on a machine without a GPU the call fails only at the
+    device (HIP error).  This guards the overlap checks against flagging a
+    legitimate call, e.g. decode reading and writing the same page pools when
+    it stores the new token."""
+    E_HIP = skv.ERR_HIP
+    assert decode() == E_HIP
+    assert decode(kn=KN, vn=VN) == E_HIP
+    assert decode(kn=KN, vn=VN, splits=4, ws=WS, ws_bytes=1 << 20) == E_HIP
+    assert prefill() == E_HIP and prefill(lse=FAKE + (20 << 24)) == E_HIP
+    assert prefill_seg() == E_HIP
+    assert pool() == E_HIP and pool(clen=FAKE + (20 << 24), gate=FAKE + (21 << 24)) == E_HIP
+    assert pool_seg() == E_HIP
+    assert fused() == E_HIP
+    assert prefill_bwd() == E_HIP
+    assert pool_bwd() == E_HIP
+    assert pool_hidden() == E_HIP

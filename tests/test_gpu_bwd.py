@@ -8,9 +8,11 @@ stage's own inputs:
     dO; the kernel uses the forward's stored output and LSE, as in training;
   - speechkv_pool_kv_bwd against oracle.pool_bwd on the same raw K/V, gate and
     fp32 dK^/dV^.
-The whole chain is then checked end to end for dQ against the all-fp64 oracle
-chain, and for the invariant that a window's raw-key gradients add up to its
-pooled gradient.  Tolerances: tests/helpers.py GRAD_TOL.
+The whole chain is then checked end to end (dQ, raw dK, raw dV and du)
+against the all-fp64 oracle chain, and for the invariant that a window's
+raw-key gradients add up to its pooled gradient.  The benchmark's training
+layer (1596 rows over 471 keys, 8 sequences, 16/8 heads) is checked in its own
+launch configuration.  Tolerances: tests/helpers.py GRAD_TOL.
 """
 import math
 
@@ -23,6 +25,7 @@ from gpu_case import Case, build
 from helpers import GRAD_TOL, f64, gather, grad_err
 from paper_2607_06827_amd import inputs
 from paper_2607_06827_amd import speechkv as skv
+from paper_2607_06827_amd.workload import TrainJob
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -209,15 +212,21 @@ def test_training_step_end_to_end(name):
     u64 = None if x["u"] is None else f64(x["u"])
     kh, vh, _ = oracle.pool(f64(x["k_raw"]), f64(x["v_raw"]), case.P, case.T, case.N, case.w,
                             case.layer, case.l0, u64, cap)
-    rq, _, _ = oracle.attention_bwd(f64(x["q"]), kh, vh, case.P, case.T, case.N, case.w, case.layer,
-                                    case.l0, f64(dout), case.mode, D ** -0.5)
+    rq, rkh, rvh = oracle.attention_bwd(f64(x["q"]), kh, vh, case.P, case.T, case.N, case.w,
+                                        case.layer, case.l0, f64(dout), case.mode, D ** -0.5)
+    rk, rv, ru = oracle.pool_bwd(f64(x["k_raw"]), f64(x["v_raw"]), case.P, case.T, case.N, case.w,
+                                 case.layer, case.l0, u64, rkh, rvh)
     tol = GRAD_TOL[case.dtype]
     w_eff = case.w if case.layer >= case.l0 else 1
     for b in range(B):
         R = case.P[b] + case.T[b] + case.N[b]
-        e = grad_err(f64(dq[b, :R]), rq[b, :R])
-        print(f"  seq {b}: dq vs the fp64 chain {e:.2e}", flush=True)
-        assert e <= tol["dq"]
+        e = {"dq": grad_err(f64(dq[b, :R]), rq[b, :R]),
+             "dk": grad_err(f64(dkr[b, :R]), rk[b, :R]),
+             "dv": grad_err(f64(dvr[b, :R]), rv[b, :R])}
+        print(f"  seq {b} vs the fp64 chain: " + " ".join(f"{k} {v:.2e}" for k, v in e.items()),
+              flush=True)
+        assert e["dq"] <= tol["dq"]
+        assert e["dk"] <= tol["chain"] and e["dv"] <= tol["chain"]
         sums = np.zeros((x["clen"][b], Hkv, D))
         gk = f64(dkr[b, :R])
         for i in range(-(-case.T[b] // w_eff)):
@@ -230,3 +239,41 @@ def test_training_step_end_to_end(name):
         # each frame gradient is rounded once (2^-9 of its size at bf16)
         assert np.max(np.abs(sums[P:P + nW] - ref)) <= (1e-2 if case.dtype == "bf16" else 1e-5) * \
             max(1.0, np.max(np.abs(gk)))
+    eu = grad_err(f64(du), ru)
+    print(f"  du vs the fp64 chain {eu:.2e}", flush=True)
+    assert eu <= tol["chain"]
+
+
+def test_training_backward_at_benched_shape():
+    """The training layer the benchmark times (workload.TrainJob on the 1596-row
+    workload: 8 sequences, 32 + 1500 + 64 rows over 471 keys, 16/8 heads,
+    d = 128, w = 4), run in that launch configuration.  Attention backward on
+    sequences 0, 3 and 7 against the oracle over the GPU's cache rows; pooling
+    backward on the whole batch (du sums over every sequence) against the
+    oracle on the GPU's dK^/dV^."""
+    wl = inputs.PREFILL_1500
+    tj = TrainJob(wl)
+    tj.run_forward()
+    tj.run_backward()
+    torch.cuda.synchronize()
+    f = tj.fwd
+    tol = GRAD_TOL["bf16"]
+    P, T, N, R, L = wl.prefix_len, wl.speech_len, wl.suffix_len, wl.prefill_len, tj.clen
+    assert L == 471
+    for b in (0, 3, 7):
+        gk, gv = gather(f.caches[0], b, L)
+        rq, rk, rv = oracle.attention_bwd(f64(f.q_prefill[0][b:b + 1]), f64(gk)[None],
+                                          f64(gv)[None], [P], [T], [N], tj.w, tj.layer, f.l0,
+                                          f64(tj.dout[b:b + 1]), 0, f.scale)
+        e = {"dq": grad_err(f64(tj.dq[b]), rq[0, :R]), "dk": grad_err(f64(tj.dk_hat[b]), rk[0, :L]),
+             "dv": grad_err(f64(tj.dv_hat[b]), rv[0, :L])}
+        print(f"  seq {b}: " + " ".join(f"{k} {v:.2e}" for k, v in e.items()), flush=True)
+        assert e["dq"] <= tol["dq"] and e["dk"] <= tol["dkv_hat"] and e["dv"] <= tol["dkv_hat"]
+    B = wl.batch
+    rk, rv, ru = oracle.pool_bwd(f64(f.k_raw[0]), f64(f.v_raw[0]), [P] * B, [T] * B, [N] * B, tj.w,
+                                 tj.layer, f.l0, f64(f.gate[0]), f64(tj.dk_hat), f64(tj.dv_hat))
+    ek = grad_err(f64(tj.dk_raw), rk)
+    ev = grad_err(f64(tj.dv_raw), rv)
+    eu = grad_err(f64(tj.du), ru)
+    print(f"  pooling backward, whole batch: dk {ek:.2e} dv {ev:.2e} du {eu:.2e}", flush=True)
+    assert ek <= tol["dkv_raw"] and ev <= tol["dkv_raw"] and eu <= tol["du"]

@@ -14,7 +14,7 @@ import torch
 
 import oracle
 from gpu_case import Case, build
-from helpers import TOL, f64, gather, rel_err
+from helpers import TOL, f64, fwd_err, gather
 from paper_2607_06827_amd import inputs
 from paper_2607_06827_amd import speechkv as skv
 from paper_2607_06827_amd.workload import Job
@@ -120,12 +120,12 @@ def check_oracle(case: Case, x, res):
         L, R = int(oclen[b]), case.P[b] + case.T[b] + case.N[b]
         if L:
             gk, gv = gather(f["cache"], b, L)
-            errs[f"pool_k[{b}]"] = rel_err(f64(gk), kh[b, :L])
-            errs[f"pool_v[{b}]"] = rel_err(f64(gv), vh[b, :L])
+            errs[f"pool_k[{b}]"] = fwd_err(f64(gk), kh[b, :L], case.dtype)
+            errs[f"pool_v[{b}]"] = fwd_err(f64(gv), vh[b, :L], case.dtype)
         if R:
             go = f64(f["out"][b, :R])
             assert np.all(np.isfinite(go))
-            errs[f"prefill[{b}]"] = rel_err(go, ref[b, :R])
+            errs[f"prefill[{b}]"] = fwd_err(go, ref[b, :R], case.dtype)
             gl, rl = f64(f["lse"][b, :, :R]), ref_lse[b, :, :R]
             assert np.array_equal(np.isneginf(gl), np.isneginf(rl))
     bad = {k: e for k, e in errs.items() if not e <= tol}
@@ -186,6 +186,6 @@ def test_fused_workloads(wl_name, layers):
     if wl_name == "prefill":
         from helpers import oracle_prefill_for
         ref, _ = oracle_prefill_for(f, 0, list(range(wl.batch)))
-        err = rel_err(f64(f.prefill_out), ref)
+        err = fwd_err(f64(f.prefill_out), ref, "bf16")
         print(f"{wl.name}: fused prefill parity {err:.3e}", flush=True)
         assert err <= TOL["bf16"]

@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import oracle
-from helpers import TOL, f64, gather, rel_err
+from helpers import TOL, f64, fwd_err, gather
 from paper_2607_06827_amd import inputs
 from paper_2607_06827_amd import speechkv as skv
 
@@ -71,8 +71,8 @@ def test_decode_independent_of_split_count():
     kh, vh, _ = oracle.pool(f64(x["k"]), f64(x["v"]), x["P"], x["T"], x["N"], x["w"], 0, 0, f64(x["u"]))
     ref, _ = oracle.decode(f64(q), kh, vh, x["clen"], x["D"] ** -0.5)
     for s, o in outs.items():
-        assert rel_err(f64(o), f64(outs[1])) <= TOL["bf16"], s
-        assert rel_err(f64(o), ref) <= TOL["bf16"], s
+        assert fwd_err(f64(o), f64(outs[1]), "bf16") <= TOL["bf16"], s
+        assert fwd_err(f64(o), ref, "bf16") <= TOL["bf16"], s
 
 
 @pytest.mark.parametrize("mode", [0, 1])
@@ -88,8 +88,10 @@ def test_constant_values_give_constant_outputs(mode):
         if mode == 0 and x["P"][b] == 0:  # rows before the first window closes see nothing
             assert torch.all(o[:x["w"] - 1] == 0)
             o = o[x["w"] - 1:]
-        # P is rounded to bf16 before the P.V product: |o - 1| is a few ulp
-        assert torch.all((o - 1.0).abs() <= 1e-2), (b, mode)
+        # P is rounded to bf16 before the P.V product while the row sum takes
+        # the unrounded weights, so the fp32 ratio is within 2^-9 of 1 and
+        # rounds to 1 or to 1 - 2^-8 (the bf16 neighbour below 1)
+        assert torch.all((o - 1.0).abs() <= 2.0 ** -8), (b, mode)
     assert torch.all(d.float() == 1.0)  # decode sums p and p*1 identically
 
 
@@ -102,7 +104,7 @@ def test_decode_equals_prefill_row():
     d = decode(x, q, x["clen"])
     torch.cuda.synchronize()
     for b in range(x["B"]):
-        assert rel_err(f64(d[b]), f64(out[b, last[b]])) <= TOL["bf16"]
+        assert fwd_err(f64(d[b]), f64(out[b, last[b]]), "bf16") <= TOL["bf16"]
 
 
 def test_page_placement_does_not_matter():

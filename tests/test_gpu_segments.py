@@ -15,7 +15,7 @@ import torch
 
 import oracle
 from oracle import segments as seg
-from helpers import GRAD_TOL, TOL, f64, gather, grad_err, rel_err
+from helpers import GRAD_TOL, TOL, f64, fwd_err, gather, grad_err
 from paper_2607_06827_amd import inputs
 from paper_2607_06827_amd import speechkv as skv
 
@@ -64,7 +64,8 @@ def check(segs, w=4, layer=1, l0=0, mode=0, **kw):
     x = build(segs, w=w, layer=layer, l0=l0, **kw)
     clen, out, lse = run_segments(x, segs, w, layer, l0, mode)
     assert clen == x["clen"]
-    tol = TOL["bf16" if x["dt"] == torch.bfloat16 else "f32"]
+    dts = "bf16" if x["dt"] == torch.bfloat16 else "f32"
+    tol = TOL[dts]
     u64 = None if x["u"] is None else f64(x["u"])
     kh, vh, oclen = seg.pool(f64(x["k"]), f64(x["v"]), segs, w, layer, l0, u64)
     assert oclen.tolist() == x["clen"]
@@ -75,8 +76,8 @@ def check(segs, w=4, layer=1, l0=0, mode=0, **kw):
         L, R = x["clen"][b], x["rows"][b]
         if L:
             gk, gv = gather(x["cache"], b, L)
-            errs[f"pool_k[{b}]"] = rel_err(f64(gk), kh[b, :L])
-            errs[f"pool_v[{b}]"] = rel_err(f64(gv), vh[b, :L])
+            errs[f"pool_k[{b}]"] = fwd_err(f64(gk), kh[b, :L], dts)
+            errs[f"pool_v[{b}]"] = fwd_err(f64(gv), vh[b, :L], dts)
             # text rows are copies, bit for bit
             slots, _ = seg.layout(s, w if layer >= l0 else 1)
             for c, (first, n, _, _) in enumerate(slots):
@@ -85,7 +86,7 @@ def check(segs, w=4, layer=1, l0=0, mode=0, **kw):
         if R:
             go = f64(out[b, :R])
             assert np.all(np.isfinite(go))
-            errs[f"prefill[{b}]"] = rel_err(go, ref[b, :R])
+            errs[f"prefill[{b}]"] = fwd_err(go, ref[b, :R], dts)
             gl, rl = f64(lse[b, :, :R]), ref_lse[b, :, :R]
             assert np.array_equal(np.isneginf(gl), np.isneginf(rl))
             fin = np.isfinite(rl)
@@ -184,7 +185,7 @@ def test_decode_after_segment_pooling():
         K[b, clen[b]] = f64(kn[b])
         V[b, clen[b]] = f64(vn[b])
     ref, _ = oracle.decode(f64(q), K, V, lens, D ** -0.5)
-    assert rel_err(f64(out), ref) <= TOL["bf16"]
+    assert fwd_err(f64(out), ref, "bf16") <= TOL["bf16"]
 
 
 def test_multi_turn_workload():

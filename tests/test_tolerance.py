@@ -9,12 +9,23 @@ kernel from a wrong one.  Under the bound the tests apply
 half of the budget (the rounding of the cached values passes into outputs
 whatever their size), while a mask that shows each speech row one window too
 early uses more than the whole budget.
+
+That per-element bound alone would pass an output scaled by (1 + e) or
+shifted by e * rms for any e below the tolerance.  The forward checks
+therefore also bound the scale <x, ref> / <ref, ref> - 1 and the bias
+mean(x - ref) / rms(ref) of each head's vectors taken together (tightly:
+rounding averages out) and of each vector alone (loosely: a small vector
+that averages larger rows keeps their rounding) (helpers.fwd_err).  A planted
+1% scale or bias error, or 0.5% on one head, passes rel_err and fails fwd_err.
 """
 import numpy as np
 import torch
 
+import pytest
+
 import oracle
-from helpers import TOL, rel_err, rms_err
+from helpers import (BIAS_TOL, GROUP_BIAS_TOL, GROUP_SCALE_TOL, SCALE_TOL, TOL, bias_err, fwd_err,
+                     group_errs, rel_err, rms_err, scale_err)
 from paper_2607_06827_amd import inputs
 
 
@@ -43,3 +54,62 @@ def test_exact_bf16_result_against_both_bounds():
     wrong, _ = oracle.attention(f(q), kh, vh, P, T, N, wl.w, 0, 0, 1, scale)
     rows = slice(wl.prefix_len, wl.prefix_len + wl.speech_len)
     assert rel_err(wrong[:, rows], ref[:, rows]) > 1.0
+
+
+def exact_rounded(wl, B):
+    """(exactly rounded bf16 output, fp64 reference, rows, pooled K, pooled V)."""
+    wl = wl.with_(batch=B)
+    k, v = inputs.raw_kv(wl, 0)
+    u = inputs.gate(wl, 0)
+    q = inputs.prefill_q(wl, 0)
+    f = lambda t: t.double().numpy()
+    P, T, N = [wl.prefix_len] * B, [wl.speech_len] * B, [wl.suffix_len] * B
+    kh, vh, _ = oracle.pool(f(k), f(v), P, T, N, wl.w, 0, 0, f(u))
+    scale = wl.head_dim ** -0.5
+    ref, _ = oracle.attention(f(q), kh, vh, P, T, N, wl.w, 0, 0, 0, scale)
+    exact, _ = oracle.attention(f(q), bf16(kh), bf16(vh), P, T, N, wl.w, 0, 0, 0, scale)
+    R = wl.prefix_len + wl.speech_len + wl.suffix_len
+    return bf16(exact)[:, :R], ref[:, :R], kh, vh
+
+
+@pytest.mark.parametrize("name", ["LAYER_30S", "PREFILL_1500"])
+def test_scale_and_bias_bounds_hold_for_exact_rounding(name):
+    """Exact rounding (of the output and of the stored pooled rows) stays well
+    inside every scale and bias bound."""
+    stored, ref, kh, vh = exact_rounded(getattr(inputs, name), 2 if name == "PREFILL_1500" else 4)
+    for x, r in ((stored, ref), (bf16(kh), kh), (bf16(vh), vh)):
+        assert 0 < scale_err(x, r) <= SCALE_TOL["bf16"] / 3
+        assert 0 < bias_err(x, r) <= BIAS_TOL["bf16"] / 2
+        gs, gb, _ = group_errs(x, r)
+        assert gs <= GROUP_SCALE_TOL["bf16"] / 4 and gb <= GROUP_BIAS_TOL["bf16"] / 4
+        assert fwd_err(x, r, "bf16") < 0.5 * TOL["bf16"]
+
+
+def test_planted_scale_and_bias_errors_fail_fwd_err():
+    """A 1% scale error and a bias of 1% of each vector's RMS, planted on the
+    exactly rounded output, pass the per-element bound and fail fwd_err."""
+    stored, ref, _, _ = exact_rounded(inputs.LAYER_30S, 4)
+    tol = TOL["bf16"]
+    scaled = stored * 1.01
+    assert rel_err(scaled, ref) < tol
+    assert group_errs(scaled, ref)[0] > 5 * GROUP_SCALE_TOL["bf16"]
+    assert fwd_err(scaled, ref, "bf16") > tol
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    shifted = stored + 0.01 * rms
+    assert rel_err(shifted, ref) < tol
+    assert bias_err(shifted, ref) > 2 * BIAS_TOL["bf16"]
+    assert fwd_err(shifted, ref, "bf16") > tol
+    # a scale error of half a percent on one head only is still caught
+    one = stored.copy()
+    one[:, :, 3] *= 1.005
+    assert rel_err(one, ref) < tol and fwd_err(one, ref, "bf16") > tol
+
+
+def test_fp32_is_gated_by_the_rms_form():
+    """fp32 outputs are checked against max|x - ref| / rms(ref) <= 1e-4, the
+    stated form, with no magnitude term."""
+    ref = np.random.default_rng(0).standard_normal((50, 64))
+    x = ref + 2e-4 * np.abs(ref)  # within 1e-4 of |ref| + rms per element
+    assert rel_err(x, ref) <= TOL["f32"] * 2.01
+    assert fwd_err(x, ref, "f32") > TOL["f32"]
+    assert fwd_err(ref + 5e-5 * np.sign(ref) * 0.5, ref, "f32") <= TOL["f32"]
