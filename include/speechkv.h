@@ -34,9 +34,10 @@
  * --------------------------------
  * - Pointers documented as "device" point into GPU memory of the current HIP
  *   device; pointers documented as "host" point into CPU memory.  The caller
- *   owns every buffer.  The library allocates nothing, frees nothing, keeps no
- *   mutable global state and never synchronises; it is safe to call from
- *   several host threads.
+ *   owns every buffer.  The library allocates nothing, frees nothing and
+ *   never synchronises; it is safe to call from several host threads.  Its
+ *   only global state is the per-device address of the static scratch of
+ *   speechkv_decode_attn_noalloc, looked up once per device.
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   Work is enqueued asynchronously on it.
  * - Every argument is validated on the host before anything is enqueued.  A
@@ -72,6 +73,7 @@ extern "C" {
 #define SPEECHKV_ERR_WORKSPACE (-3)   /* workspace missing or too small       */
 #define SPEECHKV_ERR_ALIAS (-4)       /* a buffer written overlaps one read or another written */
 #define SPEECHKV_ERR_HIP (-5)         /* the HIP runtime refused a launch     */
+#define SPEECHKV_ERR_SCRATCH (-6)     /* needs more than the static scratch   */
 
 /* Element types. */
 #define SPEECHKV_DTYPE_F32 0
@@ -81,6 +83,10 @@ extern "C" {
  * largest number of rows (raw_len, q_len) is INT32_MAX - SPEECHKV_MAX_WINDOW:
  * with these bounds no window count ceil(T / w) overflows 32-bit arithmetic. */
 #define SPEECHKV_MAX_WINDOW 65536
+
+/* Bytes of the static device scratch of speechkv_decode_attn_noalloc (one
+ * copy per GPU, held until the process ends): 16 MiB. */
+#define SPEECHKV_NOALLOC_SCRATCH_BYTES 16777216
 
 /* Largest number of segments one sequence may have (speechkv_segments):
  * every kernel that reads a segment table scans a sequence's segments. */
@@ -318,6 +324,36 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
                          const void* k_new, const void* v_new, float scale,
                          int32_t num_splits, void* out, void* workspace,
                          size_t workspace_bytes, void* stream);
+
+/*
+ * speechkv_decode_attn_noalloc - speechkv_decode_attn for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops and
+ * harnesses that forbid hipMalloc).  Same arguments, results and errors as
+ * speechkv_decode_attn, bit for bit, except that there is no workspace: the
+ * split partials go to a static device array of
+ * SPEECHKV_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs
+ * on, until the process ends.
+ *
+ * - The call allocates and frees nothing.  The first call on a device looks
+ *   up that device's copy of the array (with the device current) and keeps
+ *   its address; later calls reuse it.
+ * - Every call on one GPU shares that GPU's array, and the array keeps the
+ *   last call's contents.  Nothing in it has to start at zero: every split
+ *   writes its whole partial before the merge reads it.  Calls that overlap
+ *   in time on one GPU (different streams, or host threads without ordering)
+ *   race on the array and give wrong results; order them on one stream.
+ * - SPEECHKV_ERR_SCRATCH: the step needs more than
+ *   SPEECHKV_NOALLOC_SCRATCH_BYTES of split partials
+ *   (speechkv_decode_workspace_bytes(...) above it).  The automatic split
+ *   count (num_splits = 0) never does: it keeps the split grid at about 1024
+ *   blocks, whose partials take at most 8.5 MiB.  Nothing is enqueued.
+ * - SPEECHKV_ERR_HIP: the device's array could not be looked up.
+ */
+int speechkv_decode_attn_noalloc(const void* q, int32_t batch, int32_t num_q_heads,
+                                 const speechkv_paged_kv* cache,
+                                 const int32_t* cache_len, int32_t max_cache_len,
+                                 const void* k_new, const void* v_new, float scale,
+                                 int32_t num_splits, void* out, void* stream);
 
 /*
  * speechkv_prefill_attn - full-resolution queries over the compressed cache,

@@ -1,16 +1,26 @@
 // C-ABI host layer of libspeechkv: argument validation, grid sizing and
 // dispatch to the kernels.  Every check runs before the first HIP call, so a
-// call that returns an error has enqueued nothing.  No allocation, no global
-// mutable state, no synchronisation.
+// call that returns an error has enqueued nothing.  No allocation and no
+// synchronisation.  The only global state is the per-device address of the
+// static scratch array of speechkv_decode_attn_noalloc, set once per device.
 #include "../../include/speechkv.h"
 
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 
 #include "kernels.hpp"
 #include "kernels_bwd.hpp"
 #include "kernels_fused.hpp"
+
+// Split partials of speechkv_decode_attn_noalloc.  Each GPU holds its own
+// copy for the life of the process; every call on that GPU shares it.  The
+// name is a host-side stand-in for the array, never a device address: host
+// code uses only the address hipGetSymbolAddress returns for the current
+// device, kept per device below.
+static __device__ __align__(256) unsigned char scratch[SPEECHKV_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -124,6 +134,32 @@ bool aliased(const Region* wr, int nw, const Region* rd, int nr) {
   return false;
 }
 
+constexpr int kMaxDevices = 256;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (with that device current) and kept.
+hipError_t device_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress((void**)&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -203,6 +239,7 @@ const char* speechkv_status_string(int status) {
     case SPEECHKV_ERR_WORKSPACE: return "workspace missing or too small";
     case SPEECHKV_ERR_ALIAS: return "a buffer written overlaps one read or another written";
     case SPEECHKV_ERR_HIP: return "HIP runtime error";
+    case SPEECHKV_ERR_SCRATCH: return "the problem needs more than the library's static scratch holds";
     default: return "unknown status";
   }
 }
@@ -428,6 +465,25 @@ int speechkv_decode_attn(const void* q, int32_t batch, int32_t num_q_heads,
   if (need && (!workspace || workspace_bytes < need || !aligned16(workspace))) return SPEECHKV_ERR_WORKSPACE;
   return decode_attn_impl(q, batch, num_q_heads, cache, cache_len, max_cache_len, k_new, v_new,
                           scale, splits, out, workspace, need, stream);
+}
+
+int speechkv_decode_attn_noalloc(const void* q, int32_t batch, int32_t num_q_heads,
+                                 const speechkv_paged_kv* cache, const int32_t* cache_len,
+                                 int32_t max_cache_len, const void* k_new, const void* v_new,
+                                 float scale, int32_t num_splits, void* out, void* stream) {
+  int32_t splits = 0;
+  size_t need = 0;
+  const int st = check_decode(q, batch, num_q_heads, cache, cache_len, max_cache_len, k_new, v_new,
+                              scale, num_splits, out, &splits, &need);
+  if (st) return st;
+  if (need > (size_t)SPEECHKV_NOALLOC_SCRATCH_BYTES) return SPEECHKV_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (need) {
+    const hipError_t e = device_scratch(&ws);
+    if (e != hipSuccess) return SPEECHKV_ERR_HIP;
+  }
+  return decode_attn_impl(q, batch, num_q_heads, cache, cache_len, max_cache_len, k_new, v_new,
+                          scale, splits, out, ws, need, stream);
 }
 
 // speechkv_prefill_attn and speechkv_prefill_attn_segments (segs set)

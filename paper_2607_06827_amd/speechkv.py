@@ -28,12 +28,14 @@ ERR_UNSUPPORTED = -2
 ERR_WORKSPACE = -3
 ERR_ALIAS = -4
 ERR_HIP = -5
+ERR_SCRATCH = -6
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MASK_WINDOW_END = 0
 MASK_WINDOW_START = 1
 MAX_WINDOW = 65536  # largest window size the pooling and attention calls take
 MAX_SEGMENTS = 1024  # most segments one sequence of a segment table may have
+NOALLOC_SCRATCH_BYTES = 16 << 20  # static split scratch of speechkv_decode_attn_noalloc, per GPU
 
 LIBRARY_PATH = _LIB_PATH
 
@@ -78,6 +80,9 @@ _lib.speechkv_pool_hidden.restype = ctypes.c_int
 _lib.speechkv_decode_attn.argtypes = [_vp, _i32, _i32, ctypes.POINTER(_PagedKV), _vp, _i32, _vp,
                                       _vp, _f32, _i32, _vp, _vp, _sz, _vp]
 _lib.speechkv_decode_attn.restype = ctypes.c_int
+_lib.speechkv_decode_attn_noalloc.argtypes = [_vp, _i32, _i32, ctypes.POINTER(_PagedKV), _vp, _i32,
+                                              _vp, _vp, _f32, _i32, _vp, _vp]
+_lib.speechkv_decode_attn_noalloc.restype = ctypes.c_int
 _lib.speechkv_prefill_attn.argtypes = [_vp, _i32, _i32, _i32, ctypes.POINTER(_PagedKV),
                                        ctypes.POINTER(_Spans), _i32, _i32, _i32, _i32, _f32, _vp,
                                        _vp, _vp]
@@ -326,6 +331,28 @@ def speechkv_decode_attn(q: torch.Tensor, cache: PagedKV, cache_len: torch.Tenso
                                    max_cache_len, _ptr(k_new), _ptr(v_new), scale, num_splits,
                                    out.data_ptr(), _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "speechkv_decode_attn")
+
+
+def speechkv_decode_attn_noalloc(q: torch.Tensor, cache: PagedKV, cache_len: torch.Tensor,
+                                 max_cache_len: int, out: torch.Tensor,
+                                 k_new: Optional[torch.Tensor] = None,
+                                 v_new: Optional[torch.Tensor] = None,
+                                 scale: Optional[float] = None, num_splits: int = 0,
+                                 stream=None) -> None:
+    """speechkv_decode_attn without a workspace: split partials go to the
+    library's static per-GPU scratch.  Calls that overlap on one GPU race."""
+    for x in (q, out, cache_len) + tuple(t for t in (k_new, v_new) if t is not None):
+        if not x.is_contiguous():
+            raise ValueError("decode tensors must be contiguous")
+    B, Hq, D = q.shape
+    if scale is None:
+        scale = D ** -0.5
+    c = cache._c()
+    st = _lib.speechkv_decode_attn_noalloc(q.data_ptr(), B, Hq, ctypes.byref(c),
+                                           cache_len.data_ptr(), max_cache_len, _ptr(k_new),
+                                           _ptr(v_new), scale, num_splits, out.data_ptr(),
+                                           _stream(stream))
+    _check(st, "speechkv_decode_attn_noalloc")
 
 
 def speechkv_prefill_attn(q: torch.Tensor, cache: PagedKV, spans: Spans, w: int, layer: int,

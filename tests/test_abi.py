@@ -26,6 +26,7 @@ def declared_functions():
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert set(names) == {"speechkv_pool_kv", "speechkv_decode_attn", "speechkv_prefill_attn",
+                          "speechkv_decode_attn_noalloc",
                           "speechkv_pool_hidden", "speechkv_pool_prefill_attn",
                           "speechkv_pool_kv_segments", "speechkv_prefill_attn_segments",
                           "speechkv_compressed_len_segments", "speechkv_prefill_attn_bwd_segments",
@@ -41,7 +42,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5, -6):
         assert skv.speechkv_status_string(code) and skv.speechkv_status_string(code) != "unknown status"
     assert skv.speechkv_status_string(17) == "unknown status"
     assert re.fullmatch(r"\d+\.\d+\.\d+", skv.speechkv_version())
@@ -246,6 +247,20 @@ def test_bad_spans(skw):
 ])
 def test_decode_rejects(kw, code):
     assert decode(**kw) == code
+    # the no-alloc call takes no workspace: the WORKSPACE cases are valid
+    # there (and would reach the device), so only the others are repeated
+    if code != E_WS:
+        assert decode_noalloc(**kw) == code
+
+
+def decode_noalloc(c=None, **kw):
+    a = dict(q=FAKE + (9 << 24), batch=2, hq=4, clen=FAKE + (10 << 24), max_len=100, kn=None,
+             vn=None, scale=0.125, splits=0, out=FAKE + (11 << 24))
+    a.update({k: v for k, v in kw.items() if k in a})
+    c = c or cache()
+    return lib.speechkv_decode_attn_noalloc(a["q"], a["batch"], a["hq"], ctypes.byref(c), a["clen"],
+                                            a["max_len"], a["kn"], a["vn"], a["scale"], a["splits"],
+                                            a["out"], None)
 
 
 Q, CLEN, OUT, WS = FAKE + (9 << 24), FAKE + (10 << 24), FAKE + (11 << 24), FAKE + (14 << 24)
@@ -264,15 +279,33 @@ def test_decode_rejects_overlaps(kw):
     """out, the split partials and (with a new token to store) the page pools
     may not overlap anything the step reads or each other."""
     assert decode(**kw) == E_ALIAS
+    if "ws" not in kw:
+        assert decode_noalloc(**kw) == E_ALIAS
 
 
 def test_decode_pools_written_only_with_a_new_token():
     # the block table inside a pool is only an error when the pool is written
     c = cache(block_table=FAKE + 4096)
     assert decode(c=c, kn=KN, vn=VN) == E_ALIAS
+    assert decode_noalloc(c=c, kn=KN, vn=VN) == E_ALIAS
     assert decode(c=cache(v_pages=FAKE + 8192), kn=KN, vn=VN) == E_ALIAS
 
 
+def test_noalloc_rejects_steps_beyond_its_scratch():
+    """speechkv_decode_attn_noalloc rejects a step whose split partials need
+    more than SPEECHKV_NOALLOC_SCRATCH_BYTES before any HIP call, and the
+    automatic split count never needs that much."""
+    need = skv.speechkv_decode_workspace_bytes(8, 4, 2, 64, 100, 4096)
+    assert need > skv.NOALLOC_SCRATCH_BYTES
+    assert decode_noalloc(batch=8, splits=4096) == skv.ERR_SCRATCH
+    assert "scratch" in skv.speechkv_status_string(skv.ERR_SCRATCH)
+    worst = 0
+    for B in (1, 2, 3, 5, 8, 16, 33, 64, 127, 128, 129, 512, 2048):
+        for H in (1, 2, 4, 8, 16):
+            for L in (0, 64, 1000, 7788, 65536, 1 << 20):
+                for D in (64, 128):
+                    worst = max(worst, skv.speechkv_decode_workspace_bytes(B, 8 * H, H, D, L, 0))
+    assert 0 < worst <= skv.NOALLOC_SCRATCH_BYTES
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -336,8 +369,8 @@ def test_binding_constants_match_header():
     import re
     defs = dict(re.findall(r"#define SPEECHKV_(\w+) \(?(-?\d+)\)?", open(HEADER).read()))
     for name in ("OK", "ERR_INVALID_ARG", "ERR_UNSUPPORTED", "ERR_WORKSPACE", "ERR_ALIAS", "ERR_HIP",
-                 "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START",
-                 "MAX_WINDOW", "MAX_SEGMENTS"):
+                 "ERR_SCRATCH", "DTYPE_F32", "DTYPE_BF16", "MASK_WINDOW_END", "MASK_WINDOW_START",
+                 "MAX_WINDOW", "MAX_SEGMENTS", "NOALLOC_SCRATCH_BYTES"):
         assert int(defs[name]) == getattr(skv, name), name
 
 
@@ -545,6 +578,8 @@ def test_valid_calls_pass_every_check():
     assert decode() == E_HIP
     assert decode(kn=KN, vn=VN) == E_HIP
     assert decode(kn=KN, vn=VN, splits=4, ws=WS, ws_bytes=1 << 20) == E_HIP
+    assert decode_noalloc() == E_HIP
+    assert decode_noalloc(kn=KN, vn=VN, splits=4) == E_HIP
     assert prefill() == E_HIP and prefill(lse=FAKE + (20 << 24)) == E_HIP
     assert prefill_seg() == E_HIP
     assert pool() == E_HIP and pool(clen=FAKE + (20 << 24), gate=FAKE + (21 << 24)) == E_HIP
