@@ -29,7 +29,8 @@
 // K and V tiles are both staged row-major in LDS, double-buffered, behind a
 // branch-free pipeline: block-table entries three tiles ahead, K/V rows two
 // tiles ahead (whole 256-byte rows per wave-wide load), LDS one tile ahead,
-// one barrier per tile.  The bf16 V^T operand comes from the row-major V
+// one barrier per tile.  (bf16: entries two tiles ahead as scalar loads, K/V
+// straight into LDS one tile ahead.)  The bf16 V^T operand comes from the row-major V
 // tile through the gfx950 LDS transpose read (ds_read_b64_tr_b16), so no
 // register transpose is needed at staging; row strides put every staging
 // write and operand read on distinct banks.  The output tile goes back
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
   if (p0 >= rows) return;
   const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = g * G + wave % G;
   const int col = lane & 31, hg = lane >> 5;
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
@@ -428,7 +429,7 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
   const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = g * G + wave % G;
   const int col = lane & 31, hg = lane >> 5;
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
@@ -577,11 +578,17 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   float m_run = neg_inf(), l_run = 0.f;
 
   int pg[2][kLoadsPerWave];  // block-table entries, by tile parity
+  // One direct load fills kRowsPerLoad consecutive keys, aligned to that
+  // count, and pages hold at least 8: the load's keys (clamped to kclamp)
+  // all lie in the page of min(first key, kclamp), a wave-uniform index.  The
+  // entry is read through the constant address space, a scalar load (no kernel
+  // writes the table while this one runs), and the page base is scalar.
   auto table_load = [&](int kt, int* pgs) {
 #pragma unroll
     for (int i = 0; i < kLoadsPerWave; ++i) {
-      const int key = min(kt * kKeys + load_row0(i) + lrow, kclamp);
-      pgs[i] = table_row[min(key >> shift, a.pv.max_pages - 1)];
+      const int row0 = min(kt * kKeys + load_row0(i), kclamp);
+      typedef __attribute__((address_space(4))) const int32_t* const_ptr;
+      pgs[i] = ((const_ptr)table_row)[min(row0 >> shift, a.pv.max_pages - 1)];
     }
   };
   auto tile_load = [&](int kt, const int* pgs, T* sk, T* sv) {
@@ -592,7 +599,7 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
       const int key = min(kt * kKeys + row, kclamp);
       const int e = pgs[i];
       const int page = (e >= 0 && e < num_pages) ? e : 0;  // a bad entry reads an in-range page
-      const int64_t off = page_row<D>(page, g, key & slot_mask, a.pv);
+      const int64_t off = page_row<D>(page, g, 0, a.pv) + (int64_t)((key & slot_mask) * D);
       __builtin_amdgcn_global_load_lds((global_void_ptr)(kpool + off + ((lpos ^ Swz::k(row)) << 3)),
                                        (lds_void_ptr)(sk + load_row0(i) * D), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((global_void_ptr)(vpool + off + ((lpos ^ Swz::v(row)) << 3)),
