@@ -675,19 +675,25 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
       }
       mt = partner_max(mt) * a.scale_log2;  // the scale is > 0
       if (mt > m_run + kSlack) {
-        const float corr = fast_exp2(m_run - mt);
-        l_run *= corr;
+        if (m_run != neg_inf()) {  // (before the first visible key o and l are still 0)
+          const float corr = fast_exp2(m_run - mt);
+          l_run *= corr;
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
+          for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+            for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+        }
         m_run = mt;
       }
+      // a row that sees no key yet has m_run = -inf and every logit -inf:
+      // reference 0 turns each weight into exp2(-inf) = 0
+      const float m_use = m_run == neg_inf() ? 0.f : m_run;
+      // the sum is of the unrounded weights, so that the log-sum-exp output
+      // gives weights that sum to 1 when the backward recomputes them
       float sum = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_run));
-        if (masked) pr[i] = m_run == neg_inf() ? 0.f : pr[i];  // nothing visible yet
+        pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_use));
         sum += pr[i];
       }
       l_run += sum;
