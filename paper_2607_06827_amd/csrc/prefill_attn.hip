@@ -26,15 +26,17 @@
 // v_mfma_f32_32x32x16_bf16 (8 elements per lane per operand), fp32 uses
 // v_mfma_f32_32x32x2_f32 (1 element), both accumulating in fp32.
 //
-// K and V tiles are both staged row-major in LDS, double-buffered, behind a
-// branch-free pipeline: block-table entries three tiles ahead, K/V rows two
-// tiles ahead (whole 256-byte rows per wave-wide load), LDS one tile ahead,
-// one barrier per tile.  (bf16: entries two tiles ahead as scalar loads, K/V
-// straight into LDS one tile ahead.)  The bf16 V^T operand comes from the row-major V
-// tile through the gfx950 LDS transpose read (ds_read_b64_tr_b16), so no
-// register transpose is needed at staging; row strides put every staging
-// write and operand read on distinct banks.  The output tile goes back
-// through LDS so that rows leave as 16-byte stores.
+// K and V tiles are both staged row-major in LDS behind a branch-free
+// pipeline with one barrier per tile.  fp32: double-buffered, block-table
+// entries three tiles ahead, K/V rows two tiles ahead in registers (whole
+// 256-byte rows per wave-wide load), LDS one tile ahead.  bf16: three
+// buffers filled straight from the paged cache by direct loads two tiles
+// ahead, entries three tiles ahead as scalar loads.  The bf16 V^T operand
+// comes from the row-major V tile through the gfx950 LDS transpose read
+// (ds_read_b64_tr_b16), so no register transpose is needed at staging; row
+// strides or swizzles put every staging write and operand read on distinct
+// banks.  The output tile goes back through LDS so that rows leave as
+// 16-byte stores.
 //
 // Blocks are remapped so that the eight XCDs each run a contiguous range of
 // (sequence, head, tile) items: tiles of one (b, g) share that XCD's L2 copy
@@ -324,12 +326,9 @@ typedef __attribute__((address_space(1))) void* global_void_ptr;
 // chunk hit distinct banks) and swz_v(r) = (r mod 4) * 4 (the transposed PV
 // reads of 4 rows x 4 chunks hit distinct banks).  The loading lane picks the
 // global chunk that belongs at its LDS position.  Keys past the visible range
-// load a visible row (finite data that the mask gives zero weight).
-//
-// Pipeline: the block-table entries of tile t load at step t-2, its rows go
-// to LDS at step t-1 (two buffers, each a separate LDS array so that the
-// compiler knows the in-flight direct loads never touch the buffer being
-// read), and every step ends with a full wait and a barrier.
+// load a visible row (finite data that the mask gives zero weight).  Tile
+// buffers are 256-byte aligned, so a lane's fragment addresses differ from
+// one base register by an XOR of the swizzled chunk bits (see attend_tile).
 template <int D>
 struct LdsSwz {
   static constexpr int kChunks = D / 8;  // 16-byte chunks per row
@@ -337,76 +336,274 @@ struct LdsSwz {
   static __device__ __forceinline__ int v(int row) { return (row % (kChunks / 4)) << 2; }
 };
 
-// Waves per SIMD the compiler must fit: three where the registers allow it
-// without spilling (it measured faster than two at the same tile sizes); two
-// when the kernel also pools its tiles (the first frames of the next tile's
-// windows are held in registers across a step).
-template <int D, int G, bool kFused>
-constexpr int lds_kernel_waves() { return kFused || (D == 128 && G == 4) ? 2 : 3; }
+// Byte address of an LDS object (the 32-bit LDS address space).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void_ptr)p; }
 
-// Block shape of the pooling variant: eight waves whatever the group size, so
-// a block owns 256/G query rows.  Every block pools each key tile it reads,
-// so taller blocks pool each tile fewer times over the whole grid, and eight
-// waves share the work of a tile (one pass of D/8-lane units at D = 128).
-template <int G>
-struct FusedShape {
-  static constexpr int kRowBlocks = 8 / G;
-  static constexpr int kWaves = 8;
-  static constexpr int kThreads = 512;
-  static constexpr int kRows = 32 * kRowBlocks;
-};
-template <int G, bool kFused>
-using LdsShape = typename std::conditional<kFused, FusedShape<G>, PrefillShape<G>>::type;
-template <int G, bool kFused>
-constexpr int lds_threads() { return LdsShape<G, kFused>::kThreads; }
+// 16 bytes per lane from sbase + voff (bytes; sbase wave-uniform) into LDS at
+// lds + 16 * lane, issued from inline assembly so that the compiler neither
+// counts nor waits for it: the caller waits with an explicit vector-memory
+// count.  (The compiler cannot tell which LDS object a transposed read
+// touches, and with tracked direct loads it waits for all of them before every
+// such read.)
+__device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
 
-template <bool kFused>
-struct LdsArgs {
-  typedef PrefillArgs type;
-};
-template <>
-struct LdsArgs<true> {
-  typedef PrefillFusedArgs type;
-};
-__device__ __host__ __forceinline__ const PrefillArgs& attn_args(const PrefillArgs& a) { return a; }
-__device__ __host__ __forceinline__ const PrefillArgs& attn_args(const PrefillFusedArgs& a) { return a.at; }
+// 16 bytes at p + kOff into r, untracked like lds_dma16: the caller waits
+// explicitly before r is read.
+template <int kOff, typename F>
+__device__ __forceinline__ void untracked_load16(F& r, const void* p) {
+  static_assert(sizeof(F) == 16, "16-byte fragment");
+  asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "i"(kOff) : "memory");
+}
 
-// kFused = false: K/V tiles come from the paged cache by direct loads.
-// kFused = true: the kernel reads the raw K/V instead and pools each key tile
-// on the fly (Sec. III-C) with the pooling kernel's steps (pool_window.hpp),
-// D/8 lanes per (slot, head) unit: the first four frames of every window of
-// tile t+1 are loaded before the MFMAs of tile t and pooled after them,
-// straight into the other LDS buffer in the layout the direct loads give.
-// The block holding a sequence's last query rows (which see every key) also
-// stores each pooled row into the paged cache, and pools the rows no query
-// sees, so the cache ends up as the pooling kernel would have written it.
-template <int D, int G, bool kFused, bool kRuns>
-__global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G, kFused>())) void prefill_kernel_lds(typename LdsArgs<kFused>::type args) {
-  const PrefillArgs& a = attn_args(args);
+// s_waitcnt immediate: at most n vector-memory operations outstanding, LDS
+// and scalar loads complete (CDNA layout: vmcnt bits 3:0 and 15:14, lgkmcnt
+// 11:8, expcnt 6:4 left at its maximum)
+constexpr int wait_vm_lgkm0(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
+// f(integral_constant<int, i>) for i = 0 .. n-1, unrolled at compile time
+template <int n, int i = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (i < n) {
+    f(std::integral_constant<int, i>());
+    static_for<n, i + 1>(f);
+  }
+}
+
+// Full barrier with no memory fence: waits until at most vm of the wave's
+// (untracked) vector-memory operations are in flight and its LDS reads are
+// done, then joins the block.  Compiler and scheduler fences on both sides
+// keep every LDS access on its side.
+template <int kVm>
+__device__ __forceinline__ void bare_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(kVm));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// One 32-key tile of the online softmax for the 32 query rows of a wave
+// (bf16).  sk / sv: the swizzled row-major K and V tiles in LDS; qf: the
+// wave's query fragments (B operand of S^T = K Q^T); kb: first key of the
+// tile; nvis: keys this lane's row sees, nvis_lo: keys every row of the wave
+// sees.  The K fragments are read three ahead of the S chain, the first V
+// fragments during the softmax and the rest one ahead of the P.V chain.
+template <int D>
+__device__ __forceinline__ void attend_tile(const bf16_bits* sk, const bf16_bits* sv,
+                                            const bf16x8_t (&qf)[D / 16], f32x16_t (&o)[D / 32],
+                                            float& m_run, float& l_run, int kb, int nvis, int nvis_lo,
+                                            int lane, float scale_log2) {
+  typedef Mfma<bf16_bits> M;
+  typedef M::Frag Frag;
+  typedef LdsSwz<D> Swz;
+  typedef __attribute__((address_space(3))) const u16x8_t* lds_frag_ptr;
+  constexpr int kKeys = 32;
+  constexpr int kStep = 16;                 // head-dim elements per QK MFMA
+  constexpr int kQChunks = D / kStep;
+  constexpr int kVFrags = (kKeys / kStep) * (D / 32);
+  const int col = lane & 31, hg = lane >> 5;
+
+  // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query.
+  // K fragment kc of this lane is row col, 16-byte chunk (2kc + hg) ^ swz(col)
+  // = 2kc ^ c0 with c0 = hg ^ swz(col): byte address a0 ^ 32kc.
+  uint32_t a0 = lds_addr(sk + col * D) + ((uint32_t)(hg ^ Swz::k(col)) << 4);
+  asm volatile("" : "+v"(a0));  // one address register, not one per fragment
+  auto kfrag = [&](int kc) __attribute__((always_inline)) {
+    return __builtin_bit_cast(Frag, *(lds_frag_ptr)(uintptr_t)(a0 ^ (uint32_t)(32 * kc)));
+  };
+  f32x16_t st;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) st[i] = 0.f;
+  constexpr int kAhead = kQChunks >= 3 ? 3 : kQChunks;
+  Frag kbuf[kAhead];
+#pragma unroll
+  for (int j = 0; j < kAhead; ++j) kbuf[j] = kfrag(j);
+#pragma unroll
+  for (int kc = 0; kc < kQChunks; ++kc) {
+    const Frag cur = kbuf[kc % kAhead];
+    if (kc + kAhead < kQChunks) kbuf[kc % kAhead] = kfrag(kc + kAhead);
+    st = M::mma(cur, qf[kc], st);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);  // DS reads
+#pragma unroll
+  for (int kc = 0; kc + kAhead < kQChunks; ++kc) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+
+  // A operand of O^T += V^T P^T through the LDS transpose read (see
+  // Mfma<bf16_bits>::load_v): lane (vg, vj) reads key rows 16kk + 4(vg/2) +
+  // vj/4 (and +8), elements 32db + 16(vg%2) + 4(vj%4) .. +3, whose 16-byte
+  // chunk 4db + c1 sits at (4db + c1) ^ swz_v(row) = 4(db ^ s) + c1 (s =
+  // swz_v(row)/4, the same for both rows and every kk): byte address va ^
+  // 64db plus a constant for kk and the second row.
+  const int vg = lane >> 4, vj = lane & 15;
+  const int vr = 4 * (vg >> 1) + (vj >> 2);
+  uint32_t va = lds_addr(sv + vr * D) +
+                (uint32_t)((((Swz::v(vr) >> 2) * 4 + 2 * (vg & 1) + ((vj & 3) >> 1)) << 4) | ((vj & 1) << 3));
+  asm volatile("" : "+v"(va));
+  auto vfrag = [&](int idx) __attribute__((always_inline)) {
+    const int kk = idx / (D / 32), db = idx % (D / 32);
+    const uint32_t al = (va ^ (uint32_t)(64 * db)) + (uint32_t)(kk * 16 * D * 2);
+    const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(uintptr_t)al);
+    const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(uintptr_t)(al + 8 * D * 2));
+    const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
+                       (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
+    return __builtin_bit_cast(Frag, v);
+  };
+  Frag vbuf[2] = {vfrag(0), vfrag(1)};
+  __builtin_amdgcn_sched_barrier(0);  // (issued before the softmax)
+
+  float pr[16];
+  float mt = neg_inf();
+  if (kb + kKeys > nvis_lo) {  // uniform: the tile straddles some row's bound
+    const int lim = nvis - kb - 4 * hg;  // element i is visible iff 8(i/4) + i%4 < lim
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      pr[i] = 8 * (i / 4) + (i % 4) < lim ? st[i] : neg_inf();
+      mt = fmaxf(mt, pr[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      pr[i] = st[i];
+      mt = fmaxf(mt, pr[i]);
+    }
+  }
+  mt = partner_max(mt) * scale_log2;  // the scale is > 0
+  if (mt > m_run + kSlack) {
+    if (m_run != neg_inf()) {  // (before the first visible key o and l are still 0)
+      const float corr = fast_exp2(m_run - mt);
+      l_run *= corr;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+    }
+    m_run = mt;
+  }
+  // a row that sees no key yet has m_run = -inf and every logit -inf:
+  // reference 0 turns each weight into exp2(-inf) = 0
+  const float m_use = m_run == neg_inf() ? 0.f : m_run;
+  // the sum is of the unrounded weights, so that the log-sum-exp output
+  // gives weights that sum to 1 when the backward recomputes them
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    pr[i] = fast_exp2(__builtin_fmaf(pr[i], scale_log2, -m_use));
+    sum += pr[i];
+  }
+  l_run += sum;
+
+  // O^T += V^T P^T over the 32 keys (the key order of the C layout carried
+  // into the V reads), one V fragment ahead of each MFMA
+#pragma unroll
+  for (int kk = 0; kk < kKeys / kStep; ++kk) {
+    const Frag pf = M::pack_p(pr + kk * 8);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const int idx = kk * (D / 32) + db;
+      const Frag cur = vbuf[idx & 1];
+      if (idx + 2 < kVFrags) vbuf[idx & 1] = vfrag(idx + 2);
+      o[db] = M::mma(cur, pf, o[db]);
+    }
+  }
+#pragma unroll
+  for (int idx = 0; idx + 2 < kVFrags; ++idx) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
+}
+
+// Normalises the wave's 32 x D output tile, writes its LSE and stores it:
+// through so (a 32-row tile area of LDS no other wave uses, rows swizzled
+// like K) as 16-byte row stores, or straight from the C layout (so = null).
+template <int D>
+__device__ __forceinline__ void finish_rows(f32x16_t (&o)[D / 32], float m_run, float l_run, bf16_bits* so,
+                                            const PrefillArgs& a, int b, int h, int wrow0, int rows, int lane) {
+  typedef Mfma<bf16_bits> M;
+  typedef LdsSwz<D> Swz;
+  constexpr float kLn2 = 0.6931471805599453f;
+  const int col = lane & 31, hg = lane >> 5;
+  const int p = wrow0 + col;
+  const int hq = a.num_q_heads;
+  const float l_tot = partner_sum(l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (hg == 0 && a.lse && p < rows)
+    a.lse[((int64_t)b * hq + h) * a.q_len + p] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : neg_inf();
+  bf16_bits* out = static_cast<bf16_bits*>(a.out);
+  if (so == nullptr) {  // direct stores of the C layout: four values of a row
+    if (p < rows) {
+      bf16_bits* orow = out + (((int64_t)b * a.q_len + p) * hq + h) * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int ig = 0; ig < 4; ++ig)
+          M::store4(orow + db * 32 + 8 * ig + 4 * hg, o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
+                    o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+    }
+    return;
+  }
+  const int oswz = Swz::k(col);
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int ig = 0; ig < 4; ++ig)
+      M::store4(so + col * D + (((4 * db + ig) ^ oswz) << 3) + 4 * hg, o[db][4 * ig] * inv,
+                o[db][4 * ig + 1] * inv, o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
+  __syncthreads();  // (the same wave reads its tile back: orders its LDS traffic)
+  constexpr int kChunks = Swz::kChunks;
+  constexpr int kRowsPerPass = 64 / kChunks;
+#pragma unroll
+  for (int r0 = 0; r0 < 32; r0 += kRowsPerPass) {
+    const int rr = r0 + lane / kChunks, cch = lane % kChunks;
+    const int out_row = wrow0 + rr;
+    if (out_row < rows) {
+      const uint4 v = *reinterpret_cast<const uint4*>(so + rr * D + ((cch ^ Swz::k(rr)) << 3));
+      *reinterpret_cast<uint4*>(out + (((int64_t)b * a.q_len + out_row) * hq + h) * D + cch * 8) = v;
+    }
+  }
+}
+
+// bf16 prefill from the paged cache.  Pipeline over three tile buffers (each
+// a 256-byte-aligned LDS array): at step t the block loads the block-table
+// entries of tile t+3 (scalar loads) and the K/V rows of tile t+2 (direct
+// loads into the buffer tile t-1 used), computes tile t, then waits until
+// tile t+1 has landed in every wave's part and joins the block, so every
+// tile's loads have two steps to arrive.  The queries are loaded once, behind
+// tile 0.
+template <int D, int G, bool kRuns>
+__global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_lds(PrefillArgs a) {
   typedef bf16_bits T;
   typedef Mfma<T> M;
   typedef M::Frag Frag;
   typedef LdsSwz<D> Swz;
-  constexpr int kThreads = LdsShape<G, kFused>::kThreads;
-  constexpr int kWaves = LdsShape<G, kFused>::kWaves;
-  constexpr int kRows = LdsShape<G, kFused>::kRows;
+  constexpr int kWaves = PrefillShape<G>::kWaves;
+  constexpr int kRows = PrefillShape<G>::kRows;
   constexpr int kKeys = 32;                        // keys per tile
-  constexpr int kPack = M::kPack;
-  constexpr int kStep = 2 * kPack;                 // head-dim elements per QK MFMA
-  constexpr int kQChunks = D / kStep;
+  constexpr int kQChunks = D / 16;
   constexpr int kChunks = Swz::kChunks;
   constexpr int kRowsPerLoad = 64 / kChunks;       // rows one wave-wide direct load fills
   constexpr int kLoads = kKeys / kRowsPerLoad;     // direct loads per tile and matrix
   constexpr int kLoadsPerWave = kLoads >= kWaves ? kLoads / kWaves : 1;
   static_assert(kLoads % kWaves == 0 || kWaves % kLoads == 0, "loads must split evenly over waves");
+  constexpr int kVm = 2 * kLoadsPerWave;           // direct loads per tile of a loading wave
   constexpr int kTile = kKeys * D;                 // elements of one tile
-  constexpr float kLn2 = 0.6931471805599453f;
-  (void)kThreads;
 
-  __shared__ __attribute__((aligned(16))) T s_k0[kTile];
-  __shared__ __attribute__((aligned(16))) T s_k1[kTile];
-  __shared__ __attribute__((aligned(16))) T s_v0[kTile];
-  __shared__ __attribute__((aligned(16))) T s_v1[kTile];
+  __shared__ __attribute__((aligned(256))) T s_k0[kTile];
+  __shared__ __attribute__((aligned(256))) T s_k1[kTile];
+  __shared__ __attribute__((aligned(256))) T s_k2[kTile];
+  __shared__ __attribute__((aligned(256))) T s_v0[kTile];
+  __shared__ __attribute__((aligned(256))) T s_v1[kTile];
+  __shared__ __attribute__((aligned(256))) T s_v2[kTile];
 
   // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
   const int nblk = gridDim.x, bid = blockIdx.x;
@@ -417,14 +614,10 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   const int g = (item / a.num_tiles) % heads;
   const int b = item / a.num_tiles / heads;
 
-  const int w = a.w_eff;
-  const auto sp = span_view<kRuns>(a, b, w);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int rows = min(sp.rows(), a.q_len);
   const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
-  if constexpr (kFused) {
-    if (tile == 0 && g == 0 && threadIdx.x == 0 && args.cache_len_out) args.cache_len_out[b] = sp.clen();
-  }
   if (p0 >= rows) return;
   const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
   const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
@@ -451,42 +644,192 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   auto load_row0 = [&](int i) { return (kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * kRowsPerLoad; };
   const int lrow = lane / kChunks, lpos = lane % kChunks;  // row within the load, LDS chunk position
 
-  // on-the-fly pooling (kFused): D/8 lanes per (slot, head) unit, one unit
-  // per key of the tile; the first kPoolWaves waves pool, lane pj-th chunk
-  // of unit pslot.  The first four frames of each unit's window are staged
-  // by direct loads into this wave's own LDS area (lane i's 16 bytes of
-  // frame t at K: 2t KB + 16 i, V: 2t+1 KB + 16 i), so they cost no
-  // registers across the MFMAs and each lane reads back only what it loaded.
+  f32x16_t o[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  float m_run = neg_inf(), l_run = 0.f;
+
+  // One direct load fills kRowsPerLoad consecutive keys, aligned to that
+  // count, and pages hold at least 8: the load's keys (clamped to kclamp)
+  // all lie in the page of min(first key, kclamp), a wave-uniform index.  The
+  // entry is read through the constant address space, a scalar load (no kernel
+  // writes the table while this one runs), and the page base is scalar.
+  int pg[3][kLoadsPerWave];  // block-table entries, by tile mod 3
+  auto table_load = [&](int kt, int* pgs) {
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int row0 = min(kt * kKeys + load_row0(i), kclamp);
+      typedef __attribute__((address_space(4))) const int32_t* const_ptr;
+      pgs[i] = ((const_ptr)table_row)[min(row0 >> shift, a.pv.max_pages - 1)];
+    }
+  };
+  auto tile_load = [&](int kt, const int* pgs, T* sk, T* sv) {
+    if (!loads) return;
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int row = load_row0(i) + lrow;
+      const int key = min(kt * kKeys + row, kclamp);
+      const int e = pgs[i];
+      const int page = (e >= 0 && e < num_pages) ? e : 0;  // a bad entry reads an in-range page
+      const T* kbase = kpool + page_row<D>(page, g, 0, a.pv);  // uniform
+      const T* vbase = vpool + page_row<D>(page, g, 0, a.pv);
+      const uint32_t in_page = (uint32_t)((key & slot_mask) * D * 2);  // bytes
+      lds_dma16(kbase, in_page + ((lpos ^ Swz::k(row)) << 4), lds_addr(sk + load_row0(i) * D));
+      lds_dma16(vbase, in_page + ((lpos ^ Swz::v(row)) << 4), lds_addr(sv + load_row0(i) * D));
+    }
+  };
+
+  // prologue: tables of tiles 0..2, tile 0, this lane's query row (rows past
+  // the end read row 0 of the sequence: finite, never stored), tile 1; then
+  // wait for tile 0 and the queries (tile 1 may stay in flight)
+  table_load(0, pg[0]);
+  table_load(1, pg[1]);
+  table_load(2, pg[2]);
+  tile_load(0, pg[0], s_k0, s_v0);
+  __builtin_amdgcn_sched_barrier(0);
+  Frag qf[kQChunks];
+  {
+    const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + (qvalid ? p : 0)) * hq + h) * D + hg * 8;
+    static_for<kQChunks>([&](auto kc) { untracked_load16<decltype(kc)::value * 16 * 2>(qf[decltype(kc)::value], qrow); });
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  tile_load(1, pg[1], s_k1, s_v1);
+  bare_barrier<kVm>();
+
+  // step kt; kPar = kt mod 3 selects buffers and table registers at compile time
+  auto tile_step = [&](int kt, auto par) {
+    constexpr int kPar = decltype(par)::value;
+    constexpr int kNext2 = (kPar + 2) % 3;
+    T* const sk = kPar == 0 ? s_k0 : kPar == 1 ? s_k1 : s_k2;
+    T* const sv = kPar == 0 ? s_v0 : kPar == 1 ? s_v1 : s_v2;
+    tile_load(kt + 2, pg[kNext2], kNext2 == 0 ? s_k0 : kNext2 == 1 ? s_k1 : s_k2,
+              kNext2 == 0 ? s_v0 : kNext2 == 1 ? s_v1 : s_v2);  // into the buffer tile kt-1 used
+    table_load(kt + 3, pg[kPar]);
+    if (kt < ntiles) attend_tile<D>(sk, sv, qf, o, m_run, l_run, kt * kKeys, nvis, nvis_lo, lane, a.scale_log2);
+    // tile kt+1 has landed in every wave's part once each wave has at most
+    // the loads of tile kt+2 in flight; every wave is then done with buffer
+    // kPar, which the next step refills
+    bare_barrier<kVm>();
+  };
+  // three steps per iteration so that buffers and registers are compile-time;
+  // the loads of steps past the last tile are in range and never read
+  for (int kt = 0; kt < ntiles; kt += 3) {
+    tile_step(kt, std::integral_constant<int, 0>());
+    tile_step(kt + 1, std::integral_constant<int, 1>());
+    tile_step(kt + 2, std::integral_constant<int, 2>());
+  }
+  bare_barrier<0>();  // no direct load may still target the buffers reused below
+
+  // output: one 32 x D tile per wave through the (now idle) tile buffers
+  T* so = wave == 0 ? s_k0 : wave == 1 ? s_k1 : wave == 2 ? s_k2 : wave == 3 ? s_v0 : wave == 4 ? s_v1 : s_v2;
+  finish_rows<D>(o, m_run, l_run, kWaves <= 6 ? so : nullptr, a, b, h, wrow0, rows, lane);
+}
+
+// Block shape of the pooling variant: eight waves whatever the group size, so
+// a block owns 256/G query rows.  Every block pools each key tile it reads,
+// so taller blocks pool each tile fewer times over the whole grid, and eight
+// waves share the work of a tile (one pass of D/8-lane units at D = 128).
+template <int G>
+struct FusedShape {
+  static constexpr int kRowBlocks = 8 / G;
+  static constexpr int kWaves = 8;
+  static constexpr int kThreads = 512;
+  static constexpr int kRows = 32 * kRowBlocks;
+};
+
+// bf16 prefill that reads the raw K/V and pools each key tile on the fly
+// (Sec. III-C) with the pooling kernel's steps (pool_window.hpp), D/8 lanes
+// per (slot, head) unit: the first four frames of every window of tile t+1
+// are loaded before the MFMAs of tile t and pooled after them, straight into
+// the other of two LDS buffers in the layout the direct loads give.  The
+// block holding a sequence's last query rows (which see every key) also
+// stores each pooled row into the paged cache, and pools the rows no query
+// sees, so the cache ends up as the pooling kernel would have written it.
+// Two waves per SIMD: the first frames of the next tile's windows are held
+// in registers across a step.
+template <int D, int G>
+__global__ __launch_bounds__(FusedShape<G>::kThreads, 2) void prefill_kernel_fused(PrefillFusedArgs args) {
+  const PrefillArgs& a = args.at;
+  typedef bf16_bits T;
+  typedef Mfma<T> M;
+  typedef M::Frag Frag;
+  typedef LdsSwz<D> Swz;
+  constexpr int kWaves = FusedShape<G>::kWaves;
+  constexpr int kRows = FusedShape<G>::kRows;
+  constexpr int kKeys = 32;                        // keys per tile
+  constexpr int kQChunks = D / 16;
+  constexpr int kTile = kKeys * D;                 // elements of one tile
+
+  __shared__ __attribute__((aligned(256))) T s_k0[kTile];
+  __shared__ __attribute__((aligned(256))) T s_k1[kTile];
+  __shared__ __attribute__((aligned(256))) T s_v0[kTile];
+  __shared__ __attribute__((aligned(256))) T s_v1[kTile];
+
+  // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int tile = a.num_tiles - 1 - item % a.num_tiles;
+  const int g = (item / a.num_tiles) % heads;
+  const int b = item / a.num_tiles / heads;
+
+  const int w = a.w_eff;
+  const auto sp = span_view<false>(a, b, w);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
+  const int p0 = tile * kRows;
+  if (tile == 0 && g == 0 && threadIdx.x == 0 && args.cache_len_out) args.cache_len_out[b] = sp.clen();
+  if (p0 >= rows) return;
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
+  const int kclamp = max(kmax - 1, 0);  // last visible key: the row pooled for keys past kmax
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = g * G + wave % G;
+  const int col = lane & 31, hg = lane >> 5;
+  const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
+  const int p = wrow0 + col;
+  const bool qvalid = p < rows;
+  const int nvis = qvalid ? min(sp.visible(p, a.mask_mode), clen) : 0;
+  const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
+  const int hq = a.num_q_heads;
+  const int slot_mask = (1 << a.pv.page_shift) - 1;
+  const int shift = a.pv.page_shift;
+  const int64_t num_pages = a.pv.num_pages;
+  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
+  const int ntiles = (kmax + kKeys - 1) / kKeys;
+
+  // on-the-fly pooling: D/8 lanes per (slot, head) unit, one unit per key of
+  // the tile; the first kPoolWaves waves pool, lane pj-th chunk of unit
+  // pslot.  The first four frames of each unit's window are staged by direct
+  // loads into this wave's own LDS area (lane i's 16 bytes of frame t at K:
+  // 2t KB + 16 i, V: 2t+1 KB + 16 i), so they cost no registers across the
+  // MFMAs and each lane reads back only what it loaded.
   constexpr int kLanes = D / 8;
   constexpr int kPoolWaves = kKeys / (64 / kLanes);
-  static_assert(!kFused || kPoolWaves <= kWaves, "one pass of the pooling waves covers a tile");
+  static_assert(kPoolWaves <= kWaves, "one pass of the pooling waves covers a tile");
   const int pj = lane % kLanes;
   const int pslot = wave * (64 / kLanes) + lane / kLanes;
   const bool pool_wave = wave < kPoolWaves;  // uniform over the wave
   const bool writer = p0 + kRows >= rows;   // holds the last rows: sees every key
   int fsrc = 0, ffr = 1, fent = 0;          // the unit's first raw row, frames, page
   float u[8];
-  const T* kr = nullptr;
-  const T* vr = nullptr;
-  T* stage = nullptr;  // this wave's staging area
-  int64_t raw_stride = 0;
-  int raw_last = 0;
-  if constexpr (kFused) {
-    __shared__ __attribute__((aligned(16))) T s_stage[kPoolWaves * 8 * 512];
-    stage = s_stage + (pool_wave ? wave : 0) * 8 * 512;
-    kr = static_cast<const T*>(args.k_raw) + b * args.stride_b + g * args.stride_h + 8 * pj;
-    vr = static_cast<const T*>(args.v_raw) + b * args.stride_b + g * args.stride_h + 8 * pj;
-    raw_stride = args.stride_s;
-    raw_last = args.raw_len - 1;
-    if (args.gate) {  // without a gate every logit is 0 (uniform averaging)
-      const float4* gp = reinterpret_cast<const float4*>(args.gate + (int64_t)g * D + 8 * pj);
-      const float4 u0 = gp[0], u1 = gp[1];
-      u[0] = u0.x; u[1] = u0.y; u[2] = u0.z; u[3] = u0.w;
-      u[4] = u1.x; u[5] = u1.y; u[6] = u1.z; u[7] = u1.w;
-    } else {
+  __shared__ __attribute__((aligned(16))) T s_stage[kPoolWaves * 8 * 512];
+  T* const stage = s_stage + (pool_wave ? wave : 0) * 8 * 512;
+  const T* kr = static_cast<const T*>(args.k_raw) + b * args.stride_b + g * args.stride_h + 8 * pj;
+  const T* vr = static_cast<const T*>(args.v_raw) + b * args.stride_b + g * args.stride_h + 8 * pj;
+  const int64_t raw_stride = args.stride_s;
+  const int raw_last = args.raw_len - 1;
+  if (args.gate) {  // without a gate every logit is 0 (uniform averaging)
+    const float4* gp = reinterpret_cast<const float4*>(args.gate + (int64_t)g * D + 8 * pj);
+    const float4 u0 = gp[0], u1 = gp[1];
+    u[0] = u0.x; u[1] = u0.y; u[2] = u0.z; u[3] = u0.w;
+    u[4] = u1.x; u[5] = u1.y; u[6] = u1.z; u[7] = u1.w;
+  } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) u[i] = 0.f;
-    }
+    for (int i = 0; i < 8; ++i) u[i] = 0.f;
   }
   auto raw_at = [&](int s) __attribute__((always_inline)) { return (int64_t)min(s, raw_last) * raw_stride; };
   // stage the first four frames of unit (slot min(c0 + pslot, cmax), this
@@ -551,12 +894,10 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
   // cache row c of this head, when it exists, has a valid page and its
   // source rows lie inside the raw tensor (as the pooling kernel checks)
   auto cache_store = [&](int c, const Chunk<T>& ko, const Chunk<T>& vo) __attribute__((always_inline)) {
-    if constexpr (kFused) {
-      if (c < clen && fent >= 0 && fent < num_pages && fsrc + ffr <= raw_last + 1) {
-        const int64_t off = page_row<D>(fent, g, c & slot_mask, a.pv) + 8 * pj;
-        ko.store(static_cast<T*>(args.k_pages) + off);
-        vo.store(static_cast<T*>(args.v_pages) + off);
-      }
+    if (c < clen && fent >= 0 && fent < num_pages && fsrc + ffr <= raw_last + 1) {
+      const int64_t off = page_row<D>(fent, g, c & slot_mask, a.pv) + 8 * pj;
+      ko.store(static_cast<T*>(args.k_pages) + off);
+      vo.store(static_cast<T*>(args.v_pages) + off);
     }
   };
   // pool key tile kt into LDS; the writer also stores its visible rows
@@ -577,217 +918,48 @@ __global__ __launch_bounds__((lds_threads<G, kFused>()), (lds_kernel_waves<D, G,
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
   float m_run = neg_inf(), l_run = 0.f;
 
-  int pg[2][kLoadsPerWave];  // block-table entries, by tile parity
-  // One direct load fills kRowsPerLoad consecutive keys, aligned to that
-  // count, and pages hold at least 8: the load's keys (clamped to kclamp)
-  // all lie in the page of min(first key, kclamp), a wave-uniform index.  The
-  // entry is read through the constant address space, a scalar load (no kernel
-  // writes the table while this one runs), and the page base is scalar.
-  auto table_load = [&](int kt, int* pgs) {
-#pragma unroll
-    for (int i = 0; i < kLoadsPerWave; ++i) {
-      const int row0 = min(kt * kKeys + load_row0(i), kclamp);
-      typedef __attribute__((address_space(4))) const int32_t* const_ptr;
-      pgs[i] = ((const_ptr)table_row)[min(row0 >> shift, a.pv.max_pages - 1)];
-    }
-  };
-  auto tile_load = [&](int kt, const int* pgs, T* sk, T* sv) {
-    if (!loads) return;
-#pragma unroll
-    for (int i = 0; i < kLoadsPerWave; ++i) {
-      const int row = load_row0(i) + lrow;
-      const int key = min(kt * kKeys + row, kclamp);
-      const int e = pgs[i];
-      const int page = (e >= 0 && e < num_pages) ? e : 0;  // a bad entry reads an in-range page
-      const int64_t off = page_row<D>(page, g, 0, a.pv) + (int64_t)((key & slot_mask) * D);
-      __builtin_amdgcn_global_load_lds((global_void_ptr)(kpool + off + ((lpos ^ Swz::k(row)) << 3)),
-                                       (lds_void_ptr)(sk + load_row0(i) * D), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((global_void_ptr)(vpool + off + ((lpos ^ Swz::v(row)) << 3)),
-                                       (lds_void_ptr)(sv + load_row0(i) * D), 16, 0, 0);
-    }
-  };
-
-  // prologue: tables of tiles 0 and 1, tile 0 into LDS, then this lane's query
-  // row (issued after the tile: the memory counter is in order)
-  if constexpr (kFused) {
-    if (ntiles > 0) pool_fetch(0, kclamp);
-  } else {
-    table_load(0, pg[0]);
-    table_load(1, pg[1]);
-    tile_load(0, pg[0], s_k0, s_v0);
-  }
+  // prologue: stage tile 0's frames, load this lane's query row (rows past
+  // the end read row 0: finite, never stored), pool tile 0
+  if (ntiles > 0) pool_fetch(0, kclamp);
   __builtin_amdgcn_sched_barrier(0);
   Frag qf[kQChunks];
   {
     const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + (qvalid ? p : 0)) * hq + h) * D;
 #pragma unroll
-    for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = M::load(qrow + kc * kStep + hg * kPack);
+    for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = M::load(qrow + kc * 16 + hg * 8);
   }
-  if constexpr (kFused) {
-    if (ntiles > 0) pool_tile(0, s_k0, s_v0);
-  } else {
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  }
+  if (ntiles > 0) pool_tile(0, s_k0, s_v0);
   __syncthreads();
 
-  // one step; kPar = kt & 1 selects buffers and table registers at compile time
+  // step kt: stage the frames of tile kt+1, attend to tile kt, pool tile kt+1
+  // into the other buffer; kPar = kt & 1 selects buffers at compile time
   auto tile_step = [&](int kt, auto par) {
     constexpr int kPar = decltype(par)::value;
     T* const sk = kPar ? s_k1 : s_k0;
     T* const sv = kPar ? s_v1 : s_v0;
-    T* const sk_next = kPar ? s_k0 : s_k1;
-    T* const sv_next = kPar ? s_v0 : s_v1;
     const bool pool_next = kt + 1 < ntiles;  // uniform
-    if constexpr (kFused) {
-      if (pool_next) pool_fetch((kt + 1) * kKeys, kclamp);  // pooled after this tile's MFMAs
-    } else {
-      table_load(kt + 2, pg[kPar]);                     // parity of kt+2 = kt
-      tile_load(kt + 1, pg[1 - kPar], sk_next, sv_next);  // into the buffer tile kt-1 used
-    }
-    if (kt < ntiles) {  // (the loop runs an even number of steps)
-      const int kb = kt * kKeys;
-      // S^T tile: row = key (8*(i/4) + 4*hg + i%4), column = this lane's query
-      f32x16_t st;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) st[i] = 0.f;
-      const T* krow = sk + col * D;
-      const int kswz = Swz::k(col);
-#pragma unroll
-      for (int kc = 0; kc < kQChunks; ++kc)
-        st = M::mma(M::load(krow + (((2 * kc + hg) ^ kswz) << 3)), qf[kc], st);
-
-      float pr[16];
-      float mt = neg_inf();
-      const bool masked = kb + kKeys > nvis_lo;  // uniform over the wave
-      if (masked) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kb + 8 * (i / 4) + 4 * hg + (i % 4);
-          pr[i] = key < nvis ? st[i] : neg_inf();
-          mt = fmaxf(mt, pr[i]);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          pr[i] = st[i];
-          mt = fmaxf(mt, pr[i]);
-        }
-      }
-      mt = partner_max(mt) * a.scale_log2;  // the scale is > 0
-      if (mt > m_run + kSlack) {
-        if (m_run != neg_inf()) {  // (before the first visible key o and l are still 0)
-          const float corr = fast_exp2(m_run - mt);
-          l_run *= corr;
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) o[db][i] *= corr;
-        }
-        m_run = mt;
-      }
-      // a row that sees no key yet has m_run = -inf and every logit -inf:
-      // reference 0 turns each weight into exp2(-inf) = 0
-      const float m_use = m_run == neg_inf() ? 0.f : m_run;
-      // the sum is of the unrounded weights, so that the log-sum-exp output
-      // gives weights that sum to 1 when the backward recomputes them
-      float sum = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        pr[i] = fast_exp2(__builtin_fmaf(pr[i], a.scale_log2, -m_use));
-        sum += pr[i];
-      }
-      l_run += sum;
-
-      // O^T += V^T P^T over the 32 keys of the tile; the A operand comes
-      // through the LDS transpose read (see Mfma<bf16_bits>::load_v) from
-      // the swizzled rows
-      const int vg = lane >> 4, vj = lane & 15;
-#pragma unroll
-      for (int kk = 0; kk < kKeys / kStep; ++kk) {
-        const Frag pf = M::pack_p(pr + kk * kPack);
-        const int r0 = 16 * kk + 4 * (vg >> 1) + (vj >> 2);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const int e = 32 * db + 16 * (vg & 1) + 4 * (vj & 3);  // first element of the lane's run
-          const T* plo = sv + r0 * D + ((((e >> 3) ^ Swz::v(r0)) << 3) | (e & 4));
-          const T* phi = sv + (r0 + 8) * D + ((((e >> 3) ^ Swz::v(r0 + 8)) << 3) | (e & 4));
-          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)plo);
-          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)phi);
-          const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2],
-                             (unsigned short)lo[3], (unsigned short)hi[0], (unsigned short)hi[1],
-                             (unsigned short)hi[2], (unsigned short)hi[3]};
-          o[db] = M::mma(__builtin_bit_cast(Frag, v), pf, o[db]);
-        }
-      }
-    }
-    if constexpr (kFused) {
-      if (pool_next) pool_tile(kt + 1, sk_next, sv_next);
-    } else {
-      // the next tile's rows (and the table entries after them) have landed in
-      // every wave's part of the buffer once each wave's counter is at zero
-      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    }
+    if (pool_next) pool_fetch((kt + 1) * kKeys, kclamp);  // pooled after this tile's MFMAs
+    if (kt < ntiles) attend_tile<D>(sk, sv, qf, o, m_run, l_run, kt * kKeys, nvis, nvis_lo, lane, a.scale_log2);
+    if (pool_next) pool_tile(kt + 1, kPar ? s_k0 : s_k1, kPar ? s_v0 : s_v1);
     __syncthreads();
   };
-  // two steps per iteration so that buffers and registers are compile-time;
-  // the loads of a step past the last tile are in range and never read
   for (int kt = 0; kt < ntiles; kt += 2) {
     tile_step(kt, std::integral_constant<int, 0>());
     tile_step(kt + 1, std::integral_constant<int, 1>());
   }
-  if constexpr (kFused) {
-    // cache rows no query of this sequence sees: pooled and stored by the writer
-    if (writer) {
-      for (int c0 = kmax; c0 < clen; c0 += kKeys) {
-        pool_fetch(c0, clen - 1);
-        if (pool_wave) {
-          Chunk<T> ko, vo;
-          pool_rows(ko, vo);
-          cache_store(c0 + pslot, ko, vo);
-        }
+  // cache rows no query of this sequence sees: pooled and stored by the writer
+  if (writer) {
+    for (int c0 = kmax; c0 < clen; c0 += kKeys) {
+      pool_fetch(c0, clen - 1);
+      if (pool_wave) {
+        Chunk<T> ko, vo;
+        pool_rows(ko, vo);
+        cache_store(c0 + pslot, ko, vo);
       }
     }
   }
-
-  const float l_tot = partner_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (hg == 0 && a.lse && qvalid)
-    a.lse[((int64_t)b * hq + h) * a.q_len + p] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : neg_inf();
-
-  if constexpr (kWaves > 4) {  // direct stores of the C layout: four values per row
-    if (qvalid) {
-      T* orow = static_cast<T*>(a.out) + (((int64_t)b * a.q_len + p) * hq + h) * D;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int ig = 0; ig < 4; ++ig)
-          M::store4(orow + db * 32 + 8 * ig + 4 * hg, o[db][4 * ig] * inv, o[db][4 * ig + 1] * inv,
-                    o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
-    }
-  } else {
-    // output: one 32 x D tile per wave through one of the (now idle) tile
-    // buffers, rows swizzled like K, then 16-byte row stores
-    T* so = wave == 0 ? s_k0 : wave == 1 ? s_k1 : wave == 2 ? s_v0 : s_v1;
-    const int oswz = Swz::k(col);
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int ig = 0; ig < 4; ++ig)
-        M::store4(so + col * D + (((4 * db + ig) ^ oswz) << 3) + 4 * hg, o[db][4 * ig] * inv,
-                  o[db][4 * ig + 1] * inv, o[db][4 * ig + 2] * inv, o[db][4 * ig + 3] * inv);
-    __syncthreads();  // (the same wave reads its tile back: orders its LDS traffic)
-    constexpr int kRowsPerPass = 64 / kChunks;
-#pragma unroll
-    for (int r0 = 0; r0 < 32; r0 += kRowsPerPass) {
-      const int rr = r0 + lane / kChunks, cch = lane % kChunks;
-      const int out_row = wrow0 + rr;
-      if (out_row < rows) {
-        const uint4 v = *reinterpret_cast<const uint4*>(so + rr * D + ((cch ^ Swz::k(rr)) << 3));
-        *reinterpret_cast<uint4*>(static_cast<T*>(a.out) + (((int64_t)b * a.q_len + out_row) * hq + h) * D +
-                                  cch * 8) = v;
-      }
-    }
-  }
+  static_assert(kWaves > 4, "eight waves store their rows from the C layout");
+  finish_rows<D>(o, m_run, l_run, nullptr, a, b, h, wrow0, rows, lane);
 }
 
 template <typename T, int D, bool kRuns>
@@ -801,15 +973,26 @@ hipError_t launch_prefill_d(const PrefillArgs& a, int group, int batch, hipStrea
   }
 }
 
-template <int D, bool kFused, bool kRuns>
-hipError_t launch_prefill_lds(const typename LdsArgs<kFused>::type& args, int group, int batch, hipStream_t s) {
-  const PrefillArgs& a = attn_args(args);
+template <int D, bool kRuns>
+hipError_t launch_prefill_lds(const PrefillArgs& a, int group, int batch, hipStream_t s) {
   const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
   switch (group) {
-    case 1: return launch_struct(prefill_kernel_lds<D, 1, kFused, kRuns>, dim3(items), dim3(LdsShape<1, kFused>::kThreads), s, args);
-    case 2: return launch_struct(prefill_kernel_lds<D, 2, kFused, kRuns>, dim3(items), dim3(LdsShape<2, kFused>::kThreads), s, args);
-    case 4: return launch_struct(prefill_kernel_lds<D, 4, kFused, kRuns>, dim3(items), dim3(LdsShape<4, kFused>::kThreads), s, args);
-    default: return launch_struct(prefill_kernel_lds<D, 8, kFused, kRuns>, dim3(items), dim3(LdsShape<8, kFused>::kThreads), s, args);
+    case 1: return launch_struct(prefill_kernel_lds<D, 1, kRuns>, dim3(items), dim3(PrefillShape<1>::kThreads), s, a);
+    case 2: return launch_struct(prefill_kernel_lds<D, 2, kRuns>, dim3(items), dim3(PrefillShape<2>::kThreads), s, a);
+    case 4: return launch_struct(prefill_kernel_lds<D, 4, kRuns>, dim3(items), dim3(PrefillShape<4>::kThreads), s, a);
+    default: return launch_struct(prefill_kernel_lds<D, 8, kRuns>, dim3(items), dim3(PrefillShape<8>::kThreads), s, a);
+  }
+}
+
+template <int D>
+hipError_t launch_prefill_fused_d(const PrefillFusedArgs& args, int group, int batch, hipStream_t s) {
+  const PrefillArgs& a = args.at;
+  const unsigned items = (unsigned)(batch * a.pv.kv_heads * a.num_tiles);
+  switch (group) {
+    case 1: return launch_struct(prefill_kernel_fused<D, 1>, dim3(items), dim3(FusedShape<1>::kThreads), s, args);
+    case 2: return launch_struct(prefill_kernel_fused<D, 2>, dim3(items), dim3(FusedShape<2>::kThreads), s, args);
+    case 4: return launch_struct(prefill_kernel_fused<D, 4>, dim3(items), dim3(FusedShape<4>::kThreads), s, args);
+    default: return launch_struct(prefill_kernel_fused<D, 8>, dim3(items), dim3(FusedShape<8>::kThreads), s, args);
   }
 }
 
@@ -829,10 +1012,10 @@ hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int gro
   const bool runs = a.segs.seg_start != nullptr;
   if (dtype == 1) {
     if (head_dim == 128)
-      return runs ? launch_prefill_lds<128, false, true>(a, group, batch, s)
-                  : launch_prefill_lds<128, false, false>(a, group, batch, s);
-    return runs ? launch_prefill_lds<64, false, true>(a, group, batch, s)
-                : launch_prefill_lds<64, false, false>(a, group, batch, s);
+      return runs ? launch_prefill_lds<128, true>(a, group, batch, s)
+                  : launch_prefill_lds<128, false>(a, group, batch, s);
+    return runs ? launch_prefill_lds<64, true>(a, group, batch, s)
+                : launch_prefill_lds<64, false>(a, group, batch, s);
   }
   if (head_dim == 128)
     return runs ? launch_prefill_d<float, 128, true>(a, group, batch, s)
@@ -852,8 +1035,8 @@ int prefill_fused_rows_per_tile(int group) {
 
 hipError_t launch_prefill_fused(const PrefillFusedArgs& a, int head_dim, int group, int batch,
                                 hipStream_t s) {
-  if (head_dim == 128) return launch_prefill_lds<128, true, false>(a, group, batch, s);
-  return launch_prefill_lds<64, true, false>(a, group, batch, s);
+  if (head_dim == 128) return launch_prefill_fused_d<128>(a, group, batch, s);
+  return launch_prefill_fused_d<64>(a, group, batch, s);
 }
 
 }  // namespace skv
