@@ -651,42 +651,46 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
   float m_run = neg_inf(), l_run = 0.f;
 
-  // One direct load fills kRowsPerLoad consecutive keys, aligned to that
-  // count, and pages hold at least 8: the load's keys (clamped to kclamp)
-  // all lie in the page of min(first key, kclamp), a wave-uniform index.  The
-  // entry is read through the constant address space, a scalar load (no kernel
-  // writes the table while this one runs), and the page base is scalar.
-  int pg[3][kLoadsPerWave];  // block-table entries, by tile mod 3
-  auto table_load = [&](int kt, int* pgs) {
-#pragma unroll
-    for (int i = 0; i < kLoadsPerWave; ++i) {
-      const int row0 = min(kt * kKeys + load_row0(i), kclamp);
-      typedef __attribute__((address_space(4))) const int32_t* const_ptr;
-      pgs[i] = ((const_ptr)table_row)[min(row0 >> shift, a.pv.max_pages - 1)];
-    }
+  // A wave's direct loads of a tile fill kWaveRows <= 8 consecutive keys,
+  // aligned to that count, and pages hold at least 8: its keys (each clamped
+  // to kclamp) all lie in the page of min(first key, kclamp), so the wave
+  // needs one block-table entry per tile, a wave-uniform index.  The entry is
+  // read through the constant address space, a scalar load (no kernel writes
+  // the table while this one runs), and the page bases are scalar.
+  constexpr int kWaveRows = kLoadsPerWave * kRowsPerLoad;
+  static_assert(kWaveRows <= 8, "one page holds a wave's rows of a tile");
+  const int wrow_load = loads ? load_row0(0) : 0;
+  typedef __attribute__((address_space(4))) const int32_t* const_ptr;
+  auto table_load = [&](int kt) __attribute__((always_inline)) {
+    const int row0 = min(kt * kKeys + wrow_load, kclamp);
+    return ((const_ptr)table_row)[min(row0 >> shift, a.pv.max_pages - 1)];
   };
-  auto tile_load = [&](int kt, const int* pgs, T* sk, T* sv) {
+  // byte addresses: page p of KV head g starts at pool + p * page_bytes +
+  // g * head_bytes; the V pool is the K pool plus a fixed distance
+  const uint64_t head_bytes = (uint64_t)D * sizeof(T) << shift;
+  const uint64_t page_bytes = head_bytes * heads;
+  const uintptr_t kpool_g = (uintptr_t)kpool + (uint64_t)g * head_bytes;
+  const uintptr_t v_minus_k = (uintptr_t)vpool - (uintptr_t)kpool;
+  const uint32_t npages = (uint32_t)num_pages;
+  auto tile_load = [&](int kt, int e, T* sk, T* sv) __attribute__((always_inline)) {
     if (!loads) return;
+    const uint32_t page = (uint32_t)e < npages ? (uint32_t)e : 0u;  // a bad entry reads an in-range page
+    const uintptr_t kbase = kpool_g + (uint64_t)page * page_bytes;  // uniform
+    const uintptr_t vbase = kbase + v_minus_k;
 #pragma unroll
     for (int i = 0; i < kLoadsPerWave; ++i) {
       const int row = load_row0(i) + lrow;
       const int key = min(kt * kKeys + row, kclamp);
-      const int e = pgs[i];
-      const int page = (e >= 0 && e < num_pages) ? e : 0;  // a bad entry reads an in-range page
-      const T* kbase = kpool + page_row<D>(page, g, 0, a.pv);  // uniform
-      const T* vbase = vpool + page_row<D>(page, g, 0, a.pv);
       const uint32_t in_page = (uint32_t)((key & slot_mask) * D * 2);  // bytes
-      lds_dma16(kbase, in_page + ((lpos ^ Swz::k(row)) << 4), lds_addr(sk + load_row0(i) * D));
-      lds_dma16(vbase, in_page + ((lpos ^ Swz::v(row)) << 4), lds_addr(sv + load_row0(i) * D));
+      lds_dma16((const void*)kbase, in_page + ((lpos ^ Swz::k(row)) << 4), lds_addr(sk + load_row0(i) * D));
+      lds_dma16((const void*)vbase, in_page + ((lpos ^ Swz::v(row)) << 4), lds_addr(sv + load_row0(i) * D));
     }
   };
 
   // prologue: tables of tiles 0..2, tile 0, this lane's query row (rows past
   // the end read row 0 of the sequence: finite, never stored), tile 1; then
   // wait for tile 0 and the queries (tile 1 may stay in flight)
-  table_load(0, pg[0]);
-  table_load(1, pg[1]);
-  table_load(2, pg[2]);
+  int pg[3] = {table_load(0), table_load(1), table_load(2)};  // entries by tile mod 3
   tile_load(0, pg[0], s_k0, s_v0);
   __builtin_amdgcn_sched_barrier(0);
   Frag qf[kQChunks];
@@ -706,7 +710,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
     T* const sv = kPar == 0 ? s_v0 : kPar == 1 ? s_v1 : s_v2;
     tile_load(kt + 2, pg[kNext2], kNext2 == 0 ? s_k0 : kNext2 == 1 ? s_k1 : s_k2,
               kNext2 == 0 ? s_v0 : kNext2 == 1 ? s_v1 : s_v2);  // into the buffer tile kt-1 used
-    table_load(kt + 3, pg[kPar]);
+    pg[kPar] = table_load(kt + 3);
     if (kt < ntiles) attend_tile<D>(sk, sv, qf, o, m_run, l_run, kt * kKeys, nvis, nvis_lo, lane, a.scale_log2);
     // tile kt+1 has landed in every wave's part once each wave has at most
     // the loads of tile kt+2 in flight; every wave is then done with buffer
