@@ -691,7 +691,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
   // the end read row 0 of the sequence: finite, never stored), tile 1; then
   // wait for tile 0 and the queries (tile 1 may stay in flight)
   int pg[3] = {table_load(0), table_load(1), table_load(2)};  // entries by tile mod 3
-  tile_load(0, pg[0], s_k0, s_v0);
+  tile_load(0, pg[0], s_k0, s_v0);  // (also for a block without tiles: in range, never read)
   __builtin_amdgcn_sched_barrier(0);
   Frag qf[kQChunks];
   {
@@ -699,34 +699,46 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
     static_for<kQChunks>([&](auto kc) { untracked_load16<decltype(kc)::value * 16 * 2>(qf[decltype(kc)::value], qrow); });
   }
   __builtin_amdgcn_sched_barrier(0);
-  tile_load(1, pg[1], s_k1, s_v1);
-  bare_barrier<kVm>();
+  if (ntiles > 1) {
+    tile_load(1, pg[1], s_k1, s_v1);
+    bare_barrier<kVm>();
+  } else {
+    bare_barrier<0>();
+  }
 
-  // step kt; kPar = kt mod 3 selects buffers and table registers at compile time
+  // step kt; kPar = kt mod 3 selects buffers and table registers at compile
+  // time.  Tiles past the last one are neither loaded nor computed: the last
+  // two steps wait for everything in flight instead.
   auto tile_step = [&](int kt, auto par) {
     constexpr int kPar = decltype(par)::value;
     constexpr int kNext2 = (kPar + 2) % 3;
     T* const sk = kPar == 0 ? s_k0 : kPar == 1 ? s_k1 : s_k2;
     T* const sv = kPar == 0 ? s_v0 : kPar == 1 ? s_v1 : s_v2;
-    tile_load(kt + 2, pg[kNext2], kNext2 == 0 ? s_k0 : kNext2 == 1 ? s_k1 : s_k2,
-              kNext2 == 0 ? s_v0 : kNext2 == 1 ? s_v1 : s_v2);  // into the buffer tile kt-1 used
-    pg[kPar] = table_load(kt + 3);
-    if (kt < ntiles) attend_tile<D>(sk, sv, qf, o, m_run, l_run, kt * kKeys, nvis, nvis_lo, lane, a.scale_log2);
+    const bool more = kt + 2 < ntiles;  // uniform
+    if (more) {
+      tile_load(kt + 2, pg[kNext2], kNext2 == 0 ? s_k0 : kNext2 == 1 ? s_k1 : s_k2,
+                kNext2 == 0 ? s_v0 : kNext2 == 1 ? s_v1 : s_v2);  // into the buffer tile kt-1 used
+      if (kt + 3 < ntiles) pg[kPar] = table_load(kt + 3);
+    }
+    attend_tile<D>(sk, sv, qf, o, m_run, l_run, kt * kKeys, nvis, nvis_lo, lane, a.scale_log2);
     // tile kt+1 has landed in every wave's part once each wave has at most
     // the loads of tile kt+2 in flight; every wave is then done with buffer
     // kPar, which the next step refills
-    bare_barrier<kVm>();
+    if (more) bare_barrier<kVm>();
+    else bare_barrier<0>();
   };
-  // three steps per iteration so that buffers and registers are compile-time;
-  // the loads of steps past the last tile are in range and never read
+  // three steps per iteration so that buffers and registers are compile-time
   for (int kt = 0; kt < ntiles; kt += 3) {
     tile_step(kt, std::integral_constant<int, 0>());
+    if (kt + 1 >= ntiles) break;
     tile_step(kt + 1, std::integral_constant<int, 1>());
+    if (kt + 2 >= ntiles) break;
     tile_step(kt + 2, std::integral_constant<int, 2>());
   }
-  bare_barrier<0>();  // no direct load may still target the buffers reused below
 
-  // output: one 32 x D tile per wave through the (now idle) tile buffers
+  // output: one 32 x D tile per wave through the tile buffers, idle since the
+  // last step's barrier (or the prologue's, without tiles) left no load in
+  // flight and no wave reading them
   T* so = wave == 0 ? s_k0 : wave == 1 ? s_k1 : wave == 2 ? s_k2 : wave == 3 ? s_v0 : wave == 4 ? s_v1 : s_v2;
   finish_rows<D>(o, m_run, l_run, kWaves <= 6 ? so : nullptr, a, b, h, wrow0, rows, lane);
 }
