@@ -1,9 +1,11 @@
 // MFMA building blocks shared by the prefill attention kernels and their
 // backward (arXiv 2607.06827, Sec. III-B, Eq. 5 under the causal mask over
 // compressed positions): operand types and loads of the 32x32 bf16 / fp32
-// MFMAs, the visibility rule n_vis(p), the block shapes and the exchange with
-// the partner lane of the 32x32 C layout.
+// MFMAs, untracked global-to-LDS staging with explicit waits, the block
+// shapes and the exchange with the partner lane of the 32x32 C layout.
 #pragma once
+
+#include <type_traits>
 
 #include "common.hpp"
 #include "spans.hpp"
@@ -92,6 +94,69 @@ struct Mfma<float> {
     *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
   }
 };
+
+// ------------------------------------------------- LDS staging and waits
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) void* global_void_ptr;
+
+// Byte address of an LDS object (the 32-bit LDS address space).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void_ptr)p; }
+
+// 16 bytes per lane from sbase + voff (bytes; sbase wave-uniform) into LDS at
+// lds + 16 * lane, issued from inline assembly so that the compiler neither
+// counts nor waits for it: the caller waits with an explicit vector-memory
+// count.  (The compiler cannot tell which LDS object a transposed read
+// touches, and with tracked direct loads it waits for all of them before every
+// such read.)
+__device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+
+// 4 bytes per lane from the per-lane address p into LDS at lds + 4 * lane,
+// untracked like lds_dma16.
+__device__ __forceinline__ void lds_dma4(const void* p, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" : : "v"(p), "s"(lds) : "memory", "m0");
+}
+
+// 16 bytes at p + kOff into r, untracked like lds_dma16: the caller waits
+// explicitly before r is read.
+template <int kOff, typename F>
+__device__ __forceinline__ void untracked_load16(F& r, const void* p) {
+  static_assert(sizeof(F) == 16, "16-byte fragment");
+  asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "i"(kOff) : "memory");
+}
+
+// s_waitcnt immediate: at most n vector-memory operations outstanding, LDS
+// and scalar loads complete (CDNA layout: vmcnt bits 3:0 and 15:14, lgkmcnt
+// 11:8, expcnt 6:4 left at its maximum)
+constexpr int wait_vm_lgkm0(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
+// f(integral_constant<int, i>) for i = 0 .. n-1, unrolled at compile time
+template <int n, int i = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (i < n) {
+    f(std::integral_constant<int, i>());
+    static_for<n, i + 1>(f);
+  }
+}
+
+// Full barrier with no memory fence: waits until at most vm of the wave's
+// (untracked) vector-memory operations are in flight and its LDS reads are
+// done, then joins the block.  Compiler and scheduler fences on both sides
+// keep every LDS access on its side.
+template <int kVm>
+__device__ __forceinline__ void bare_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(kVm));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
 
 template <int G>
 struct PrefillShape {

@@ -257,9 +257,6 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_bwd_dq_kern
 
 // --------------------------------------------------------------- dK / dV
 
-typedef __attribute__((address_space(3))) void* lds_void_ptr;
-typedef __attribute__((address_space(1))) void* global_void_ptr;
-
 // Q / dO tiles of the dK/dV kernel: 32 unpadded rows in LDS, filled by
 // direct loads (global_load_lds: a wave-wide load writes 64 x 16 bytes in
 // lane order), 16-byte chunks XOR-swizzled within a row: chunk c of row r sits
@@ -535,6 +532,245 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
     }
 }
 
+// ----------------------------------------------- dK / dV, bf16, 16 keys a wave
+//
+// The bf16 dK/dV kernel on the 16x16x32 MFMA: a wave owns 16 keys, so its K
+// and V operands (16 VGPRs each at d = 128) and its dK^T and dV^T
+// accumulators (32 each) leave room for three waves per SIMD.  A block of four
+// waves owns 64 keys of one (sequence, KV head) and walks the (query head,
+// 32-row query tile) steps that see them; each step's Q, dO, LSE and Delta are
+// staged once in LDS for the four waves by untracked direct loads, two steps
+// ahead in three buffers, as in the forward.  Per step a wave computes
+//   S  = Q K^T  - LSE/scale    (two 16 x 16 blocks: query rows 0-15, 16-31)
+//   dP = dO V^T - Delta
+//   P = exp2(scale log2e S),  dZ = P dP     (masked)
+//   dV^T += dO^T P,  dK^T += Q^T dZ          (d x keys, 16-row blocks of d)
+// The C layout of the 16x16 MFMA gives lane (g, j) (g = lane / 16) rows 4g +
+// i (i < 4) and column j; the P.V-type products take their K index (query
+// rows) in the order k = 8g + t <-> row 4g + t (t < 4), 16 + 4g + t - 4
+// (t >= 4), so P and dZ are their own B operands and dO^T / Q^T come from two
+// transposed LDS reads (rows 4g.., 16 + 4g..) per head-dim block.
+template <int D, int G, bool kRuns>
+__global__ __launch_bounds__(256, 3) void prefill_bwd_dkdv16_kernel(PrefillBwdArgs a) {
+  typedef bf16_bits T;
+  typedef QTile<T, D> Q;
+  typedef bf16x8_t Frag;
+  constexpr int kWaves = 4;
+  constexpr int kBlockKeys = 16 * kWaves;
+  constexpr int kQ = 32;           // query rows per step
+  constexpr int kDC = D / 32;      // K-dim chunks of the S and dP products
+  constexpr int kDB = D / 16;      // 16-row blocks of dK^T and dV^T
+  constexpr int kLoadsPerWave = 2 * Q::kLoads / kWaves;  // Q and dO direct loads per step
+  static_assert((2 * Q::kLoads) % kWaves == 0, "loads split evenly over waves");
+  constexpr int kVm = kLoadsPerWave;                     // (+1 for the wave that loads LSE / Delta)
+
+  struct __attribute__((aligned(256))) Buf {
+    T q[Q::kElems];
+    T g[Q::kElems];
+    float l[2 * kQ];  // LSE, Delta
+  };
+  __shared__ Buf s_b0, s_b1, s_b2;
+
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int kt = item % a.num_key_tiles;  // early keys (most query rows) first
+  const int g = (item / a.num_key_tiles) % heads;
+  const int b = item / a.num_key_tiles / heads;
+
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(min(sp.clen(), a.pv.max_pages << a.pv.page_shift), a.hat_cap);
+  const int kb0 = kt * kBlockKeys;
+  if (kb0 >= clen || rows == 0) return;  // block-uniform
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int gq = lane >> 4, j = lane & 15;  // lane group, column of the 16x16 C layout
+  const int hq = a.num_q_heads;
+  const int kw = kb0 + 16 * wave;   // this wave's first key
+  const int key = kw + j;           // this lane's key
+  const int tau = key < clen ? sp.visible_from(key, a.mask_mode) : INT_MAX;
+  // first row that sees a key of this wave, and from which row on every
+  // valid key of the wave is visible
+  const int wave_from = kw < clen ? sp.visible_from(kw, a.mask_mode) : INT_MAX;
+  const int wave_all = kw < clen ? sp.visible_from(min(kw + 15, clen - 1), a.mask_mode) : INT_MAX;
+
+  // K and V operands of this lane's key: elements 32c + 8 gq .. +7 (B operand
+  // layout of S = Q K^T and dP = dO V^T); a key past the cache or without a
+  // page reads a row of page 0 (its column of every product is never stored)
+  Frag kf[kDC], vf[kDC];
+  {
+    const int shift = a.pv.page_shift;
+    const int32_t e = a.table[(int64_t)b * a.pv.max_pages + min(key >> shift, a.pv.max_pages - 1)];
+    const bool ok = key < clen && e >= 0 && e < a.pv.num_pages;
+    const int64_t off = page_row<D>(ok ? e : 0, g, key & ((1 << shift) - 1), a.pv) + 8 * gq;
+    const T* kp = static_cast<const T*>(a.k_pages) + off;
+    const T* vp = static_cast<const T*>(a.v_pages) + off;
+    static_for<kDC>([&](auto c) {
+      constexpr int kC = decltype(c)::value;
+      untracked_load16<kC * 64>(kf[kC], kp);
+      untracked_load16<kC * 64>(vf[kC], vp);
+    });
+  }
+
+  // steps: (query head, 32-row tile) pairs from the first tile a key of the
+  // block is visible in
+  const int q_first = sp.visible_from(kb0, a.mask_mode);
+  const int t0 = q_first / kQ, t1 = (rows + kQ - 1) / kQ;
+  const int n_steps = max(t1 - t0, 0) * G;
+
+  // Step n's Q and dO rows (rows past the end read the last row: finite, and
+  // masked), 16-byte chunks swizzled per row (QTile), plus LSE (lanes 0-31)
+  // and Delta (32-63) of its rows by the last wave.  The row base is uniform.
+  const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
+  const int rlast = rows - 1;
+  auto load_step = [&](int n, Buf& bf) __attribute__((always_inline)) {
+    const int h = g * G + n % G;
+    const int q0 = (t0 + n / G) * kQ;
+    const int rbase = min(q0, rlast);
+    const uint64_t row_bytes = (uint64_t)hq * D * sizeof(T);
+    const uint64_t base_off = (((uint64_t)b * a.q_len + rbase) * hq + h) * D * sizeof(T);
+    const char* qb = static_cast<const char*>(a.q) + base_off;
+    const char* gb = static_cast<const char*>(a.dout) + base_off;
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int l = wave * kLoadsPerWave + i;           // 0 .. 2 kLoads - 1: Q loads, then dO loads
+      const bool is_g = l >= Q::kLoads;                 // uniform
+      const int lq = is_g ? l - Q::kLoads : l;
+      const int r = lq * Q::kRowsPerLoad + lrow;        // row within the tile
+      const uint32_t off = (uint32_t)((uint64_t)(min(q0 + r, rlast) - rbase) * row_bytes) +
+                           ((lpos ^ Q::swz(r)) << 4);
+      lds_dma16(is_g ? gb : qb, off, lds_addr((is_g ? bf.g : bf.q) + lq * Q::kRowsPerLoad * D));
+    }
+    if (wave == kWaves - 1) {
+      const float* src = lane < 32 ? a.lse : a.delta;
+      const int64_t stat = ((int64_t)b * hq + h) * a.q_len + min(q0 + (lane & 31), rlast);
+      lds_dma4(src + stat, lds_addr(bf.l));
+    }
+  };
+
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  f32x4 dk[kDB], dv[kDB];
+#pragma unroll
+  for (int db = 0; db < kDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dk[db][i] = dv[db][i] = 0.f;
+
+  // Fragment addresses (bytes), one register per tile and pattern:
+  //  - row-wise A operand of S / dP: lane (gq, j) reads row 16blk + j, chunk
+  //    (4c + gq) ^ swz(row) = 4c ^ x with x = gq ^ swz(j) (swz(16blk + j) =
+  //    swz(j)): address ar ^ 64c, plus 16 rows for blk = 1;
+  //  - transposed A operand of dV^T / dK^T (ds_read_b64_tr_b16): lane j of
+  //    group gq points at row 4gq + j/4 (and 16 + 4gq + j/4), elements 16db +
+  //    4(j%4) .. +3, i.e. chunk 2db + e (e = (j%4)/2) at position 2db ^ (e ^
+  //    swz(row)), swz(row) the same for both rows: address at ^ 32db.
+  const int rr = 4 * gq + (j >> 2);
+  const uint32_t ar_off = (uint32_t)(j * D * 2 + ((gq ^ Q::swz(j)) << 4));
+  const uint32_t at_off = (uint32_t)(rr * D * 2 + ((((j & 3) >> 1) ^ Q::swz(rr)) << 4) + ((j & 1) << 3));
+  const float neg_inv_scale = -1.f / a.scale;
+  typedef __attribute__((address_space(3))) const u16x8_t* lds_frag_ptr;
+
+  // step n from buffer bf; the loads of steps n+1 and n+2 may be in flight
+  auto compute = [&](int n, const Buf& bf) __attribute__((always_inline)) {
+    const int q0 = (t0 + n / G) * kQ;
+    if (q0 + kQ <= wave_from) return;  // no row of the tile sees a key of this wave
+    uint32_t ar_q = lds_addr(bf.q) + ar_off, ar_g = lds_addr(bf.g) + ar_off;
+    uint32_t at_q = lds_addr(bf.q) + at_off, at_g = lds_addr(bf.g) + at_off;
+    asm volatile("" : "+v"(ar_q), "+v"(ar_g), "+v"(at_q), "+v"(at_g));
+    auto arow = [&](uint32_t base, int blk, int c) __attribute__((always_inline)) {
+      return __builtin_bit_cast(Frag, *(lds_frag_ptr)(uintptr_t)((base ^ (uint32_t)(64 * c)) + (uint32_t)(blk * 16 * D * 2)));
+    };
+    auto atr = [&](uint32_t base, int db) __attribute__((always_inline)) {
+      const uint32_t al = base ^ (uint32_t)(32 * db);
+      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(uintptr_t)al);
+      const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(uintptr_t)(al + 16 * D * 2));
+      const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
+                         (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
+      return __builtin_bit_cast(Frag, v);
+    };
+    // S and dP accumulators start from -LSE/scale and -Delta of their rows
+    f32x4 s[2], dp[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      const float4 lv = *reinterpret_cast<const float4*>(bf.l + 16 * blk + 4 * gq);
+      const float4 dl = *reinterpret_cast<const float4*>(bf.l + kQ + 16 * blk + 4 * gq);
+      s[blk][0] = lv.x * neg_inv_scale; s[blk][1] = lv.y * neg_inv_scale;
+      s[blk][2] = lv.z * neg_inv_scale; s[blk][3] = lv.w * neg_inv_scale;
+      dp[blk][0] = -dl.x; dp[blk][1] = -dl.y; dp[blk][2] = -dl.z; dp[blk][3] = -dl.w;
+    }
+#pragma unroll
+    for (int c = 0; c < kDC; ++c)
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(arow(ar_q, blk, c), kf[c], s[blk], 0, 0, 0);
+        dp[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(arow(ar_g, blk, c), vf[c], dp[blk], 0, 0, 0);
+      }
+    // P and dZ in the B-operand order of the dV / dK products: element t of
+    // a lane is row 4gq + t (t < 4) or 16 + 4gq + t - 4
+    Frag pf, zf;
+    const bool full = q0 >= wave_all && q0 + kQ <= rows;  // uniform: nothing masked
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = q0 + 16 * blk + 4 * gq + i;
+        const float e = fast_exp2(s[blk][i] * a.scale_log2);
+        const bool vis = full || (q >= tau && q < rows);
+        const float pv = vis ? e : 0.f;
+        pf[4 * blk + i] = (__bf16)pv;
+        zf[4 * blk + i] = (__bf16)(pv * dp[blk][i]);
+      }
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+      dv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(atr(at_g, db), pf, dv[db], 0, 0, 0);
+      dk[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(atr(at_q, db), zf, dk[db], 0, 0, 0);
+    }
+  };
+
+  // prologue: this wave's K/V operands, steps 0 and 1; wait for the operands
+  // and step 0 (step 1 may stay in flight)
+  const int my_vm = kVm + (wave == kWaves - 1 ? 1 : 0);
+  if (n_steps > 0) load_step(0, s_b0);
+  if (n_steps > 1) load_step(1, s_b1);
+  auto barrier_after = [&](int n) __attribute__((always_inline)) {
+    // step n+1's loads landed once only step n+2's are in flight
+    if (n + 2 < n_steps) {
+      if (my_vm == kVm) bare_barrier<kVm>();
+      else bare_barrier<kVm + 1>();
+    } else {
+      bare_barrier<0>();
+    }
+  };
+  barrier_after(-1);
+  auto step = [&](int n, auto par) __attribute__((always_inline)) {
+    constexpr int kPar = decltype(par)::value;
+    Buf& cur = kPar == 0 ? s_b0 : kPar == 1 ? s_b1 : s_b2;
+    Buf& nxt2 = kPar == 0 ? s_b2 : kPar == 1 ? s_b0 : s_b1;  // the buffer step n-1 used
+    if (n + 2 < n_steps) load_step(n + 2, nxt2);
+    compute(n, cur);
+    barrier_after(n);
+  };
+  for (int n = 0; n < n_steps; n += 3) {
+    step(n, std::integral_constant<int, 0>());
+    if (n + 1 >= n_steps) break;
+    step(n + 1, std::integral_constant<int, 1>());
+    if (n + 2 >= n_steps) break;
+    step(n + 2, std::integral_constant<int, 2>());
+  }
+
+  // lane (gq, j) holds d = 16db + 4gq + i (i < 4) of its key
+  if (key >= clen) return;
+  float* dkrow = a.dk_hat + (((int64_t)b * a.hat_cap + key) * heads + g) * D + 4 * gq;
+  float* dvrow = a.dv_hat + (((int64_t)b * a.hat_cap + key) * heads + g) * D + 4 * gq;
+  const float sc = a.scale;
+#pragma unroll
+  for (int db = 0; db < kDB; ++db) {
+    *reinterpret_cast<float4*>(dkrow + 16 * db) = make_float4(dk[db][0] * sc, dk[db][1] * sc, dk[db][2] * sc, dk[db][3] * sc);
+    *reinterpret_cast<float4*>(dvrow + 16 * db) = make_float4(dv[db][0], dv[db][1], dv[db][2], dv[db][3]);
+  }
+}
+
 template <typename T, int D, int G, bool kRuns>
 hipError_t launch_bwd_r(const PrefillBwdArgs& a, int batch, hipStream_t s) {
   const unsigned qitems = (unsigned)(batch * a.pv.kv_heads * a.num_q_tiles);
@@ -542,8 +778,11 @@ hipError_t launch_bwd_r(const PrefillBwdArgs& a, int batch, hipStream_t s) {
                                dim3(PrefillShape<G>::kThreads), s, a);
   if (e != hipSuccess) return e;
   const unsigned kitems = (unsigned)(batch * a.pv.kv_heads * a.num_key_tiles);
-  return launch_struct(prefill_bwd_dkdv_kernel<T, D, G, kRuns>, dim3(kitems),
-                       dim3(KvBwdShape<T, D>::kThreads), s, a);
+  if constexpr (sizeof(T) == 2)
+    return launch_struct(prefill_bwd_dkdv16_kernel<D, G, kRuns>, dim3(kitems), dim3(256), s, a);
+  else
+    return launch_struct(prefill_bwd_dkdv_kernel<T, D, G, kRuns>, dim3(kitems),
+                         dim3(KvBwdShape<T, D>::kThreads), s, a);
 }
 
 template <typename T, int D, int G>
@@ -574,7 +813,7 @@ int prefill_bwd_rows_per_tile(int group) {
 }
 
 int prefill_bwd_keys_per_block(int dtype, int head_dim) {
-  if (dtype == 1) return head_dim == 128 ? KvBwdShape<bf16_bits, 128>::kKeys : KvBwdShape<bf16_bits, 64>::kKeys;
+  if (dtype == 1) return 64;  // prefill_bwd_dkdv16_kernel: 16 keys per wave, four waves
   return head_dim == 128 ? KvBwdShape<float, 128>::kKeys : KvBwdShape<float, 64>::kKeys;
 }
 
