@@ -540,7 +540,8 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
 // waves owns 64 keys of one (sequence, KV head) and walks the (query head,
 // 32-row query tile) steps that see them; each step's Q, dO, LSE and Delta are
 // staged once in LDS for the four waves by untracked direct loads, two steps
-// ahead in three buffers, as in the forward.  Per step a wave computes
+// ahead in three buffers, as in the forward, and each wave reads its MFMA
+// operands four ahead of the products.  Per step a wave computes
 //   S  = Q K^T  - LSE/scale    (two 16 x 16 blocks: query rows 0-15, 16-31)
 //   dP = dO V^T - Delta
 //   P = exp2(scale log2e S),  dZ = P dP     (masked)
@@ -699,13 +700,43 @@ __global__ __launch_bounds__(256, 3) void prefill_bwd_dkdv16_kernel(PrefillBwdAr
       s[blk][2] = lv.z * neg_inv_scale; s[blk][3] = lv.w * neg_inv_scale;
       dp[blk][0] = -dl.x; dp[blk][1] = -dl.y; dp[blk][2] = -dl.z; dp[blk][3] = -dl.w;
     }
+    __builtin_amdgcn_sched_barrier(0);  // (these reads first)
+    // S / dP: 4 kDC MFMAs over 2 kDC row-wise operands of each tile, read
+    // kAheadS ahead of the chain
+    constexpr int kNS = 4 * kDC;  // (c, blk, S or dP)
+    auto aop = [&](int idx) __attribute__((always_inline)) {
+      const int c = idx / 4, blk = (idx / 2) % 2, t = idx % 2;
+      return arow(t ? ar_g : ar_q, blk, c);
+    };
+    constexpr int kAheadS = 4;
+    Frag sb[kAheadS];
 #pragma unroll
-    for (int c = 0; c < kDC; ++c)
+    for (int i = 0; i < kAheadS; ++i) sb[i] = aop(i);
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(arow(ar_q, blk, c), kf[c], s[blk], 0, 0, 0);
-        dp[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(arow(ar_g, blk, c), vf[c], dp[blk], 0, 0, 0);
-      }
+    for (int idx = 0; idx < kNS; ++idx) {
+      const Frag cur = sb[idx % kAheadS];
+      if (idx + kAheadS < kNS) sb[idx % kAheadS] = aop(idx + kAheadS);
+      const int c = idx / 4, blk = (idx / 2) % 2;
+      if (idx % 2 == 0) s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, kf[c], s[blk], 0, 0, 0);
+      else dp[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, vf[c], dp[blk], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, kAheadS, 0);  // DS reads
+#pragma unroll
+    for (int idx = 0; idx + kAheadS < kNS; ++idx) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAheadS, 0);
+
+    // the first transposed operands of dV / dK, read during the softmax
+    constexpr int kNT = 2 * kDB;  // (db, dV or dK)
+    auto top = [&](int idx) __attribute__((always_inline)) { return atr(idx % 2 ? at_q : at_g, idx / 2); };
+    constexpr int kAheadT = 4;
+    Frag tb[kAheadT];
+#pragma unroll
+    for (int i = 0; i < kAheadT; ++i) tb[i] = top(i);
+    __builtin_amdgcn_sched_barrier(0);
+
     // P and dZ in the B-operand order of the dV / dK products: element t of
     // a lane is row 4gq + t (t < 4) or 16 + 4gq + t - 4
     Frag pf, zf;
@@ -722,10 +753,19 @@ __global__ __launch_bounds__(256, 3) void prefill_bwd_dkdv16_kernel(PrefillBwdAr
         zf[4 * blk + i] = (__bf16)(pv * dp[blk][i]);
       }
 #pragma unroll
-    for (int db = 0; db < kDB; ++db) {
-      dv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(atr(at_g, db), pf, dv[db], 0, 0, 0);
-      dk[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(atr(at_q, db), zf, dk[db], 0, 0, 0);
+    for (int idx = 0; idx < kNT; ++idx) {
+      const Frag cur = tb[idx % kAheadT];
+      if (idx + kAheadT < kNT) tb[idx % kAheadT] = top(idx + kAheadT);
+      const int db = idx / 2;
+      if (idx % 2 == 0) dv[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, pf, dv[db], 0, 0, 0);
+      else dk[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, zf, dk[db], 0, 0, 0);
     }
+#pragma unroll
+    for (int idx = 0; idx + kAheadT < kNT; ++idx) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);  // (two transposed reads)
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAheadT, 1);
   };
 
   // prologue: this wave's K/V operands, steps 0 and 1; wait for the operands
