@@ -701,7 +701,7 @@ static int prefill_attn_bwd_impl(const void* q, int32_t batch, int32_t num_q_hea
       return SPEECHKV_ERR_ALIAS;
   }
   if (spans->max_total_len == 0) return SPEECHKV_OK;
-  const int rows_per_tile = skv::prefill_bwd_rows_per_tile(group);
+  const int rows_per_tile = skv::prefill_bwd_rows_per_tile(cache->dtype, group);
   const int64_t q_tiles = (spans->max_total_len + rows_per_tile - 1) / rows_per_tile;
   const int64_t keys = spans->max_total_len < hat_capacity ? spans->max_total_len : hat_capacity;
   const int keys_per_block = skv::prefill_bwd_keys_per_block(cache->dtype, cache->head_dim);

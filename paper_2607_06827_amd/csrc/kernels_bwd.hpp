@@ -65,7 +65,7 @@ struct PoolBwdArgs {
   SegmentTable segs;    // several speech runs per sequence when segs.seg_start is set
 };
 
-int prefill_bwd_rows_per_tile(int group);
+int prefill_bwd_rows_per_tile(int dtype, int group);
 int prefill_bwd_keys_per_block(int dtype, int head_dim);  // keys of one dK/dV block
 hipError_t launch_prefill_bwd(const PrefillBwdArgs& a, int dtype, int head_dim, int group,
                               int batch, hipStream_t s);

@@ -532,6 +532,304 @@ __global__ __launch_bounds__((KvBwdShape<T, D>::kThreads)) void prefill_bwd_dkdv
     }
 }
 
+// ---------------------------------------------------- dQ, bf16, 16 rows a wave
+//
+// The bf16 dQ kernel on the 16x16x32 MFMA.  A wave owns 16 query rows of one
+// query head and keeps their Q and dO operands in registers; a block of
+// kWaves waves owns 16 * kWaves / G rows of one (sequence, KV head) for all G
+// heads and streams the 32-key tiles they see through LDS (three buffers,
+// untracked direct loads two tiles ahead, as in the forward).  Per tile a
+// wave computes, keys as rows of the 16x16 blocks (so that P and dZ0 are
+// their own B operands, as in the dK/dV kernel):
+//   S^T = K Q^T,  dP^T = V dO^T       (two 16-key blocks)
+//   P = exp2(scale log2e S - log2e LSE),  dZ0 = P (dP - Delta0)
+//   dQ^T += K^T dZ0^T,  Kbar^T += K^T P^T    (16-row blocks of d)
+// with Delta0 = dO . O (the stored output) and the exact Delta = sum P dP
+// beside it; at the end dQ = scale (dZ0 K + (Delta0 - Delta) Kbar).
+template <int G>
+struct DqShape16 {
+  static constexpr int kRowBlocks = G >= 4 ? 1 : 4 / G;
+  static constexpr int kWaves = G * kRowBlocks;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kRows = 16 * kRowBlocks;
+};
+
+template <int D, int G, bool kRuns>
+__global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_kernel(PrefillBwdArgs a) {
+  typedef bf16_bits T;
+  typedef QTile<T, D> Q;  // the K and V tiles: 32 rows, chunks swizzled per row
+  typedef bf16x8_t Frag;
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  constexpr int kWaves = DqShape16<G>::kWaves;
+  constexpr int kRows = DqShape16<G>::kRows;
+  constexpr int kKeys = 32;
+  constexpr int kDC = D / 32;  // K-dim chunks of S^T and dP^T
+  constexpr int kDB = D / 16;  // 16-row blocks of dQ^T and Kbar^T
+  constexpr int kLoadsPerWave = Q::kLoads >= kWaves ? Q::kLoads / kWaves : 1;
+  static_assert(Q::kLoads % kWaves == 0 || kWaves % Q::kLoads == 0, "loads split evenly over waves");
+  constexpr int kVm = 2 * kLoadsPerWave;
+
+  __shared__ __attribute__((aligned(256))) T s_k0[Q::kElems];
+  __shared__ __attribute__((aligned(256))) T s_k1[Q::kElems];
+  __shared__ __attribute__((aligned(256))) T s_k2[Q::kElems];
+  __shared__ __attribute__((aligned(256))) T s_v0[Q::kElems];
+  __shared__ __attribute__((aligned(256))) T s_v1[Q::kElems];
+  __shared__ __attribute__((aligned(256))) T s_v2[Q::kElems];
+
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
+  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  const int heads = a.pv.kv_heads;
+  const int tile = a.num_q_tiles - 1 - item % a.num_q_tiles;  // heavy tiles (late rows) first
+  const int g = (item / a.num_q_tiles) % heads;
+  const int b = item / a.num_q_tiles / heads;
+
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
+  const int p0 = tile * kRows;
+  if (p0 >= rows) return;
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
+  const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int gq = lane >> 4, j = lane & 15;
+  const int h = g * G + wave % G;
+  const int wrow0 = p0 + (wave / G) * 16;  // first row of this wave
+  const int q = wrow0 + j;                 // this lane's row (column of the C layout)
+  const bool qvalid = q < rows;
+  const int nvis = qvalid ? min(sp.visible(q, a.mask_mode), clen) : 0;
+  const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
+  const int hq = a.num_q_heads;
+  const int shift = a.pv.page_shift, slot_mask = (1 << shift) - 1;
+  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
+  const int ntiles = (kmax + kKeys - 1) / kKeys;
+  const bool loads = Q::kLoads >= kWaves || wave < Q::kLoads;
+  auto load_row0 = [&](int i) { return (Q::kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * Q::kRowsPerLoad; };
+  const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
+
+  // this lane's row of Q, dO and O (elements 32c + 8gq .. +7, the B operand
+  // layout of S^T = K Q^T) and its LSE; rows past the end read row 0 of the
+  // sequence (finite, never stored)
+  Frag qf[kDC], gf[kDC], of[kDC];
+  float lse = 0.f;
+  {
+    const int64_t row = ((int64_t)b * a.q_len + (qvalid ? q : 0)) * hq + h;
+    const T* qp = static_cast<const T*>(a.q) + row * D + 8 * gq;
+    const T* gp = static_cast<const T*>(a.dout) + row * D + 8 * gq;
+    const T* op = static_cast<const T*>(a.out) + row * D + 8 * gq;
+    static_for<kDC>([&](auto c) {
+      constexpr int kC = decltype(c)::value;
+      untracked_load16<kC * 64>(qf[kC], qp);
+      untracked_load16<kC * 64>(gf[kC], gp);
+      untracked_load16<kC * 64>(of[kC], op);
+    });
+    const float* lp = a.lse + ((int64_t)b * hq + h) * a.q_len + (qvalid ? q : 0);
+    asm volatile("global_load_dword %0, %1, off" : "=v"(lse) : "v"(lp) : "memory");
+  }
+
+  // block-table entries: one per wave and tile (the forward's scheme)
+  constexpr int kWaveRows = kLoadsPerWave * Q::kRowsPerLoad;
+  static_assert(kWaveRows <= 8, "one page holds a wave's rows of a tile");
+  const int wrow_load = loads ? load_row0(0) : 0;
+  typedef __attribute__((address_space(4))) const int32_t* const_ptr;
+  auto table_load = [&](int kt) __attribute__((always_inline)) {
+    const int row0 = min(kt * kKeys + wrow_load, kclamp);
+    return ((const_ptr)table_row)[min(row0 >> shift, a.pv.max_pages - 1)];
+  };
+  const uint64_t head_bytes = (uint64_t)D * sizeof(T) << shift;
+  const uint64_t page_bytes = head_bytes * heads;
+  const uintptr_t kpool_g = (uintptr_t)a.k_pages + (uint64_t)g * head_bytes;
+  const uintptr_t v_minus_k = (uintptr_t)a.v_pages - (uintptr_t)a.k_pages;
+  const uint32_t npages = (uint32_t)a.pv.num_pages;
+  auto tile_load = [&](int kt, int e, T* sk, T* sv) __attribute__((always_inline)) {
+    if (!loads) return;
+    const uint32_t page = (uint32_t)e < npages ? (uint32_t)e : 0u;  // a bad entry reads an in-range page
+    const uintptr_t kbase = kpool_g + (uint64_t)page * page_bytes;
+    const uintptr_t vbase = kbase + v_minus_k;
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+      const int r = load_row0(i) + lrow;
+      const int key = min(kt * kKeys + r, kclamp);
+      const uint32_t off = (uint32_t)((key & slot_mask) * D * 2) + ((lpos ^ Q::swz(r)) << 4);
+      lds_dma16((const void*)kbase, off, lds_addr(sk + load_row0(i) * D));
+      lds_dma16((const void*)vbase, off, lds_addr(sv + load_row0(i) * D));
+    }
+  };
+
+  f32x4 dq[kDB], kbar[kDB];
+#pragma unroll
+  for (int db = 0; db < kDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dq[db][i] = kbar[db][i] = 0.f;
+  float dsum = 0.f;  // this lane's share of Delta = sum over keys of P dP
+
+  // prologue: the row operands (issued above), tiles 0 and 1; wait for the
+  // operands and tile 0
+  int pg[3] = {table_load(0), table_load(1), table_load(2)};
+  tile_load(0, pg[0], s_k0, s_v0);
+  if (ntiles > 1) {
+    tile_load(1, pg[1], s_k1, s_v1);
+    bare_barrier<kVm>();
+  } else {
+    bare_barrier<0>();
+  }
+  // Delta0 = dO . O over the row: the lane's 32 products, then the four lane
+  // groups that share the row
+  float delta0 = 0.f;
+#pragma unroll
+  for (int c = 0; c < kDC; ++c) delta0 += frag_dot(gf[c], of[c]);
+  delta0 += __shfl_xor(delta0, 16, 64);
+  delta0 += __shfl_xor(delta0, 32, 64);
+  const float lse2 = lse * kLog2eF;
+
+  // fragment addresses (bytes), one register per tile and pattern, as in the
+  // dK/dV kernel: row-wise operands of S^T / dP^T at ar ^ 64c (+16 rows for
+  // the second key block), transposed K^T operands at at ^ 32db (+16 rows)
+  const int rr = 4 * gq + (j >> 2);
+  const uint32_t ar_off = (uint32_t)(j * D * 2 + ((gq ^ Q::swz(j)) << 4));
+  const uint32_t at_off = (uint32_t)(rr * D * 2 + ((((j & 3) >> 1) ^ Q::swz(rr)) << 4) + ((j & 1) << 3));
+  typedef __attribute__((address_space(3))) const u16x8_t* lds_frag_ptr;
+
+  auto attend = [&](int kt, const T* sk, const T* sv) __attribute__((always_inline)) {
+    uint32_t ar_k = lds_addr(sk) + ar_off, ar_v = lds_addr(sv) + ar_off, at_k = lds_addr(sk) + at_off;
+    asm volatile("" : "+v"(ar_k), "+v"(ar_v), "+v"(at_k));
+    auto arow = [&](uint32_t base, int blk, int c) __attribute__((always_inline)) {
+      return __builtin_bit_cast(Frag, *(lds_frag_ptr)(uintptr_t)((base ^ (uint32_t)(64 * c)) + (uint32_t)(blk * 16 * D * 2)));
+    };
+    auto atr = [&](int db) __attribute__((always_inline)) {
+      const uint32_t al = at_k ^ (uint32_t)(32 * db);
+      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(uintptr_t)al);
+      const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(uintptr_t)(al + 16 * D * 2));
+      const u16x8_t v = {(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
+                         (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
+      return __builtin_bit_cast(Frag, v);
+    };
+    // S^T and dP^T: rows = keys 16 blk + 4 gq + i of the tile, column = row q
+    f32x4 s[2], dp[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[blk][i] = dp[blk][i] = 0.f;
+    constexpr int kNS = 4 * kDC;  // (c, blk, S or dP)
+    auto aop = [&](int idx) __attribute__((always_inline)) {
+      const int c = idx / 4, blk = (idx / 2) % 2, t = idx % 2;
+      return arow(t ? ar_v : ar_k, blk, c);
+    };
+    constexpr int kAheadS = 3;
+    Frag sb[kAheadS];
+#pragma unroll
+    for (int i = 0; i < kAheadS; ++i) sb[i] = aop(i);
+#pragma unroll
+    for (int idx = 0; idx < kNS; ++idx) {
+      const Frag cur = sb[idx % kAheadS];
+      if (idx + kAheadS < kNS) sb[idx % kAheadS] = aop(idx + kAheadS);
+      const int c = idx / 4, blk = (idx / 2) % 2;
+      if (idx % 2 == 0) s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, qf[c], s[blk], 0, 0, 0);
+      else dp[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, gf[c], dp[blk], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, kAheadS, 0);
+#pragma unroll
+    for (int idx = 0; idx + kAheadS < kNS; ++idx) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAheadS, 0);
+
+    constexpr int kAheadT = 2;
+    Frag tb[kAheadT];
+#pragma unroll
+    for (int i = 0; i < kAheadT; ++i) tb[i] = atr(i);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // P and dZ0 in the order of the B operand (element t: key 4gq + t, t < 4,
+    // or 16 + 4gq + t - 4); keys past the row's bound get weight 0
+    float pv[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) pv[t] = fast_exp2(__builtin_fmaf(s[t / 4][t % 4], a.scale_log2, -lse2));
+    const int kb = kt * kKeys;
+    if (kb + kKeys > nvis_lo) {  // uniform: the tile straddles some row's bound
+      const int lim = nvis - kb - 4 * gq;  // element t is visible iff 16 (t/4) + t%4 < lim
+#pragma unroll
+      for (int t = 0; t < 8; ++t) pv[t] = 16 * (t / 4) + t % 4 < lim ? pv[t] : 0.f;
+    }
+    Frag pf, zf;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const float d = dp[t / 4][t % 4];
+      dsum = __builtin_fmaf(pv[t], d, dsum);
+      pf[t] = (__bf16)pv[t];
+      zf[t] = (__bf16)(pv[t] * (d - delta0));
+    }
+    // dQ^T += K^T dZ0^T and Kbar^T += K^T P^T, one transposed K operand each
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+      const Frag cur = tb[db % kAheadT];
+      if (db + kAheadT < kDB) tb[db % kAheadT] = atr(db + kAheadT);
+      dq[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, zf, dq[db], 0, 0, 0);
+      kbar[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur, pf, kbar[db], 0, 0, 0);
+    }
+#pragma unroll
+    for (int db = 0; db + kAheadT < kDB; ++db) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * kAheadT, 1);
+  };
+
+  auto tile_step = [&](int kt, auto par) {
+    constexpr int kPar = decltype(par)::value;
+    constexpr int kNext2 = (kPar + 2) % 3;
+    T* const sk = kPar == 0 ? s_k0 : kPar == 1 ? s_k1 : s_k2;
+    T* const sv = kPar == 0 ? s_v0 : kPar == 1 ? s_v1 : s_v2;
+    const bool more = kt + 2 < ntiles;  // uniform
+    if (more) {
+      tile_load(kt + 2, pg[kNext2], kNext2 == 0 ? s_k0 : kNext2 == 1 ? s_k1 : s_k2,
+                kNext2 == 0 ? s_v0 : kNext2 == 1 ? s_v1 : s_v2);
+      if (kt + 3 < ntiles) pg[kPar] = table_load(kt + 3);
+    }
+    attend(kt, sk, sv);
+    if (more) bare_barrier<kVm>();
+    else bare_barrier<0>();
+  };
+  for (int kt = 0; kt < ntiles; kt += 3) {
+    tile_step(kt, std::integral_constant<int, 0>());
+    if (kt + 1 >= ntiles) break;
+    tile_step(kt + 1, std::integral_constant<int, 1>());
+    if (kt + 2 >= ntiles) break;
+    tile_step(kt + 2, std::integral_constant<int, 2>());
+  }
+
+  // Delta over the whole row, then dQ = scale (dZ0 K + (Delta0 - Delta) Kbar)
+  float delta = dsum;
+  delta += __shfl_xor(delta, 16, 64);
+  delta += __shfl_xor(delta, 32, 64);
+  const int64_t stat = ((int64_t)b * hq + h) * a.q_len + q;
+  if (gq == 0 && qvalid) a.delta[stat] = delta;
+  const float sc = a.scale, fix = delta0 - delta;
+  // rows leave through LDS (the idle tile buffers, 4 KB per wave: row j,
+  // 16-byte chunks swizzled as in the tiles) as 16-byte row stores
+  static_assert(kWaves <= 8, "a 16-row half of one tile buffer per wave");
+  T* const so = (wave / 2 == 0 ? s_k0 : wave / 2 == 1 ? s_k1 : wave / 2 == 2 ? s_k2 : s_v0) + (wave % 2) * 16 * D;
+#pragma unroll
+  for (int db = 0; db < kDB; ++db) {
+    const int e = 16 * db + 4 * gq;  // first of the lane's four elements
+    Mfma<T>::store4(so + j * D + ((((e >> 3) ^ Q::swz(j)) << 3) | (e & 7)),
+                    sc * __builtin_fmaf(fix, kbar[db][0], dq[db][0]), sc * __builtin_fmaf(fix, kbar[db][1], dq[db][1]),
+                    sc * __builtin_fmaf(fix, kbar[db][2], dq[db][2]), sc * __builtin_fmaf(fix, kbar[db][3], dq[db][3]));
+  }
+  __syncthreads();
+  T* const dqp = static_cast<T*>(a.dq);
+#pragma unroll
+  for (int r0 = 0; r0 < 16; r0 += Q::kRowsPerLoad) {
+    const int r = r0 + lrow, row = wrow0 + r;
+    if (row < rows) {
+      const uint4 v = *reinterpret_cast<const uint4*>(so + r * D + ((lpos ^ Q::swz(r)) << 3));
+      *reinterpret_cast<uint4*>(dqp + (((int64_t)b * a.q_len + row) * hq + h) * D + lpos * 8) = v;
+    }
+  }
+}
+
 // ----------------------------------------------- dK / dV, bf16, 16 keys a wave
 //
 // The bf16 dK/dV kernel on the 16x16x32 MFMA: a wave owns 16 keys, so its K
@@ -740,18 +1038,26 @@ __global__ __launch_bounds__(256, 3) void prefill_bwd_dkdv16_kernel(PrefillBwdAr
     // P and dZ in the B-operand order of the dV / dK products: element t of
     // a lane is row 4gq + t (t < 4) or 16 + 4gq + t - 4
     Frag pf, zf;
-    const bool full = q0 >= wave_all && q0 + kQ <= rows;  // uniform: nothing masked
+    float pv[8];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = q0 + 16 * blk + 4 * gq + i;
-        const float e = fast_exp2(s[blk][i] * a.scale_log2);
-        const bool vis = full || (q >= tau && q < rows);
-        const float pv = vis ? e : 0.f;
-        pf[4 * blk + i] = (__bf16)pv;
-        zf[4 * blk + i] = (__bf16)(pv * dp[blk][i]);
+      for (int i = 0; i < 4; ++i) pv[4 * blk + i] = fast_exp2(s[blk][i] * a.scale_log2);
+    if (q0 < wave_all || q0 + kQ > rows) {  // uniform: some row or key masked
+      // row 16 blk + 4 gq + i of the tile is visible to this lane's key iff
+      // it lies in [tau, rows): 16 blk + i in [lo, hi)
+      const int lo = tau - q0 - 4 * gq, hi = rows - q0 - 4 * gq;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int r = 16 * (t / 4) + t % 4;
+        pv[t] = r >= lo && r < hi ? pv[t] : 0.f;
       }
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      pf[t] = (__bf16)pv[t];
+      zf[t] = (__bf16)(pv[t] * dp[t / 4][t % 4]);
+    }
 #pragma unroll
     for (int idx = 0; idx < kNT; ++idx) {
       const Frag cur = tb[idx % kAheadT];
@@ -814,8 +1120,11 @@ __global__ __launch_bounds__(256, 3) void prefill_bwd_dkdv16_kernel(PrefillBwdAr
 template <typename T, int D, int G, bool kRuns>
 hipError_t launch_bwd_r(const PrefillBwdArgs& a, int batch, hipStream_t s) {
   const unsigned qitems = (unsigned)(batch * a.pv.kv_heads * a.num_q_tiles);
-  hipError_t e = launch_struct(prefill_bwd_dq_kernel<T, D, G, kRuns>, dim3(qitems),
-                               dim3(PrefillShape<G>::kThreads), s, a);
+  hipError_t e;
+  if constexpr (sizeof(T) == 2)
+    e = launch_struct(prefill_bwd_dq16_kernel<D, G, kRuns>, dim3(qitems), dim3(DqShape16<G>::kThreads), s, a);
+  else
+    e = launch_struct(prefill_bwd_dq_kernel<T, D, G, kRuns>, dim3(qitems), dim3(PrefillShape<G>::kThreads), s, a);
   if (e != hipSuccess) return e;
   const unsigned kitems = (unsigned)(batch * a.pv.kv_heads * a.num_key_tiles);
   if constexpr (sizeof(T) == 2)
@@ -843,7 +1152,15 @@ hipError_t launch_bwd_d(const PrefillBwdArgs& a, int group, int batch, hipStream
 
 }  // namespace
 
-int prefill_bwd_rows_per_tile(int group) {
+int prefill_bwd_rows_per_tile(int dtype, int group) {
+  if (dtype == 1) {  // prefill_bwd_dq16_kernel
+    switch (group) {
+      case 1: return DqShape16<1>::kRows;
+      case 2: return DqShape16<2>::kRows;
+      case 4: return DqShape16<4>::kRows;
+      default: return DqShape16<8>::kRows;
+    }
+  }
   switch (group) {
     case 1: return PrefillShape<1>::kRows;
     case 2: return PrefillShape<2>::kRows;
