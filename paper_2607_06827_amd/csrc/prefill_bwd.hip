@@ -31,8 +31,12 @@
 //     S = Q K^T,  dP = dO V^T               (queries x keys, one key per lane)
 //     dV^T += dO^T P,  dK^T += Q^T dZ        (dO^T, Q^T read transposed)
 //   starting S and dP from -LSE/scale and -Delta of their rows.
-// All products run on the 32x32 MFMAs (bf16 operands with P and dZ rounded to
-// bf16, or fp32), accumulating in fp32; dK^ and dV^ are written in fp32.
+// The fp32 kernels below run every product on the 32x32x2 fp32 MFMA.  The
+// bf16 kernels (further down) keep this split and these formulas on the
+// 16x16x32 bf16 MFMA with smaller per-wave tiles (16 query rows, or 16 keys, a
+// wave), so that three waves share each SIMD; P and dZ are rounded to bf16 as
+// MFMA operands, every product accumulates in fp32, and dK^ and dV^ are
+// written in fp32.
 // The mask's visibility rule comes from the span view (spans.hpp): one run
 // per sequence, or the runs of a segment table (kRuns).
 #include <climits>
