@@ -644,10 +644,12 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
     static_for<kQChunks>([&](auto kc) { untracked_load16<decltype(kc)::value * 16 * 2>(qf[decltype(kc)::value], qrow); });
   }
   __builtin_amdgcn_sched_barrier(0);
-  if (ntiles > 1) {
+  if (ntiles > 1 && loads) {
     tile_load(1, pg[1], s_k1, s_v1);
     bare_barrier<kVm>();
   } else {
+    // (a wave that loads no tile rows has only its query loads in flight:
+    // it waits for all of them)
     bare_barrier<0>();
   }
 

@@ -672,10 +672,12 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
   // operands and tile 0
   int pg[3] = {table_load(0), table_load(1), table_load(2)};
   tile_load(0, pg[0], s_k0, s_v0);
-  if (ntiles > 1) {
+  if (ntiles > 1 && loads) {
     tile_load(1, pg[1], s_k1, s_v1);
     bare_barrier<kVm>();
   } else {
+    // (a wave that loads no tile rows has only its row operands in flight:
+    // it waits for all of them)
     bare_barrier<0>();
   }
   // Delta0 = dO . O over the row: the lane's 32 products, then the four lane

@@ -39,6 +39,7 @@ CASES = {
     "prefix-empty": Case(P=[0, 0], T=[37, 9], N=[3, 0], w=4, D=128),
     "gqa-g4": Case(P=[5], T=[70], N=[6], Hq=8, Hkv=2, D=128),
     "gqa-g8": Case(P=[5], T=[33], N=[2], Hq=8, Hkv=1, D=64),
+    "gqa-g8-d64-tiles": Case(P=[5, 2], T=[300, 90], N=[8, 4], Hq=16, Hkv=2, D=64),
     "w8": Case(P=[4, 2], T=[77, 64], N=[6, 1], w=8, D=128),
     "w12-three-groups": Case(P=[1], T=[61], N=[2], w=12, D=64),
     "zero-gate": Case(P=[4], T=[70], N=[3], zero_gate=True, D=128),

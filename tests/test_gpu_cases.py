@@ -33,6 +33,9 @@ CASES = {
     "g4": Case(P=[4], T=[70], N=[3], Hq=8, Hkv=2, D=128),
     "g8": Case(P=[4], T=[70], N=[3], Hq=8, Hkv=1, D=128),
     "g8-f32-d64": Case(P=[4], T=[70], N=[3], Hq=16, Hkv=2, D=64, dtype="f32"),
+    # bf16, 64-wide heads, group 8: half the waves of a prefill block load no
+    # tile rows and wait only for their query rows
+    "g8-bf16-d64": Case(P=[4, 9], T=[170, 61], N=[3, 12], Hq=16, Hkv=2, D=64),
     "zero-gate": Case(P=[4], T=[70], N=[3], zero_gate=True),
     "sharp-gate-and-queries": Case(P=[4, 1], T=[70, 33], N=[3, 2], gate_scale=10.0, q_scale=3.0,
                                    D=128),
