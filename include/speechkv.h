@@ -517,8 +517,8 @@ size_t speechkv_prefill_attn_bwd_workspace_bytes(int32_t batch,
  * du = 0.
  *
  * k_raw, v_raw   device, element type dtype, strides as for speechkv_pool_kv.
- * num_kv_heads, head_dim  the raw tensors' heads and head size (64 or 128);
- *                num_kv_heads * head_dim / 8 must divide 256 (UNSUPPORTED).
+ * num_kv_heads, head_dim  the raw tensors' heads (at most 65535) and head
+ *                size (64 or 128); otherwise UNSUPPORTED.
  * spans, w, gate_u, layer, l0  as for the forward call (gate_u NULL: zero gate).
  * dk_hat, dv_hat device fp32 [batch][hat_capacity][num_kv_heads][head_dim],
  *                e.g. from speechkv_prefill_attn_bwd.  Caller obligation:

@@ -789,6 +789,7 @@ static int pool_kv_bwd_impl(const void* k_raw, const void* v_raw, int64_t stride
   if (dtype != SPEECHKV_DTYPE_F32 && dtype != SPEECHKV_DTYPE_BF16) return SPEECHKV_ERR_UNSUPPORTED;
   if (head_dim != 64 && head_dim != 128) return SPEECHKV_ERR_UNSUPPORTED;
   if (num_kv_heads < 1 || batch < 1) return SPEECHKV_ERR_INVALID_ARG;
+  if (num_kv_heads > kMaxGrid) return SPEECHKV_ERR_UNSUPPORTED;
   if (spans->max_total_len > raw_len) return SPEECHKV_ERR_INVALID_ARG;
   const int spb = skv::pool_bwd_slots_per_block(batch, spans->max_total_len, num_kv_heads, head_dim);
   if (spb == 0) return SPEECHKV_ERR_UNSUPPORTED;
@@ -843,8 +844,8 @@ static int pool_kv_bwd_impl(const void* k_raw, const void* v_raw, int64_t stride
   a.du = du;
   a.du_part = du ? static_cast<float*>(workspace) : nullptr;
   a.max_out = spans->max_total_len;
-  a.slots_per_block = spb;
-  a.blocks_per_seq = spans->max_total_len > 0 ? (spans->max_total_len + spb - 1) / spb : 1;
+  skv::pool_bwd_grid(batch, spans->max_total_len, hat_capacity, num_kv_heads, head_dim, &a.slots_per_block,
+                     &a.blocks_per_seq);
   if (segs) a.segs = *segs;
   return status_of(skv::launch_pool_bwd(a, dtype, head_dim, batch, static_cast<hipStream_t>(stream)));
 }

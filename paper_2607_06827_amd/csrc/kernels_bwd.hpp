@@ -73,6 +73,11 @@ hipError_t launch_prefill_bwd(const PrefillBwdArgs& a, int dtype, int head_dim, 
 // slots one pass of 256 threads covers), and so the size of the partial
 // gate-gradient buffer; 0 when (kv_heads, head_dim) is not supported.
 int pool_bwd_slots_per_block(int batch, int max_out, int kv_heads, int head_dim);
+// The launch's slots per block and blocks per (sequence, head): sized from
+// min(max_out, hat_cap), the slots that can hold work, and never more blocks
+// than the workspace of pool_bwd_slots_per_block holds.  Arguments must have
+// passed pool_bwd_slots_per_block.
+void pool_bwd_grid(int batch, int max_out, int hat_cap, int kv_heads, int head_dim, int* spb, int* blocks);
 hipError_t launch_pool_bwd(const PoolBwdArgs& a, int dtype, int head_dim, int batch,
                            hipStream_t s);
 

@@ -11,15 +11,17 @@
 // the row it became.  The slots' source rows come from the span view
 // (spans.hpp): one run per sequence, or the runs of a segment table (kRuns).
 //
-// Layout: each thread owns 8 consecutive elements of one KV head; D/8 threads
-// cover a head, kv_heads * D/8 a slot of the compressed sequence, and a block
-// walks `iters` groups of 256 / (kv_heads * D/8) slots of one sequence, iters
-// chosen so that the whole launch has about a thousand blocks.  Every
+// Layout: each thread owns 8 consecutive elements of one KV head; D/8
+// threads cover a (slot, head) unit, and a 256-thread block covers
+// 256 / (D/8) consecutive slots of one head of one sequence per pass, `iters`
+// passes (iters chosen so that the launch has a few thousand blocks).  Every
 // raw row is read at most twice (once more for windows longer than four
 // frames) and every gradient row written once: the kernel is bound by HBM
-// bandwidth.  The gate gradient is kept per thread, summed over the block in
-// LDS into one partial per block, and the partials are summed by a second
-// kernel in a fixed order, so the result does not depend on scheduling.
+// bandwidth.  The gate gradient is kept per thread, summed over the block
+// (lanes with the same elements by a butterfly within the wave, then the
+// waves in LDS) into one D-float partial per block, and the partials are
+// summed by a second kernel in a fixed order, so the result does not depend
+// on scheduling.
 #include "kernels.hpp"
 #include "kernels_bwd.hpp"
 
@@ -28,7 +30,7 @@ namespace skv {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kTargetBlocks = 1024;  // about four blocks per CU, and as many gate partials
+constexpr int kTargetBlocks = 4096;  // ~16 blocks per CU; more are taken one pass each
 
 template <int D>
 constexpr int lanes_per_head() { return D / 8; }
@@ -36,13 +38,11 @@ constexpr int lanes_per_head() { return D / 8; }
 template <typename T, int D, bool kGate, bool kRuns>
 __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
   constexpr int kLanes = lanes_per_head<D>();
+  constexpr int kSlotLanes = 256 / kLanes;  // slots per pass
   const int heads = a.kv_heads;
-  const int per_slot = heads * kLanes;   // threads per slot (divides 256)
-  const int slot_lanes = 256 / per_slot;
   const int tid = threadIdx.x;
-  const int sl = tid / per_slot, u = tid % per_slot;
-  const int g = u / kLanes, j = u % kLanes;
-  const int b = blockIdx.y;
+  const int sl = tid / kLanes, j = tid % kLanes;
+  const int g = blockIdx.y, b = blockIdx.z;
 
   const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int len = min(min(sp.clen(), a.max_out), a.hat_cap);
@@ -68,10 +68,10 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) du[e] = 0.f;
 
-  const int iters = a.slots_per_block / slot_lanes;
+  const int iters = a.slots_per_block / kSlotLanes;
   for (int k = 0; k < iters; ++k) {
-    const int c = (blockIdx.x * iters + k) * slot_lanes + sl;
-    if (sl >= slot_lanes || c >= len) continue;
+    const int c = (blockIdx.x * iters + k) * kSlotLanes + sl;
+    if (c >= len) continue;
     const SlotSource slot = sp.slot(c);
     const int src = slot.first, n = slot.frames;
     if (src + n > a.raw_len) continue;  // a broken caller obligation: rows left alone
@@ -167,52 +167,80 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
   }
 
   if (!a.du_part) return;
-  // this block's gate gradient: the slot lanes' sums, in LDS, in a fixed order
-  __shared__ float s_du[256 * 8];
+  // this block's gate gradient: the slots of each wave by a butterfly over
+  // the lanes that hold the same elements (lane bits above the unit's), then
+  // the four waves in LDS, in a fixed order
 #pragma unroll
-  for (int e = 0; e < 8; ++e) s_du[tid * 8 + e] = du[e];
+  for (int m = kLanes; m < 64; m <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) du[e] += xor_shuffle(du[e], m);
+  __shared__ float s_du[4][D];
+  const int wave = tid >> 6, lane = tid & 63;
+  if (lane < kLanes) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s_du[wave][8 * lane + e] = du[e];
+  }
   __syncthreads();
-  if (tid < per_slot) {
-    float acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-    for (int q = 0; q < slot_lanes; ++q)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += s_du[(q * per_slot + tid) * 8 + e];
-    float* dst = a.du_part + ((int64_t)b * a.blocks_per_seq + blockIdx.x) * heads * D + g * D + 8 * j;
-    reinterpret_cast<float4*>(dst)[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-    reinterpret_cast<float4*>(dst)[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  if (tid < D) {
+    const float sum = (s_du[0][tid] + s_du[1][tid]) + (s_du[2][tid] + s_du[3][tid]);
+    a.du_part[(((int64_t)b * a.blocks_per_seq + blockIdx.x) * heads + g) * D + tid] = sum;
   }
 }
 
-// du[i] = sum over the per-block partials: 64 threads per output each add
-// every 64th partial (four independent sums), then the 64 sums are added in
-// LDS in a fixed order.
-constexpr int kReduceOut = 4;  // outputs per 256-thread block
-__global__ __launch_bounds__(256) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
-  __shared__ float s_sum[256];
-  const int o = threadIdx.x % kReduceOut, r = threadIdx.x / kReduceOut;  // r < 64
-  const int i = blockIdx.x * kReduceOut + o;
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  if (i < n) {
-    int p = r;
-    for (; p + 3 * 64 < parts; p += 4 * 64)
+// du[i] = sum over the per-block partials (a block that saw no slot of its
+// head wrote zeros).  A 1024-thread block sums 64 consecutive outputs: each
+// thread four of them (one 16-byte load per partial) over every 64th partial,
+// eight loads in flight; the 64 lanes of an output quad are then added in a
+// fixed order, four within each wave (a butterfly) and the 16 waves in LDS.
+constexpr int kReduceLanes = 64;
+__global__ __launch_bounds__(1024) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
+  __shared__ float4 s_sum[16][16];
+  const int q = threadIdx.x % 16, r = threadIdx.x / 16;  // output quad, part lane
+  const int i = blockIdx.x * 64 + 4 * q;                 // first of this thread's outputs
+  float4 acc[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[q] += part[(int64_t)(p + q * 64) * n + i];
-    for (int q = 0; p < parts; p += 64, ++q) acc[q & 3] += part[(int64_t)p * n + i];
+  for (int u = 0; u < 8; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < n) {
+    for (int p0 = 0; p0 < parts; p0 += 8 * kReduceLanes) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + u * kReduceLanes + r;
+        if (p < parts) {
+          const float4 v = *reinterpret_cast<const float4*>(part + (int64_t)p * n + i);
+          acc[u].x += v.x; acc[u].y += v.y; acc[u].z += v.z; acc[u].w += v.w;
+        }
+      }
+    }
   }
-  s_sum[threadIdx.x] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll
+  for (int w = 4; w >= 1; w >>= 1)
+#pragma unroll
+    for (int u = 0; u < w; ++u) {
+      acc[u].x += acc[u + w].x; acc[u].y += acc[u + w].y; acc[u].z += acc[u + w].z; acc[u].w += acc[u + w].w;
+    }
+  // lanes q, q + 16, q + 32, q + 48 of a wave hold the same outputs
+#pragma unroll
+  for (int m = 16; m < 64; m <<= 1) {
+    acc[0].x += xor_shuffle(acc[0].x, m); acc[0].y += xor_shuffle(acc[0].y, m);
+    acc[0].z += xor_shuffle(acc[0].z, m); acc[0].w += xor_shuffle(acc[0].w, m);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) < 16) s_sum[wave][q] = acc[0];
   __syncthreads();
-  if (r == 0 && i < n) {
-    float sum = 0.f;
-    for (int k = 0; k < 64; ++k) sum += s_sum[k * kReduceOut + o];
-    du[i] = sum;
+  if (threadIdx.x < 16 && i < n) {
+    float4 sum = s_sum[0][q];
+#pragma unroll
+    for (int k = 1; k < 16; ++k) {
+      const float4 v = s_sum[k][q];
+      sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+    }
+    *reinterpret_cast<float4*>(du + i) = sum;
   }
 }
 
 template <typename T, int D>
 hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
-  const dim3 grid((unsigned)a.blocks_per_seq, batch);
+  const dim3 grid((unsigned)a.blocks_per_seq, (unsigned)a.kv_heads, (unsigned)batch);
   hipError_t e;
   if (a.segs.seg_start)
     e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true, true>, grid, dim3(256), s, a)
@@ -221,9 +249,9 @@ hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
     e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true, false>, grid, dim3(256), s, a)
                : launch_struct(pool_bwd_kernel<T, D, false, false>, grid, dim3(256), s, a);
   if (e != hipSuccess || !a.du) return e;
-  const int n = a.kv_heads * D;
-  hipLaunchKernelGGL(du_reduce_kernel, dim3((n + kReduceOut - 1) / kReduceOut), dim3(256), 0, s,
-                     a.du_part, batch * a.blocks_per_seq, n, a.du);
+  const int n = a.kv_heads * D;  // a multiple of 64
+  hipLaunchKernelGGL(du_reduce_kernel, dim3((n + 63) / 64), dim3(1024), 0, s, a.du_part,
+                     batch * a.blocks_per_seq, n, a.du);
   return hipGetLastError();
 }
 
@@ -231,12 +259,23 @@ hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
 
 int pool_bwd_slots_per_block(int batch, int max_out, int kv_heads, int head_dim) {
   if (head_dim != 64 && head_dim != 128) return 0;
-  const int per_slot = kv_heads * (head_dim / 8);
-  if (batch < 1 || kv_heads < 1 || per_slot > 256 || 256 % per_slot) return 0;
-  const int lanes = 256 / per_slot;
-  const int groups = max_out > 0 ? (max_out + lanes - 1) / lanes : 1;  // slot groups per sequence
-  const int blocks = batch >= kTargetBlocks ? 1 : kTargetBlocks / batch;  // per sequence
-  return ((groups + blocks - 1) / blocks) * lanes;
+  if (batch < 1 || kv_heads < 1) return 0;
+  const int lanes = 256 / (head_dim / 8);                                 // slots per pass
+  const int64_t groups = max_out > 0 ? (max_out + lanes - 1) / lanes : 1;  // passes per (sequence, head)
+  const int64_t pairs = (int64_t)batch * kv_heads;
+  const int64_t blocks = pairs >= kTargetBlocks ? 1 : (kTargetBlocks + pairs - 1) / pairs;  // per pair
+  return (int)((groups + blocks - 1) / blocks) * lanes;
+}
+
+void pool_bwd_grid(int batch, int max_out, int hat_cap, int kv_heads, int head_dim, int* spb, int* blocks) {
+  const int lanes = 256 / (head_dim / 8);
+  const int spb_ws = pool_bwd_slots_per_block(batch, max_out, kv_heads, head_dim);
+  const int cap = max_out > 0 ? (max_out + spb_ws - 1) / spb_ws : 1;  // blocks the workspace holds
+  const int bound = max(min(max_out, hat_cap), 1);                     // slots that can hold work
+  const int groups = (bound + lanes - 1) / lanes;
+  const int use = min(cap, groups);
+  *spb = ((groups + use - 1) / use) * lanes;
+  *blocks = (bound + *spb - 1) / *spb;
 }
 
 hipError_t launch_pool_bwd(const PoolBwdArgs& a, int dtype, int head_dim, int batch,

@@ -413,14 +413,18 @@ def test_prefill_bwd_rejects_bad_cache_and_spans():
 def test_bwd_workspace_sizes():
     assert skv.speechkv_prefill_attn_bwd_workspace_bytes(8, 16, 1596) == 8 * 16 * 1596 * 4
     assert skv.speechkv_prefill_attn_bwd_workspace_bytes(0, 16, 1596) == 0
-    # per-block partial gate gradients, about 1024 blocks in all: at 8 heads x
-    # 128 a 256-thread pass covers 2 slots; 64 sequences of 782 slots take 16
-    # blocks of 25 passes (50 slots) each
-    assert skv.speechkv_pool_kv_bwd_workspace_bytes(64, 782, 8, 128) == 64 * 16 * 8 * 128 * 4
-    # 8 sequences of 1596: 128 blocks of 7 passes (14 slots) -> 114 blocks cover them
-    assert skv.speechkv_pool_kv_bwd_workspace_bytes(8, 1596, 8, 128) == 8 * 114 * 8 * 128 * 4
+    # per-block partial gate gradients (head_dim floats per block), about
+    # 4096 blocks in all: at head_dim 128 a 256-thread pass covers 16 slots of
+    # one head; 64 x 8 (sequence, head) pairs of 782 slots (49 passes) take 8
+    # blocks of 7 passes (112 slots) each -> 7 blocks cover them
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(64, 782, 8, 128) == 64 * 7 * 8 * 128 * 4
+    # 8 x 8 pairs of 1596 slots (100 passes): 64 blocks of 2 passes (32 slots) -> 50 blocks
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(8, 1596, 8, 128) == 8 * 50 * 8 * 128 * 4
     assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 0, 8, 128) == 2 * 1 * 8 * 128 * 4
-    assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 3, 128) == 0   # 3 x 16 does not divide 256
+    # any head count: 60 slots take 4 one-pass blocks per pair
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 3, 128) == 2 * 4 * 3 * 128 * 4
+    # at head_dim 64 a pass covers 32 slots
+    assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 2, 64) == 2 * 2 * 2 * 64 * 4
     assert skv.speechkv_pool_kv_bwd_workspace_bytes(2, 60, 8, 96) == 0
 
 
@@ -439,7 +443,7 @@ def pool_bwd(s=None, **kw):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(k=None), E_ARG), (dict(dk=None), E_ARG), (dict(dkr=None), E_ARG), (dict(dvr=None), E_ARG),
-    (dict(dtype=7), E_UNS), (dict(hd=96), E_UNS), (dict(heads=3), E_UNS), (dict(heads=64), E_UNS),
+    (dict(dtype=7), E_UNS), (dict(hd=96), E_UNS), (dict(heads=65536), E_UNS),
     (dict(heads=0), E_ARG), (dict(batch=0), E_ARG), (dict(raw_len=50), E_ARG), (dict(w=0), E_ARG),
     (dict(w=skv.MAX_WINDOW + 1), E_ARG), (dict(cap=0), E_ARG), (dict(layer=-1), E_ARG),
     (dict(sb=-8), E_ARG), (dict(ss=3), E_ARG), (dict(dkr=FAKE + (25 << 24) + 4), E_ARG),
