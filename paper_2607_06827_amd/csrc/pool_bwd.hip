@@ -35,8 +35,18 @@ constexpr int kTargetBlocks = 4096;  // ~16 blocks per CU; more are taken one pa
 template <int D>
 constexpr int lanes_per_head() { return D / 8; }
 
+// Four waves per SIMD (a bound of 128 registers: below it the kernel spills),
+// and the raw gradients written with non-temporal stores (no later access of
+// this kernel reads them; -5% at 1596 x 471, b=8).
+#ifndef SKV_POOLBWD_OCC
+#define SKV_POOLBWD_OCC 4
+#endif
+#ifndef SKV_POOLBWD_NT
+#define SKV_POOLBWD_NT 1
+#endif
+
 template <typename T, int D, bool kGate, bool kRuns>
-__global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
+__global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdArgs a) {
   constexpr int kLanes = lanes_per_head<D>();
   constexpr int kSlotLanes = 256 / kLanes;  // slots per pass
   const int heads = a.kv_heads;
@@ -90,8 +100,13 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
       Chunk<T> ok, ov;
       ok.from_float(gk);
       ov.from_float(gv);
-      ok.store(dkr + at(src));
-      ov.store(dvr + at(src));
+      if (SKV_POOLBWD_NT) {
+        ok.store_nt(dkr + at(src));
+        ov.store_nt(dvr + at(src));
+      } else {
+        ok.store(dkr + at(src));
+        ov.store(dvr + at(src));
+      }
       continue;
     }
 
@@ -159,8 +174,13 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolBwdArgs a) {
           ok.from_float(gkf);
           ov.from_float(gvf);
           const int64_t o = at(src + f0 + t);
-          ok.store(dkr + o);
-          ov.store(dvr + o);
+          if (SKV_POOLBWD_NT) {
+            ok.store_nt(dkr + o);
+            ov.store_nt(dvr + o);
+          } else {
+            ok.store(dkr + o);
+            ov.store(dvr + o);
+          }
         }
       }
     }
