@@ -274,12 +274,17 @@ struct QTile {
   static constexpr int kLoads = 32 / kRowsPerLoad;          // wave-wide loads per tile
   static constexpr int kElems = 32 * D;
   // XOR swizzle of the 16-byte chunks of row r.  With 16 chunks per row
-  // (bf16, D = 128) the tile is read both row-wise (A operands: 16 rows x one
-  // chunk per pass) and transposed (ds_read_b64_tr_b16: 4 rows x 4 chunks per
-  // 32 lanes); ((r & 3) << 2) | ((r >> 2) & 3) gives distinct chunk positions
-  // to both patterns (a plain r & 15 folds the transposed one onto 4 chunks).
+  // (bf16, D = 128: a row spans the 64 banks once) the tile is read both
+  // row-wise (16x16x32 A operands: 16 consecutive rows at one chunk per 16
+  // lanes) and transposed (ds_read_b64_tr_b16: 8 consecutive rows x 2
+  // neighbouring chunks per 32 lanes).  ((r & 7) << 1) | ((r >> 3) & 1) is a
+  // permutation of 16 consecutive rows (the row-wise reads hit 16 distinct
+  // chunk positions) whose bits 1-3 differ over 8 consecutive rows (the
+  // transposed reads hit 16 distinct positions).  (The 32x32 layout's
+  // ((r & 3) << 2) | ((r >> 2) & 3) gives rows r and r + 4 the same pair of
+  // positions in the transposed reads: a 2-way bank conflict on each.)
   static __device__ __forceinline__ int swz(int r) {
-    if constexpr (kChunks == 16) return ((r & 3) << 2) | ((r >> 2) & 3);
+    if constexpr (kChunks == 16) return ((r & 7) << 1) | ((r >> 3) & 1);
     return r & (kChunks >= 16 ? 15 : kChunks - 1);
   }
   // element e of row r
