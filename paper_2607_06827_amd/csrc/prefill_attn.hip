@@ -82,14 +82,12 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_kernel(Pref
 
   __shared__ __attribute__((aligned(16))) T s_buf[2 * (kTileK + kTileV)];
 
-  // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
-  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  // XCD-aware, heaviest-first item order
+  int pair, tile;
+  query_tile_item(blockIdx.x, gridDim.x, a.num_tiles, pair, tile);
   const int heads = a.pv.kv_heads;
-  const int tile = a.num_tiles - 1 - item % a.num_tiles;
-  const int g = (item / a.num_tiles) % heads;
-  const int b = item / a.num_tiles / heads;
+  const int g = pair % heads;
+  const int b = pair / heads;
 
   const int w = a.w_eff;
   const auto sp = span_view<kRuns>(a, b, w);
@@ -550,14 +548,12 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
   __shared__ __attribute__((aligned(256))) T s_v1[kTile];
   __shared__ __attribute__((aligned(256))) T s_v2[kTile];
 
-  // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
-  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  // XCD-aware, heaviest-first item order
+  int pair, tile;
+  query_tile_item(blockIdx.x, gridDim.x, a.num_tiles, pair, tile);
   const int heads = a.pv.kv_heads;
-  const int tile = a.num_tiles - 1 - item % a.num_tiles;
-  const int g = (item / a.num_tiles) % heads;
-  const int b = item / a.num_tiles / heads;
+  const int g = pair % heads;
+  const int b = pair / heads;
 
   const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int rows = min(sp.rows(), a.q_len);
@@ -730,14 +726,12 @@ __global__ __launch_bounds__(FusedShape<G>::kThreads, 2) void prefill_kernel_fus
   __shared__ __attribute__((aligned(256))) T s_v0[kTile];
   __shared__ __attribute__((aligned(256))) T s_v1[kTile];
 
-  // XCD-aware item order: XCD x (= block id mod 8) runs a contiguous item range
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
-  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  // XCD-aware, heaviest-first item order
+  int pair, tile;
+  query_tile_item(blockIdx.x, gridDim.x, a.num_tiles, pair, tile);
   const int heads = a.pv.kv_heads;
-  const int tile = a.num_tiles - 1 - item % a.num_tiles;
-  const int g = (item / a.num_tiles) % heads;
-  const int b = item / a.num_tiles / heads;
+  const int g = pair % heads;
+  const int b = pair / heads;
 
   const int w = a.w_eff;
   const auto sp = span_view<false>(a, b, w);

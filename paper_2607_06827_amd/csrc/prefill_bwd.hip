@@ -87,14 +87,12 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads) void prefill_bwd_dq_kern
 
   __shared__ __attribute__((aligned(16))) T s_buf[2 * 2 * kTile];  // [buffer][K, V]
 
-  // XCD-aware item order (as in the forward): XCD x runs a contiguous range
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
-  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  // XCD-aware, heaviest-first item order (as in the forward)
+  int pair, tile;
+  query_tile_item(blockIdx.x, gridDim.x, a.num_q_tiles, pair, tile);
   const int heads = a.pv.kv_heads;
-  const int tile = a.num_q_tiles - 1 - item % a.num_q_tiles;
-  const int g = (item / a.num_q_tiles) % heads;
-  const int b = item / a.num_q_tiles / heads;
+  const int g = pair % heads;
+  const int b = pair / heads;
 
   const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int rows = min(sp.rows(), a.q_len);
@@ -606,13 +604,12 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
   __shared__ __attribute__((aligned(256))) T s_v1[Q::kElems];
   __shared__ __attribute__((aligned(256))) T s_v2[Q::kElems];
 
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, per = nblk >> 3, rem = nblk & 7;
-  const int item = xcd * per + min(xcd, rem) + (bid >> 3);
+  // XCD-aware, heaviest-first item order (as in the forward)
+  int pair, tile;
+  query_tile_item(blockIdx.x, gridDim.x, a.num_q_tiles, pair, tile);
   const int heads = a.pv.kv_heads;
-  const int tile = a.num_q_tiles - 1 - item % a.num_q_tiles;  // heavy tiles (late rows) first
-  const int g = (item / a.num_q_tiles) % heads;
-  const int b = item / a.num_q_tiles / heads;
+  const int g = pair % heads;
+  const int b = pair / heads;
 
   const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int rows = min(sp.rows(), a.q_len);
