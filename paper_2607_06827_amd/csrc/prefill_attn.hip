@@ -510,8 +510,10 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&o)[D / 32], float m_run, 
     const int rr = r0 + lane / kChunks, cch = lane % kChunks;
     const int out_row = wrow0 + rr;
     if (out_row < rows) {
+      // (non-temporal: the output is written once and not read by this kernel)
       const uint4 v = *reinterpret_cast<const uint4*>(so + rr * D + ((cch ^ Swz::k(rr)) << 3));
-      *reinterpret_cast<uint4*>(out + (((int64_t)b * a.q_len + out_row) * hq + h) * D + cch * 8) = v;
+      __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w},
+                                  reinterpret_cast<u32x4_t*>(out + (((int64_t)b * a.q_len + out_row) * hq + h) * D + cch * 8));
     }
   }
 }
