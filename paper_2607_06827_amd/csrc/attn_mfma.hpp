@@ -123,14 +123,11 @@ __device__ __forceinline__ void lds_dma4(const void* p, uint32_t lds) {
 }
 
 // 16 bytes at p + kOff into r, untracked like lds_dma16: the caller waits
-// explicitly before r is read.  kNt: a non-temporal load (data read once).
-template <int kOff, bool kNt = false, typename F>
+// explicitly before r is read.
+template <int kOff, typename F>
 __device__ __forceinline__ void untracked_load16(F& r, const void* p) {
   static_assert(sizeof(F) == 16, "16-byte fragment");
-  if constexpr (kNt)
-    asm volatile("global_load_dwordx4 %0, %1, off offset:%2 nt" : "=v"(r) : "v"(p), "i"(kOff) : "memory");
-  else
-    asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "i"(kOff) : "memory");
+  asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "i"(kOff) : "memory");
 }
 
 // s_waitcnt immediate: at most n vector-memory operations outstanding, LDS
