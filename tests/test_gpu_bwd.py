@@ -47,6 +47,13 @@ CASES = {
     "page64": Case(P=[5, 2], T=[77, 64], N=[6, 1], page_size=64, w=5, D=128),
     "varlen": Case(P=[0, 17, 3, 40], T=[150, 7, 91, 0], N=[9, 33, 0, 1], w=3, D=128, Hq=8, Hkv=2),
     "long-rows": Case(P=[32], T=[750], N=[16], D=128, Hq=4, Hkv=2),
+    # 26 (sequence, KV head) pairs of 11 key blocks: 286 dK/dV blocks, more
+    # than 32 per XCD and pairs that straddle the XCD ranges, so the key
+    # blocks of some pairs run in descending order
+    "dkdv-grid-rounds": Case(P=[9, 3, 17, 0, 5, 11, 2, 8, 14, 6, 1, 12, 4],
+                             T=[660, 655, 640, 670, 650, 645, 665, 652, 648, 661, 657, 643, 668],
+                             N=[5, 12, 3, 8, 0, 9, 6, 2, 11, 4, 7, 10, 1], layer=2, l0=5, D=128,
+                             Hq=2, Hkv=2),
 }
 
 
