@@ -66,10 +66,27 @@ def capture(fn):
     return g
 
 
-def time_graph(g, reps):
+WARM_MS = 30.0  # untimed replays before a measurement: clocks ramp up over ~20 ms of load
+
+
+def time_graph(g, reps, warm=None):
+    """Average milliseconds per replay of graph g over `reps` replays, after
+    untimed replays: `warm` of them, or by default as many as take WARM_MS
+    (at least one; a short graph timed right after an idle gap otherwise
+    reads up to 15% slow while the clocks ramp up)."""
     import torch
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
+    if warm is None:
+        torch.cuda.synchronize()
+        start.record()
+        g.replay()
+        end.record()
+        torch.cuda.synchronize()
+        once = max(start.elapsed_time(end), 1e-3)
+        warm = min(int(WARM_MS / once), 1000)
+    for _ in range(warm):
+        g.replay()
     torch.cuda.synchronize()
     start.record()
     for _ in range(reps):
@@ -182,7 +199,7 @@ def measure(job, steps, warmup, label):
              for k, ix in classes.items() if ix}
     for _ in range(warmup):
         g_step.replay()
-    ms_step = time_graph(g_step, steps)
+    ms_step = time_graph(g_step, steps, warm=0)  # (the W warmup steps ran above)
     ms_dec = time_graph(g_dec, max(2, steps))
     ms_pre = time_graph(g_pre, max(2, steps))
     ms_pool = time_graph(g_pool, max(2, steps))
@@ -245,7 +262,7 @@ def measure_adaptive(base, steps, warmup, num_splits):
     g_dec = capture(lambda: [job.run_decode_step(s) for s in range(wl.decode_steps)])
     for _ in range(warmup):
         g_step.replay()
-    ms_step = time_graph(g_step, steps)
+    ms_step = time_graph(g_step, steps, warm=0)
     ms_dec = time_graph(g_dec, max(2, steps))
     dec_bytes, _ = decode_launch_stats(job)
     res = {"workload": wl.name, "w_layers": list(wl.w_layers[wl.l0:]), "ms_per_step": ms_step,
