@@ -65,15 +65,8 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
   auto at = [&](int s) { return (int64_t)min(s, a.raw_len - 1) * a.stride_s; };
 
   float uu[8];
-  if constexpr (kGate) {
-    const float4* gp = reinterpret_cast<const float4*>(a.gate + (int64_t)g * D + 8 * j);
-    const float4 u0 = gp[0], u1 = gp[1];
-    uu[0] = u0.x; uu[1] = u0.y; uu[2] = u0.z; uu[3] = u0.w;
-    uu[4] = u1.x; uu[5] = u1.y; uu[6] = u1.z; uu[7] = u1.w;
-  } else {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) uu[e] = 0.f;
-  }
+  for (int e = 0; e < 8; ++e) uu[e] = 0.f;
   float du[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) du[e] = 0.f;
@@ -110,6 +103,15 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
       continue;
     }
 
+    // the gate row, requested behind this slot's gradient rows (a load at the
+    // top of the kernel would make the first slot's loads wait for it)
+    if constexpr (kGate) {
+      asm volatile("" ::: "memory");
+      const float4* gp = reinterpret_cast<const float4*>(a.gate + (int64_t)g * D + 8 * j);
+      const float4 u0 = gp[0], u1 = gp[1];
+      uu[0] = u0.x; uu[1] = u0.y; uu[2] = u0.z; uu[3] = u0.w;
+      uu[4] = u1.x; uu[5] = u1.y; uu[6] = u1.z; uu[7] = u1.w;
+    }
     // frames f0..f0+3 (past the window: its last frame, weight 0), their log2
     // logits and dalpha
     Chunk<T> kc[4], vc[4];
@@ -208,53 +210,47 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
 }
 
 // du[i] = sum over the per-block partials (a block that saw no slot of its
-// head wrote zeros).  A 1024-thread block sums 64 consecutive outputs: each
-// thread four of them (one 16-byte load per partial) over every 64th partial,
-// eight loads in flight; the 64 lanes of an output quad are then added in a
-// fixed order, four within each wave (a butterfly) and the 16 waves in LDS.
-constexpr int kReduceLanes = 64;
-__global__ __launch_bounds__(1024) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
-  __shared__ float4 s_sum[16][16];
-  const int q = threadIdx.x % 16, r = threadIdx.x / 16;  // output quad, part lane
-  const int i = blockIdx.x * 64 + 4 * q;                 // first of this thread's outputs
-  float4 acc[8];
+// head wrote zeros).  One 256-thread block per four consecutive outputs:
+// thread t adds the 16-byte loads of partials t, t + 256, ... (four in
+// flight), then the block's 256 sums are added in a fixed order, a butterfly
+// within each wave and the four waves in LDS.
+constexpr int kReduceThreads = 256;
+__global__ __launch_bounds__(kReduceThreads) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
+  const int i = blockIdx.x * 4;
+  const int t = threadIdx.x;
+  float4 acc[4];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (i < n) {
-    for (int p0 = 0; p0 < parts; p0 += 8 * kReduceLanes) {
+  for (int u = 0; u < 4; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int p0 = 0; p0 < parts; p0 += 4 * kReduceThreads) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int p = p0 + u * kReduceLanes + r;
-        if (p < parts) {
-          const float4 v = *reinterpret_cast<const float4*>(part + (int64_t)p * n + i);
-          acc[u].x += v.x; acc[u].y += v.y; acc[u].z += v.z; acc[u].w += v.w;
-        }
+    for (int u = 0; u < 4; ++u) {
+      const int p = p0 + u * kReduceThreads + t;
+      if (p < parts) {
+        const float4 v = *reinterpret_cast<const float4*>(part + (int64_t)p * n + i);
+        acc[u].x += v.x; acc[u].y += v.y; acc[u].z += v.z; acc[u].w += v.w;
       }
     }
   }
+  float4 s4;
+  s4.x = (acc[0].x + acc[1].x) + (acc[2].x + acc[3].x);
+  s4.y = (acc[0].y + acc[1].y) + (acc[2].y + acc[3].y);
+  s4.z = (acc[0].z + acc[1].z) + (acc[2].z + acc[3].z);
+  s4.w = (acc[0].w + acc[1].w) + (acc[2].w + acc[3].w);
 #pragma unroll
-  for (int w = 4; w >= 1; w >>= 1)
-#pragma unroll
-    for (int u = 0; u < w; ++u) {
-      acc[u].x += acc[u + w].x; acc[u].y += acc[u + w].y; acc[u].z += acc[u + w].z; acc[u].w += acc[u + w].w;
-    }
-  // lanes q, q + 16, q + 32, q + 48 of a wave hold the same outputs
-#pragma unroll
-  for (int m = 16; m < 64; m <<= 1) {
-    acc[0].x += xor_shuffle(acc[0].x, m); acc[0].y += xor_shuffle(acc[0].y, m);
-    acc[0].z += xor_shuffle(acc[0].z, m); acc[0].w += xor_shuffle(acc[0].w, m);
+  for (int m = 1; m < 64; m <<= 1) {
+    s4.x += xor_shuffle(s4.x, m); s4.y += xor_shuffle(s4.y, m);
+    s4.z += xor_shuffle(s4.z, m); s4.w += xor_shuffle(s4.w, m);
   }
-  const int wave = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) < 16) s_sum[wave][q] = acc[0];
+  __shared__ float4 s_sum[kReduceThreads / 64];
+  if ((t & 63) == 0) s_sum[t >> 6] = s4;
   __syncthreads();
-  if (threadIdx.x < 16 && i < n) {
-    float4 sum = s_sum[0][q];
-#pragma unroll
-    for (int k = 1; k < 16; ++k) {
-      const float4 v = s_sum[k][q];
-      sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
-    }
-    *reinterpret_cast<float4*>(du + i) = sum;
+  if (t == 0) {
+    float4 r;
+    r.x = (s_sum[0].x + s_sum[1].x) + (s_sum[2].x + s_sum[3].x);
+    r.y = (s_sum[0].y + s_sum[1].y) + (s_sum[2].y + s_sum[3].y);
+    r.z = (s_sum[0].z + s_sum[1].z) + (s_sum[2].z + s_sum[3].z);
+    r.w = (s_sum[0].w + s_sum[1].w) + (s_sum[2].w + s_sum[3].w);
+    *reinterpret_cast<float4*>(du + i) = r;
   }
 }
 
@@ -270,7 +266,7 @@ hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
                : launch_struct(pool_bwd_kernel<T, D, false, false>, grid, dim3(256), s, a);
   if (e != hipSuccess || !a.du) return e;
   const int n = a.kv_heads * D;  // a multiple of 64
-  hipLaunchKernelGGL(du_reduce_kernel, dim3((n + 63) / 64), dim3(1024), 0, s, a.du_part,
+  hipLaunchKernelGGL(du_reduce_kernel, dim3(n / 4), dim3(kReduceThreads), 0, s, a.du_part,
                      batch * a.blocks_per_seq, n, a.du);
   return hipGetLastError();
 }
