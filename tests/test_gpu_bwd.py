@@ -120,6 +120,11 @@ def check_attention_bwd(case):
 POOL_CASES = {k: CASES[k] for k in ("bf16-d128", "bf16-d64-g1", "f32-d64", "identity-below-l0",
                                      "prefix-empty", "w8", "w12-three-groups", "zero-gate",
                                      "sharp-gate", "varlen", "long-rows")}
+# 64 sequences of 17 pooling-backward blocks each: 1088 gate partials, more
+# than the 1024 that one round of the gate-gradient sum's threads takes
+POOL_CASES["many-partials"] = Case(P=[(7 * i) % 23 for i in range(64)],
+                                   T=[1000 - (13 * i) % 37 for i in range(64)],
+                                   N=[(5 * i) % 11 for i in range(64)], w=2, D=64, Hq=2, Hkv=1)
 
 
 def pool_bwd(case, x, dkh, dvh, with_du=True):
