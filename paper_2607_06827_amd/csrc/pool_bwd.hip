@@ -213,10 +213,13 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
 // head wrote zeros).  One 256-thread block per four consecutive outputs:
 // thread t adds the 16-byte loads of partials t, t + 256, ... (four in
 // flight), then the block's 256 sums are added in a fixed order, a butterfly
-// within each wave and the four waves in LDS.
+// within each wave and the four waves in LDS.  Blocks go to the XCDs in turn
+// (block i to XCD i mod 8), so the output quads are dealt out in eight runs,
+// one per XCD: the eight quads of a 128-byte line of a partial are read by
+// one XCD's L2, not by eight.  The grid is n / 4 blocks, a multiple of 8.
 constexpr int kReduceThreads = 256;
 __global__ __launch_bounds__(kReduceThreads) void du_reduce_kernel(const float* part, int parts, int n, float* du) {
-  const int i = blockIdx.x * 4;
+  const int i = ((blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3)) * 4;
   const int t = threadIdx.x;
   float4 acc[4];
 #pragma unroll
@@ -265,7 +268,7 @@ hipError_t launch_t(const PoolBwdArgs& a, int batch, hipStream_t s) {
     e = a.gate ? launch_struct(pool_bwd_kernel<T, D, true, false>, grid, dim3(256), s, a)
                : launch_struct(pool_bwd_kernel<T, D, false, false>, grid, dim3(256), s, a);
   if (e != hipSuccess || !a.du) return e;
-  const int n = a.kv_heads * D;  // a multiple of 64
+  const int n = a.kv_heads * D;  // a multiple of 64, so n / 4 blocks are a multiple of 8
   hipLaunchKernelGGL(du_reduce_kernel, dim3(n / 4), dim3(kReduceThreads), 0, s, a.du_part,
                      batch * a.blocks_per_seq, n, a.du);
   return hipGetLastError();
