@@ -211,7 +211,9 @@ typedef struct speechkv_segments {
  * cache_len_out  device int32 [batch] receiving P + nW + N, or NULL.
  * Errors: INVALID_ARG, UNSUPPORTED, HIP; ALIAS when a page pool or
  *         cache_len_out overlaps the raw K/V byte range, the gate, the block
- *         table, the span lengths or another of the three.
+ *         table, the span lengths or another of the three.  UNSUPPORTED also
+ *         when max_total_len * num_kv_heads * head_dim / 512 exceeds
+ *         2^31 - 1 (the blocks one sequence's launch would need).
  */
 int speechkv_pool_kv(const void* k_raw, const void* v_raw, int64_t stride_b,
                      int64_t stride_s, int64_t stride_h, int32_t batch,

@@ -283,6 +283,8 @@ static int pool_kv_impl(const void* k_raw, const void* v_raw, int64_t stride_b, 
   const Region wr[] = {{cache->k_pages, pool_bytes}, {cache->v_pages, pool_bytes},
                        {cache_len_out, lens}};
   if (aliased(wr, 3, rd, 7)) return SPEECHKV_ERR_ALIAS;
+  if (skv::pool_grid_blocks(spans->max_total_len, cache->num_kv_heads, D) > INT32_MAX)
+    return SPEECHKV_ERR_UNSUPPORTED;
   skv::PoolArgs a;
   a.k_raw = k_raw;
   a.v_raw = v_raw;

@@ -88,6 +88,8 @@ struct PrefillArgs {
 
 // dtype: 0 = fp32, 1 = bf16.  Each launcher returns the launch status.
 hipError_t launch_pool(const PoolArgs& a, int dtype, int head_dim, int batch, hipStream_t s);
+// blocks per sequence of launch_pool's grid (at most INT32_MAX for a launch)
+int64_t pool_grid_blocks(int max_out, int kv_heads, int head_dim);
 bool pool_hidden_supported(int hidden);
 hipError_t launch_pool_hidden(const PoolHiddenArgs& a, int dtype, int hidden, int batch,
                               hipStream_t s);

@@ -74,6 +74,9 @@ struct OneRun {
     w = w_;
     nW = (T + w - 1) / w;
   }
+  // from the three lengths themselves
+  __device__ __forceinline__ OneRun(int p, int t, int n, int w_)
+      : P(max(p, 0)), T(max(t, 0)), N(max(n, 0)), w(w_), nW((T + w_ - 1) / w_) {}
   __device__ __forceinline__ int rows() const { return P + T + N; }
   __device__ __forceinline__ int clen() const { return P + nW + N; }
   __device__ __forceinline__ SlotSource slot(int c) const { return SlotSource(c, P, T, nW, w); }

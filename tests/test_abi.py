@@ -178,6 +178,17 @@ def test_pool_rejects(kw, code):
     assert pool(**kw) == code
 
 
+def test_pool_rejects_an_oversized_grid():
+    """One sequence's pooling launch has max_total_len * Hkv * D / 512 blocks;
+    past 2^31 - 1 the call is UNSUPPORTED before any launch."""
+    H, D = 65535, 128
+    rows = (1 << 33) // H + 1  # rows * H * D / 512 > 2^31 - 1
+    base = 1 << 44  # far-apart fake ranges: nothing overlaps
+    c = cache(num_kv_heads=H, head_dim=D, k_pages=base, v_pages=2 * base, block_table=3 * base)
+    s = spans(max_speech_len=rows, max_total_len=rows)
+    assert pool(c=c, s=s, k=4 * base, v=6 * base, raw_len=rows, sb=rows * H * D, ss=H * D, sh=D) == E_UNS
+
+
 @pytest.mark.parametrize("kw,ckw", [
     (dict(clen=FAKE + 256), {}), (dict(clen=FAKE + (3 << 24)), {}), (dict(clen=RAW + 64), {}),
     (dict(gate=FAKE + (1 << 24) + 1024), {}), ({}, dict(block_table=FAKE + 2048)),
