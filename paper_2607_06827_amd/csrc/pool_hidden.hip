@@ -65,11 +65,8 @@ __global__ __launch_bounds__(256) void pool_hidden_kernel(PoolHiddenArgs a) {
   const int cb = blockIdx.x * kRows;
   const int c = cb + rib;      // output row
 
-  const int P = max(a.prefix_len[b], 0);
-  const int T_ = max(a.speech_len[b], 0);
-  const int N = max(a.suffix_len[b], 0);
-  const int w = a.w;
-  const int nW = (T_ + w - 1) / w;
+  const OneRun run = one_run_now(a.prefix_len, a.speech_len, a.suffix_len, b, a.w);
+  const int P = run.P, T_ = run.T, N = run.N, w = run.w, nW = run.nW;
   const int L = P + nW + N;
   if (blockIdx.x == 0 && tid == 0 && a.out_len) a.out_len[b] = L;
   const int lim = min(L, a.out_cap);

@@ -7,7 +7,7 @@
 // contiguous run when the raw tensor is [B][S][Hkv][D].  A block is one
 // wave: the blocks are short-lived (a few loads, a few stores), and one-wave
 // blocks measured 1.2% faster than four-wave blocks on the 60 s stack (1.9%
-// with the sequence lengths requested together, below).
+// with the sequence lengths requested together: span_view_now).
 //   slot c < P                 copy raw row c                       (bitwise)
 //   slot P + i, i < nW         softmax-of-gate-logits weighted sum over the
 //                              window [P + i*w, min(P + (i+1)*w, P + T))
@@ -33,30 +33,6 @@ namespace {
 
 constexpr int kPoolThreads = 64;
 
-// The three lengths of sequence b (one run), requested together: one scalar
-// round trip before the slot's rows are known, where the compiler had waited
-// for each load in turn.
-__device__ __forceinline__ OneRun one_run_now(const PoolArgs& a, int b) {
-  int p, t, n;
-  asm volatile(
-      "s_load_dword %0, %3, 0x0\n\t"
-      "s_load_dword %1, %4, 0x0\n\t"
-      "s_load_dword %2, %5, 0x0\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&s"(p), "=&s"(t), "=&s"(n)
-      : "s"(a.prefix_len + b), "s"(a.speech_len + b), "s"(a.suffix_len + b)
-      : "memory");
-  return OneRun(p, t, n, a.w_eff);
-}
-
-template <bool kRuns>
-__device__ __forceinline__ auto pool_span_view(const PoolArgs& a, int b) {
-  if constexpr (kRuns)
-    return Runs(a.segs, b, a.w_eff);
-  else
-    return one_run_now(a, b);
-}
-
 template <typename T, int D, bool kGate, bool kRuns>
 __global__ __launch_bounds__(kPoolThreads) void pool_kv_kernel(PoolArgs a) {
   constexpr int kLanes = D / 8;                   // lanes per unit
@@ -70,7 +46,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kv_kernel(PoolArgs a) {
   const int g = (int)(unit % heads);
   const int64_t c64 = unit / heads;
 
-  const auto sp = pool_span_view<kRuns>(a, b);
+  const auto sp = span_view_now<kRuns>(a, b, a.w_eff);
   const int len = sp.clen();
   if (blockIdx.x == 0 && tid == 0 && a.cache_len_out) a.cache_len_out[b] = len;
   if (c64 >= len || c64 >= a.max_out) return;

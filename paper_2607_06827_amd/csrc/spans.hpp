@@ -198,4 +198,31 @@ __device__ __forceinline__ auto span_view(const A& a, int b, int w) {
     return OneRun(a.prefix_len, a.speech_len, a.suffix_len, b, w);
 }
 
+// One run's three lengths requested in one batch of scalar loads: one round
+// trip before anything that depends on them, where the compiler had waited
+// for each load in turn.  For kernels of short-lived blocks, whose prologue
+// is a good part of their time.
+__device__ __forceinline__ OneRun one_run_now(const int32_t* prefix, const int32_t* speech,
+                                              const int32_t* suffix, int b, int w) {
+  int p, t, n;
+  asm volatile(
+      "s_load_dword %0, %3, 0x0\n\t"
+      "s_load_dword %1, %4, 0x0\n\t"
+      "s_load_dword %2, %5, 0x0\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&s"(p), "=&s"(t), "=&s"(n)
+      : "s"(prefix + b), "s"(speech + b), "s"(suffix + b)
+      : "memory");
+  return OneRun(p, t, n, w);
+}
+
+// span_view with one_run_now for a single run
+template <bool kRuns, typename A>
+__device__ __forceinline__ auto span_view_now(const A& a, int b, int w) {
+  if constexpr (kRuns)
+    return Runs(a.segs, b, w);
+  else
+    return one_run_now(a.prefix_len, a.speech_len, a.suffix_len, b, w);
+}
+
 }  // namespace skv
