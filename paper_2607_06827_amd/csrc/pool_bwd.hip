@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
   const int sl = tid / kLanes, j = tid % kLanes;
   const int g = blockIdx.y, b = blockIdx.z;
 
-  const auto sp = span_view_now<kRuns>(a, b, a.w_eff);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int len = min(min(sp.clen(), a.max_out), a.hat_cap);
 
   const int64_t base = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h + 8 * j;

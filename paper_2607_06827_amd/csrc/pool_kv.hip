@@ -7,7 +7,7 @@
 // contiguous run when the raw tensor is [B][S][Hkv][D].  A block is one
 // wave: the blocks are short-lived (a few loads, a few stores), and one-wave
 // blocks measured 1.2% faster than four-wave blocks on the 60 s stack (1.9%
-// with the sequence lengths requested together: span_view_now).
+// with the sequence lengths requested together, one_run_now).
 //   slot c < P                 copy raw row c                       (bitwise)
 //   slot P + i, i < nW         softmax-of-gate-logits weighted sum over the
 //                              window [P + i*w, min(P + (i+1)*w, P + T))
@@ -46,7 +46,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kv_kernel(PoolArgs a) {
   const int g = (int)(unit % heads);
   const int64_t c64 = unit / heads;
 
-  const auto sp = span_view_now<kRuns>(a, b, a.w_eff);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int len = sp.clen();
   if (blockIdx.x == 0 && tid == 0 && a.cache_len_out) a.cache_len_out[b] = len;
   if (c64 >= len || c64 >= a.max_out) return;

@@ -66,15 +66,6 @@ struct SegmentTable {
 
 struct OneRun {
   int P, T, N, w, nW;
-  __device__ __forceinline__ OneRun(const int32_t* prefix, const int32_t* speech,
-                                    const int32_t* suffix, int b, int w_) {
-    P = max(prefix[b], 0);
-    T = max(speech[b], 0);
-    N = max(suffix[b], 0);
-    w = w_;
-    nW = (T + w - 1) / w;
-  }
-  // from the three lengths themselves
   __device__ __forceinline__ OneRun(int p, int t, int n, int w_)
       : P(max(p, 0)), T(max(t, 0)), N(max(n, 0)), w(w_), nW((T + w_ - 1) / w_) {}
   __device__ __forceinline__ int rows() const { return P + T + N; }
@@ -188,22 +179,15 @@ struct Runs {
   }
 };
 
-// The span view of sequence b: the segment table when kRuns, else the
-// one-run spans of the argument struct.
-template <bool kRuns, typename A>
-__device__ __forceinline__ auto span_view(const A& a, int b, int w) {
-  if constexpr (kRuns)
-    return Runs(a.segs, b, w);
-  else
-    return OneRun(a.prefix_len, a.speech_len, a.suffix_len, b, w);
-}
-
-// One run's three lengths requested in one batch of scalar loads: one round
+// One run's three lengths, requested in one batch of scalar loads: one round
 // trip before anything that depends on them, where the compiler had waited
-// for each load in turn.  For kernels of short-lived blocks, whose prologue
-// is a good part of their time.
+// for each load in turn (blocks of a few steps spend a good part of their
+// time in that prologue).  b must be uniform over the wave, as it is in every
+// kernel here (it comes from the block index; the compiler cannot always tell,
+// hence the readfirstlane).
 __device__ __forceinline__ OneRun one_run_now(const int32_t* prefix, const int32_t* speech,
                                               const int32_t* suffix, int b, int w) {
+  b = __builtin_amdgcn_readfirstlane(b);
   int p, t, n;
   asm volatile(
       "s_load_dword %0, %3, 0x0\n\t"
@@ -216,9 +200,10 @@ __device__ __forceinline__ OneRun one_run_now(const int32_t* prefix, const int32
   return OneRun(p, t, n, w);
 }
 
-// span_view with one_run_now for a single run
+// The span view of sequence b: the segment table when kRuns, else the
+// one-run spans of the argument struct.
 template <bool kRuns, typename A>
-__device__ __forceinline__ auto span_view_now(const A& a, int b, int w) {
+__device__ __forceinline__ auto span_view(const A& a, int b, int w) {
   if constexpr (kRuns)
     return Runs(a.segs, b, w);
   else
