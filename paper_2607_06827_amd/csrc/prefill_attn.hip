@@ -523,8 +523,9 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&o)[D / 32], float m_run, 
 // entries of tile t+3 (scalar loads) and the K/V rows of tile t+2 (direct
 // loads into the buffer tile t-1 used), computes tile t, then waits until
 // tile t+1 has landed in every wave's part and joins the block, so every
-// tile's loads have two steps to arrive.  The queries are loaded once, behind
-// tile 0.
+// tile's loads have two steps to arrive.  The queries are loaded once, first
+// of all (their rows do not depend on the span lengths), so they travel
+// during the span and block-table round trips.
 template <int D, int G, bool kRuns>
 __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_lds(PrefillArgs a) {
   typedef bf16_bits T;
@@ -557,24 +558,37 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
   const int g = pair % heads;
   const int b = pair / heads;
 
-  const auto sp = span_view<kRuns>(a, b, a.w_eff);
-  const int rows = min(sp.rows(), a.q_len);
-  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
-  if (p0 >= rows) return;
-  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
-  const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
-
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = g * G + wave % G;
   const int col = lane & 31, hg = lane >> 5;
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
   const int p = wrow0 + col;
+  const int hq = a.num_q_heads;
+  // the queries first: their rows do not depend on the span lengths, so they
+  // are in flight during the span and block-table round trips (a row past
+  // the tensor reads its last row: in range, never stored)
+  Frag qf[kQChunks];
+  {
+    const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + min(p, a.q_len - 1)) * hq + h) * D + hg * 8;
+    static_for<kQChunks>([&](auto kc) { untracked_load16<decltype(kc)::value * 16 * 2>(qf[decltype(kc)::value], qrow); });
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
+  if (p0 >= rows) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the query loads land before the wave ends
+    return;
+  }
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
+  const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
+
   const bool qvalid = p < rows;
   const int nvis = qvalid ? min(sp.visible(p, a.mask_mode), clen) : 0;
   // keys every valid row of the wave sees (n_vis grows with the row)
   const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
-  const int hq = a.num_q_heads;
   const int slot_mask = (1 << a.pv.page_shift) - 1;
   const int shift = a.pv.page_shift;
   const int64_t num_pages = a.pv.num_pages;
@@ -630,17 +644,11 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
     }
   };
 
-  // prologue: tables of tiles 0..2, tile 0, this lane's query row (rows past
-  // the end read row 0 of the sequence: finite, never stored), tile 1; then
-  // wait for tile 0 and the queries (tile 1 may stay in flight)
+  // prologue (the queries are already in flight): tables of tiles 0..2,
+  // tile 0, tile 1; then wait for the queries and tile 0 (tile 1 may stay in
+  // flight)
   int pg[3] = {table_load(0), table_load(1), table_load(2)};  // entries by tile mod 3
   tile_load(0, pg[0], s_k0, s_v0);  // (also for a block without tiles: in range, never read)
-  __builtin_amdgcn_sched_barrier(0);
-  Frag qf[kQChunks];
-  {
-    const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + (qvalid ? p : 0)) * hq + h) * D + hg * 8;
-    static_for<kQChunks>([&](auto kc) { untracked_load16<decltype(kc)::value * 16 * 2>(qf[decltype(kc)::value], qrow); });
-  }
   __builtin_amdgcn_sched_barrier(0);
   if (ntiles > 1 && loads) {
     tile_load(1, pg[1], s_k1, s_v1);

@@ -610,38 +610,25 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
   const int heads = a.pv.kv_heads;
   const int g = pair % heads;
   const int b = pair / heads;
-
-  const auto sp = span_view<kRuns>(a, b, a.w_eff);
-  const int rows = min(sp.rows(), a.q_len);
-  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   const int p0 = tile * kRows;
-  if (p0 >= rows) return;
-  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
-  const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int gq = lane >> 4, j = lane & 15;
   const int h = g * G + wave % G;
   const int wrow0 = p0 + (wave / G) * 16;  // first row of this wave
   const int q = wrow0 + j;                 // this lane's row (column of the C layout)
-  const bool qvalid = q < rows;
-  const int nvis = qvalid ? min(sp.visible(q, a.mask_mode), clen) : 0;
-  const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
   const int hq = a.num_q_heads;
-  const int shift = a.pv.page_shift, slot_mask = (1 << shift) - 1;
-  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
-  const int ntiles = (kmax + kKeys - 1) / kKeys;
-  const bool loads = Q::kLoads >= kWaves || wave < Q::kLoads;
-  auto load_row0 = [&](int i) { return (Q::kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * Q::kRowsPerLoad; };
-  const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
 
   // this lane's row of Q, dO and O (elements 32c + 8gq .. +7, the B operand
-  // layout of S^T = K Q^T) and its LSE; rows past the end read row 0 of the
-  // sequence (finite, never stored)
+  // layout of S^T = K Q^T) and its LSE, requested first: the rows do not
+  // depend on the span lengths, so they are in flight during the span and
+  // block-table round trips (a row past the tensor reads its last row: in
+  // range, never stored)
   Frag qf[kDC], gf[kDC], of[kDC];
   float lse = 0.f;
   {
-    const int64_t row = ((int64_t)b * a.q_len + (qvalid ? q : 0)) * hq + h;
+    const int qr = min(q, a.q_len - 1);
+    const int64_t row = ((int64_t)b * a.q_len + qr) * hq + h;
     const T* qp = static_cast<const T*>(a.q) + row * D + 8 * gq;
     const T* gp = static_cast<const T*>(a.dout) + row * D + 8 * gq;
     const T* op = static_cast<const T*>(a.out) + row * D + 8 * gq;
@@ -651,9 +638,30 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
       untracked_load16<kC * 64>(gf[kC], gp);
       untracked_load16<kC * 64>(of[kC], op);
     });
-    const float* lp = a.lse + ((int64_t)b * hq + h) * a.q_len + (qvalid ? q : 0);
+    const float* lp = a.lse + ((int64_t)b * hq + h) * a.q_len + qr;
     asm volatile("global_load_dword %0, %1, off" : "=v"(lse) : "v"(lp) : "memory");
   }
+  __builtin_amdgcn_sched_barrier(0);
+
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int rows = min(sp.rows(), a.q_len);
+  const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
+  if (p0 >= rows) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the row loads land before the wave ends
+    return;
+  }
+  const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
+  const int kclamp = max(kmax - 1, 0);  // last visible key: the row loaded for keys past kmax
+
+  const bool qvalid = q < rows;
+  const int nvis = qvalid ? min(sp.visible(q, a.mask_mode), clen) : 0;
+  const int nvis_lo = wrow0 < rows ? min(sp.visible(wrow0, a.mask_mode), clen) : 0;
+  const int shift = a.pv.page_shift, slot_mask = (1 << shift) - 1;
+  const int32_t* table_row = a.table + (int64_t)b * a.pv.max_pages;
+  const int ntiles = (kmax + kKeys - 1) / kKeys;
+  const bool loads = Q::kLoads >= kWaves || wave < Q::kLoads;
+  auto load_row0 = [&](int i) { return (Q::kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * Q::kRowsPerLoad; };
+  const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
 
   // block-table entries: one per wave and tile (the forward's scheme)
   constexpr int kWaveRows = kLoadsPerWave * Q::kRowsPerLoad;
