@@ -565,21 +565,28 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
   const int wrow0 = p0 + (wave / G) * 32;  // first row of this wave
   const int p = wrow0 + col;
   const int hq = a.num_q_heads;
-  // the queries first: their rows do not depend on the span lengths, so they
-  // are in flight during the span and block-table round trips (a row past
-  // the tensor reads its last row: in range, never stored)
+  // the queries: their rows do not depend on the span lengths, so with one
+  // run they go first and are in flight during the span and block-table
+  // round trips (a row past the tensor reads its last row: in range, never
+  // stored).  A segment table is scanned with loads the compiler tracks, and
+  // its waits would take these untracked loads along: there they follow the
+  // scans, behind tile 0.
   Frag qf[kQChunks];
-  {
-    const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + min(p, a.q_len - 1)) * hq + h) * D + hg * 8;
+  auto load_queries = [&](int row) __attribute__((always_inline)) {
+    const T* qrow = static_cast<const T*>(a.q) + (((int64_t)b * a.q_len + row) * hq + h) * D + hg * 8;
     static_for<kQChunks>([&](auto kc) { untracked_load16<decltype(kc)::value * 16 * 2>(qf[decltype(kc)::value], qrow); });
-  }
-  __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if constexpr (!kRuns) load_queries(min(p, a.q_len - 1));
 
   const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int rows = min(sp.rows(), a.q_len);
   const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   if (p0 >= rows) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the query loads land before the wave ends
+    // the query loads land before the wave ends (with one run they were
+    // issued above; an asm statement ahead of a segment scan would turn its
+    // scalar loads into vector loads)
+    if constexpr (!kRuns) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     return;
   }
   const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
@@ -650,6 +657,7 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
   int pg[3] = {table_load(0), table_load(1), table_load(2)};  // entries by tile mod 3
   tile_load(0, pg[0], s_k0, s_v0);  // (also for a block without tiles: in range, never read)
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kRuns) load_queries(qvalid ? p : 0);  // behind tile 0, after every segment scan
   if (ntiles > 1 && loads) {
     tile_load(1, pg[1], s_k1, s_v1);
     bare_barrier<kVm>();
@@ -657,6 +665,15 @@ __global__ __launch_bounds__(PrefillShape<G>::kThreads, 3) void prefill_kernel_l
     // (a wave that loads no tile rows has only its query loads in flight:
     // it waits for all of them)
     bare_barrier<0>();
+  }
+  // A row past the sequence read before the span lengths were known may hold
+  // anything: zero it (its queries have landed), so that its scores are 0 and
+  // never force the online softmax to rescale.
+  if constexpr (!kRuns) {
+    if (!qvalid) {
+#pragma unroll
+      for (int kc = 0; kc < kQChunks; ++kc) qf[kc] = Frag{};
+    }
   }
 
   // step kt; kPar = kt mod 3 selects buffers and table registers at compile

@@ -620,13 +620,14 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
   const int hq = a.num_q_heads;
 
   // this lane's row of Q, dO and O (elements 32c + 8gq .. +7, the B operand
-  // layout of S^T = K Q^T) and its LSE, requested first: the rows do not
-  // depend on the span lengths, so they are in flight during the span and
-  // block-table round trips (a row past the tensor reads its last row: in
-  // range, never stored)
+  // layout of S^T = K Q^T) and its LSE: the rows do not depend on the span
+  // lengths, so with one run they are requested first and are in flight
+  // during the span and block-table round trips (a row past the tensor reads
+  // its last row: in range, never stored); a segment table's scan comes
+  // first (its tracked loads' waits would take these along)
   Frag qf[kDC], gf[kDC], of[kDC];
   float lse = 0.f;
-  {
+  auto load_rows = [&]() __attribute__((always_inline)) {
     const int qr = min(q, a.q_len - 1);
     const int64_t row = ((int64_t)b * a.q_len + qr) * hq + h;
     const T* qp = static_cast<const T*>(a.q) + row * D + 8 * gq;
@@ -640,14 +641,18 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
     });
     const float* lp = a.lse + ((int64_t)b * hq + h) * a.q_len + qr;
     asm volatile("global_load_dword %0, %1, off" : "=v"(lse) : "v"(lp) : "memory");
-  }
-  __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if constexpr (!kRuns) load_rows();
 
   const auto sp = span_view<kRuns>(a, b, a.w_eff);
   const int rows = min(sp.rows(), a.q_len);
   const int clen = min(sp.clen(), a.pv.max_pages << a.pv.page_shift);
   if (p0 >= rows) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the row loads land before the wave ends
+    // the row loads land before the wave ends (with one run they were
+    // issued above; an asm statement ahead of a segment scan would turn its
+    // scalar loads into vector loads)
+    if constexpr (!kRuns) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     return;
   }
   const int kmax = min(sp.visible(min(p0 + kRows, rows) - 1, a.mask_mode), clen);
@@ -662,6 +667,7 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
   const bool loads = Q::kLoads >= kWaves || wave < Q::kLoads;
   auto load_row0 = [&](int i) { return (Q::kLoads >= kWaves ? wave * kLoadsPerWave + i : wave) * Q::kRowsPerLoad; };
   const int lrow = lane / Q::kChunks, lpos = lane % Q::kChunks;
+  if constexpr (kRuns) load_rows();  // after every segment scan
 
   // block-table entries: one per wave and tile (the forward's scheme)
   constexpr int kWaveRows = kLoadsPerWave * Q::kRowsPerLoad;
