@@ -54,9 +54,6 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
   const int sl = tid / kLanes, j = tid % kLanes;
   const int g = blockIdx.y, b = blockIdx.z;
 
-  const auto sp = span_view<kRuns>(a, b, a.w_eff);
-  const int len = min(min(sp.clen(), a.max_out), a.hat_cap);
-
   const int64_t base = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h + 8 * j;
   const T* kr = static_cast<const T*>(a.k_raw) + base;
   const T* vr = static_cast<const T*>(a.v_raw) + base;
@@ -71,21 +68,18 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
 #pragma unroll
   for (int e = 0; e < 8; ++e) du[e] = 0.f;
 
-  const int iters = a.slots_per_block / kSlotLanes;
-  for (int k = 0; k < iters; ++k) {
-    const int c = (blockIdx.x * iters + k) * kSlotLanes + sl;
-    if (c >= len) continue;
+  // one pass: slot c of this block, its gradient rows k0, k1 (dK^) and v0,
+  // v1 (dV^) already loaded
+  auto pass = [&](int c, const auto& sp, int len, float4 k0, float4 k1, float4 v0, float4 v1)
+                  __attribute__((always_inline)) {
+    if (c >= len) return;
     const SlotSource slot = sp.slot(c);
     const int src = slot.first, n = slot.frames;
-    if (src + n > a.raw_len) continue;  // a broken caller obligation: rows left alone
+    if (src + n > a.raw_len) return;  // a broken caller obligation: rows left alone
 
     // gradient of pooled row c (fp32)
     float gk[8], gv[8];
-    const float* hk = a.dk_hat + (((int64_t)b * a.hat_cap + c) * heads + g) * D + 8 * j;
-    const float* hv = a.dv_hat + (((int64_t)b * a.hat_cap + c) * heads + g) * D + 8 * j;
     {
-      const float4 k0 = reinterpret_cast<const float4*>(hk)[0], k1 = reinterpret_cast<const float4*>(hk)[1];
-      const float4 v0 = reinterpret_cast<const float4*>(hv)[0], v1 = reinterpret_cast<const float4*>(hv)[1];
       gk[0] = k0.x; gk[1] = k0.y; gk[2] = k0.z; gk[3] = k0.w; gk[4] = k1.x; gk[5] = k1.y; gk[6] = k1.z; gk[7] = k1.w;
       gv[0] = v0.x; gv[1] = v0.y; gv[2] = v0.z; gv[3] = v0.w; gv[4] = v1.x; gv[5] = v1.y; gv[6] = v1.z; gv[7] = v1.w;
     }
@@ -100,7 +94,7 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
         ok.store(dkr + at(src));
         ov.store(dvr + at(src));
       }
-      continue;
+      return;
     }
 
     // the gate row, requested behind this slot's gradient rows (a load at the
@@ -186,6 +180,29 @@ __global__ __launch_bounds__(256, SKV_POOLBWD_OCC) void pool_bwd_kernel(PoolBwdA
         }
       }
     }
+  };
+  // the gradient rows of slot c (clamped to the dK^ capacity: a slot past the
+  // sequence is never used)
+  auto hat_rows = [&](int c, float4& k0, float4& k1, float4& v0, float4& v1) __attribute__((always_inline)) {
+    const int64_t row = (((int64_t)b * a.hat_cap + min(c, a.hat_cap - 1)) * heads + g) * D + 8 * j;
+    const float4* hk = reinterpret_cast<const float4*>(a.dk_hat + row);
+    const float4* hv = reinterpret_cast<const float4*>(a.dv_hat + row);
+    k0 = hk[0]; k1 = hk[1];
+    v0 = hv[0]; v1 = hv[1];
+  };
+  const int iters = a.slots_per_block / kSlotLanes;
+  auto slot_of = [&](int k) { return (blockIdx.x * iters + k) * kSlotLanes + sl; };
+  // the first pass's gradient rows do not depend on the span lengths (the slot
+  // comes from the block index): requested before them
+  float4 f0k, f1k, f0v, f1v;
+  hat_rows(slot_of(0), f0k, f1k, f0v, f1v);
+  const auto sp = span_view<kRuns>(a, b, a.w_eff);
+  const int len = min(min(sp.clen(), a.max_out), a.hat_cap);
+  if (iters > 0) pass(slot_of(0), sp, len, f0k, f1k, f0v, f1v);
+  for (int k = 1; k < iters; ++k) {
+    float4 k0, k1, v0, v1;
+    hat_rows(slot_of(k), k0, k1, v0, v1);
+    pass(slot_of(k), sp, len, k0, k1, v0, v1);
   }
 
   if (!a.du_part) return;
