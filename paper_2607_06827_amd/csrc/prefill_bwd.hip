@@ -868,7 +868,10 @@ __global__ __launch_bounds__(DqShape16<G>::kThreads, 3) void prefill_bwd_dq16_ke
     const int r = r0 + lrow, row = wrow0 + r;
     if (row < rows) {
       const uint4 v = *reinterpret_cast<const uint4*>(so + r * D + ((lpos ^ Q::swz(r)) << 3));
-      *reinterpret_cast<uint4*>(dqp + (((int64_t)b * a.q_len + row) * hq + h) * D + lpos * 8) = v;
+      // non-temporal: nothing later in the backward reads dQ (-1%)
+      typedef unsigned int nt_u32x4 __attribute__((ext_vector_type(4)));
+      __builtin_nontemporal_store(nt_u32x4{v.x, v.y, v.z, v.w},
+                                  reinterpret_cast<nt_u32x4*>(dqp + (((int64_t)b * a.q_len + row) * hq + h) * D + lpos * 8));
     }
   }
 }
